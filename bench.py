@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Throughput of the MI355X fp32 implicit-GEMM convolution on one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload vgg16_n64]
+
+A step is one forward pass of every conv layer of the workload (default: the
+13 VGG-16 conv layers at batch 64, 224x224 input), each layer a call of the
+C ABI's conv2d_fwd_f32 on device-resident seeded synthetic inputs.  Prints
+one JSON line: aggregate fp32 TFLOPS (2*N*K*C*R*S*Ho*Wo per layer), the
+per-layer TFLOPS and % of the 157.3 TFLOPS fp32-MFMA peak, the roofline
+figures of the dominant kernel, and the fp64 CPU oracle timed on a bounded
+sample of the same layers.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = 157.3          # MI355X dense fp32 MFMA
+HBM_GBS = 8000.0             # MI355X HBM3E
+METRIC = "fp32 conv TFLOPS and % of MI355X fp32 MFMA peak per layer, 1 GPU"
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("conv_igemm.hip", "plan.cpp", "abi.cpp", "mg3m_internal.h"):
+        with open(os.path.join(ROOT, "paper_2307_04941_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def layer_flops(L, Ho, Wo) -> float:
+    return 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo
+
+
+def layer_alg_bytes(L, Ho, Wo) -> float:
+    # each tensor read or written once; input rows/cols never touched by a tap
+    # (1x1 stride-2 layers) are not counted
+    if L.R == 1 and L.S == 1 and L.pad == 0:
+        ht, wt = Ho, Wo
+    else:
+        ht, wt = L.H, L.W
+    return 4.0 * (L.N * L.C * ht * wt + L.K * L.C * L.R * L.S + L.N * L.K * Ho * Wo)
+
+
+def cpu_baseline(layers, tensors, budget_s: float):
+    """Time the fp64 oracle on a seeded sample of outputs of every layer,
+    growing the sample until about `budget_s` seconds of CPU work."""
+    import numpy as np
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(cores))
+    rng = np.random.Generator(np.random.PCG64(7))
+    pts = 256
+    total_flops = 0.0
+    total_t = 0.0
+    n_pts = 0
+    while True:
+        t0 = time.perf_counter()
+        for (L, Ho, Wo), (x, w) in zip(layers, tensors):
+            n_out = L.N * L.K * Ho * Wo
+            idx = rng.integers(0, n_out, pts)
+            oracle.conv2d_points(x, w, idx, L.stride, L.pad, "HWCN")
+            total_flops += 2.0 * L.C * L.R * L.S * pts
+            n_pts += pts
+        total_t += time.perf_counter() - t0
+        if total_t >= budget_s or pts >= 1 << 22:
+            break
+        pts *= 2
+    return {
+        "value": total_flops / total_t / 1e12,
+        "unit": "TFLOPS",
+        "cores": int(os.environ.get("OMP_NUM_THREADS", cores)),
+        "kind": "oracle",
+        "sample": f"{n_pts} output elements drawn uniformly from every layer of the workload "
+                  f"(same seeded inputs), {total_t:.1f} s of fp64 seven-loop direct convolution; "
+                  f"throughput counts 2*C*R*S flop per output",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="vgg16_n64")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU work budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--plan", default=None, help="plan override for every layer (diagnostics)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md, 'How the path would shard')", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2307_04941_amd import mg3m
+
+    mg3m.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layers_def = workloads.workload(args.workload)
+
+    # ---- inputs: seeded, generated on the host, resident in HBM before timing
+    layers, tensors, dev_bufs = [], [], []
+    for i, L in enumerate(layers_def):
+        sx, sw = workloads.seeds(args.workload, i)
+        x, w = workloads.make_tensors(L, sx, sw, "HWCN")
+        Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
+        xd = torch.from_numpy(x).to(dev)
+        wd = torch.from_numpy(w).to(dev)
+        yd = torch.empty((Ho, Wo, L.K, L.N), dtype=torch.float32, device=dev)
+        layers.append((L, Ho, Wo))
+        tensors.append((x, w))
+        dev_bufs.append((xd, wd, yd))
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    def one_step(evs=None):
+        for j, ((L, Ho, Wo), (xd, wd, yd)) in enumerate(zip(layers, dev_bufs)):
+            if evs is not None:
+                evs[j][0].record(stream)
+            if args.plan:
+                mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", plan=args.plan, out=yd)
+            else:
+                mg3m.conv2d_fwd_f32(xd, wd, yd, L.N, L.C, L.H, L.W, L.K, L.R, L.S,
+                                    L.stride, L.pad, "HWCN", sp)
+            if evs is not None:
+                evs[j][1].record(stream)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in layers] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_step(evs[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    step_flops = sum(layer_flops(L, Ho, Wo) for (L, Ho, Wo) in layers)
+    value = step_flops * args.steps / elapsed / 1e12
+
+    per_layer = []
+    for j, (L, Ho, Wo) in enumerate(layers):
+        us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j][1]) for k in range(args.steps)])) * 1e3
+        fl = layer_flops(L, Ho, Wo)
+        by = layer_alg_bytes(L, Ho, Wo)
+        plan = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad,
+                                             "HWCN", args.plan)
+        ai = fl / by
+        attainable = min(PEAK_TFLOPS, ai * HBM_GBS / 1e3)
+        per_layer.append({
+            "layer": L.name, "N": L.N, "C": L.C, "H": L.H, "K": L.K, "R": L.R, "stride": L.stride,
+            "pad": L.pad, "us": round(us, 2), "tflops": round(fl / us / 1e6, 2),
+            "pct_peak": round(100 * fl / us / 1e6 / PEAK_TFLOPS, 1),
+            "pct_roofline": round(100 * fl / us / 1e6 / attainable, 1),
+            "bound": "mfma" if ai * HBM_GBS / 1e3 >= PEAK_TFLOPS else "hbm",
+            "tile": f"{plan['mt']}x{plan['nt']}", "split": plan["split"], "grid": plan["grid"],
+            "flops": fl, "alg_bytes": by,
+        })
+
+    # dominant kernel: the (tile, split) plan with the largest share of step time
+    groups = {}
+    for r in per_layer:
+        key = (r["tile"], r["split"])
+        g = groups.setdefault(key, {"us": 0.0, "flops": 0.0, "n": 0})
+        g["us"] += r["us"]
+        g["flops"] += r["flops"]
+        g["n"] += 1
+    (dtile, dsplit), dg = max(groups.items(), key=lambda kv: kv[1]["us"])
+    achieved = dg["flops"] / dg["us"] / 1e6
+    traffic = None
+    prof = os.path.join(ROOT, "profiles", "traffic_vgg16_n64.json")
+    if os.path.exists(prof) and args.workload == "vgg16_n64" and not args.plan:
+        with open(prof) as f:
+            t = json.load(f)
+        if t.get("kernel_digest") == kernel_source_digest() and t.get("tile") == dtile:
+            traffic = t.get("hbm_bytes_per_launch")
+    roofline = {
+        "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
+        "frac": round(achieved / PEAK_TFLOPS, 4), "traffic": traffic,
+        "kernel": f"conv_igemm_f32 tile {dtile} split {dsplit}",
+        "launches_per_step": dg["n"],
+        "alg_flops_per_launch": dg["flops"] / dg["n"],
+        "avg_launch_us": round(dg["us"] / dg["n"], 2),
+    }
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu = cpu_baseline(layers, tensors, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded uniform[-1,1) inputs, He-normal filters; HWCN layout)",
+        "config": {"workload": args.workload, "layers": len(layers),
+                   "batch": layers[0][0].N, "layout": "HWCN",
+                   "gflop_per_step": round(step_flops / 1e9, 3)},
+        "pct_peak": round(100 * value / PEAK_TFLOPS, 2),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "layers": per_layer,
+        "kernel_digest": kernel_source_digest(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,152 @@
+/*
+ * mg3m.h -- C ABI of the MI355X (gfx950) forward 2-D convolution library.
+ *
+ * The operation is the single-precision forward convolution of Eq. 1 of the
+ * MG3MConv paper (Sec. 2.1), with the symbols of its Table 1:
+ *
+ *   OUT[b,oc,oh,ow] = sum_{ic,fh,fw} IN[b,ic,ih,iw] * FLT[oc,ic,fh,fw],
+ *   ih = oh*stride + fh - pad,  iw = ow*stride + fw - pad,
+ *
+ * taps outside the input contributing nothing (zero padding; the skip rule
+ * of Alg. 2, Sec. 4.3.1).  No filter flip (cross-correlation).  The output
+ * size is outH = floor((inH + 2*pad - fltH)/stride) + 1, likewise outW.
+ * It is computed as an implicit matrix multiplication (Sec. 4.1.1, Eq. 2,
+ * Alg. 1): Mg = OC rows, Ng = B*outH*outW columns, Kg = IC*fltH*fltW depth,
+ * on fp32 MFMA, with a per-shape tile / split-K plan standing in for the
+ * paper's multi-grained thread-block mapping (Sec. 4.1.2).
+ *
+ * Symbols in the argument lists: N = B (batch), C = IC, K = OC, H,W =
+ * inH,inW, R,S = fltH,fltW.
+ *
+ * Layouts (argument `layout`):
+ *   MG3M_LAYOUT_HWCN (0): the paper's storage order (Sec. 4.1.1)
+ *       x[H][W][C][N], w[R][S][C][K], y[Ho][Wo][K][N]  -- the tuned path
+ *   MG3M_LAYOUT_NCHW (1): Eq. 1's index order
+ *       x[N][C][H][W], w[K][C][R][S], y[N][K][Ho][Wo]
+ * All tensors are dense, fp32, row-major in the order written.
+ *
+ * Pointers: x, w, y and workspace are DEVICE pointers on the current HIP
+ * device; stream is a hipStream_t (NULL = the default stream).  Every
+ * compute call is asynchronous and stream-ordered: it returns once the work
+ * is queued.  The caller owns every buffer; the library never frees or keeps
+ * a caller pointer.  y is overwritten (no accumulation, bias or activation).
+ *
+ * Errors: every entry point returns an mg3m_status.  Argument validation is
+ * synchronous and happens before anything is launched, so a rejected call
+ * writes nothing.  Checked: dimensions >= 1, stride >= 1, pad >= 0, a
+ * non-empty output, non-NULL pointers, 4-byte aligned pointers, every tensor
+ * below 2^31 elements, y not overlapping x or w, a known layout, a large
+ * enough workspace, a valid plan override.  HIP launch failures return
+ * MG3M_ERR_HIP with the HIP error text in mg3m_last_error().  No C++
+ * exception crosses this interface.  Calls on different streams may run
+ * concurrently from different host threads.
+ */
+#ifndef MG3M_H
+#define MG3M_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum mg3m_layout {
+    MG3M_LAYOUT_HWCN = 0,
+    MG3M_LAYOUT_NCHW = 1
+};
+
+enum mg3m_status {
+    MG3M_OK = 0,
+    MG3M_ERR_NULL = 1,        /* a required pointer is NULL */
+    MG3M_ERR_SHAPE = 2,       /* a dimension < 1, stride < 1, pad < 0 or empty output */
+    MG3M_ERR_LAYOUT = 3,      /* unknown layout */
+    MG3M_ERR_TOO_LARGE = 4,   /* a tensor has 2^31 elements or more */
+    MG3M_ERR_ALIAS = 5,       /* y overlaps x or w */
+    MG3M_ERR_WORKSPACE = 6,   /* workspace missing or too small for the plan */
+    MG3M_ERR_PLAN = 7,        /* malformed or inapplicable plan override */
+    MG3M_ERR_HIP = 8,         /* HIP runtime or launch error (see mg3m_last_error) */
+    MG3M_ERR_ALIGN = 9,       /* a pointer is not 4-byte aligned */
+    MG3M_ERR_ARG = 10         /* bad auxiliary argument (output buffer, length) */
+};
+
+/* Output size by the floor formula above.  Ho, Wo: host out-parameters.
+ * Returns MG3M_OK or MG3M_ERR_SHAPE / MG3M_ERR_NULL. */
+int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, int *Wo);
+
+/* y = conv(x, w) in `layout`.  Plan chosen by the per-shape selector.  When
+ * the plan splits the Kg reduction (split-K), the partial sums go to a
+ * workspace that this call takes from HIP's stream-ordered allocator
+ * (hipMallocAsync / hipFreeAsync on `stream`); the splits are summed in a
+ * fixed order, so results are deterministic run to run. */
+int conv2d_fwd_f32(const float *x, const float *w, float *y,
+                   int N, int C, int H, int W, int K, int R, int S,
+                   int stride, int pad, int layout, void *stream);
+
+/* Bytes of workspace the plan for this shape needs (0 without split-K).
+ * plan: NULL for the selector's choice, or an override string (below).
+ * bytes: host out-parameter. */
+int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S,
+                                   int stride, int pad, int layout,
+                                   const char *plan, size_t *bytes);
+
+/* As conv2d_fwd_f32, with a caller-owned device workspace (may be NULL when
+ * the plan needs none; must be 16-byte aligned and at least
+ * conv2d_fwd_f32_workspace_bytes() long otherwise) and an optional plan
+ * override.  Override syntax: comma-separated key=value pairs,
+ *   tile=<MT>x<NT>   one of the kernel tile shapes (e.g. 128x128, 64x256)
+ *   split=<n>        split-K factor (1..64; clamped so no split is empty)
+ *   xcd=0|1          XCD-aware work-group order (default 1)
+ * e.g. "tile=128x128,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
+int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
+                      int N, int C, int H, int W, int K, int R, int S,
+                      int stride, int pad, int layout,
+                      void *workspace, size_t workspace_bytes,
+                      const char *plan, void *stream);
+
+/* The plan the selector (or the override) picks for this shape, as text,
+ * e.g. "tile=128x128,waves=2x2,kt=16,split=1,grid=1568,...".  Host only; no
+ * HIP call.  buf: host buffer of `len` bytes, always NUL-terminated on
+ * success; MG3M_ERR_ARG if it is too short. */
+int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S,
+                               int stride, int pad, int layout, const char *plan,
+                               char *buf, size_t len);
+
+/* Numbers behind a plan, for tests and benchmarks.  Host only. */
+typedef struct mg3m_plan_info {
+    int mt, nt, kt;           /* work-group tile: rows (OC), columns (B*outH*outW), depth step */
+    int waves_m, waves_n;     /* waves per work-group along rows / columns */
+    int split;                /* split-K factor actually used */
+    int k_tiles;              /* ceil(Kg / kt) */
+    int k_tiles_per_split;
+    int tiles_m, tiles_n;     /* ceil(Mg / mt), ceil(Ng / nt) */
+    long long grid;           /* work-groups launched by the main kernel */
+    long long Mg, Ng, Kg;     /* implicit-GEMM sizes */
+    size_t workspace_bytes;
+    int lds_bytes;            /* LDS per work-group */
+    double pad_efficiency;    /* Mg*Ng*Kg / (padded tile volume), in (0, 1] */
+    double est_us;            /* the selector's predicted time */
+} mg3m_plan_info;
+
+int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,
+                             int stride, int pad, int layout, const char *plan,
+                             mg3m_plan_info *info);
+
+/* Padding overhead of computing an M x N (x C deep) product in whole
+ * mt x nt register blocks, as in the remainder analysis of Sec. 4.4.2:
+ *   flop_overhead = (ceil(M/mt)*mt * ceil(N/nt)*nt) / (M*N) - 1
+ *   data_overhead = (C*Mp + C*Np + Mp*Np) / (C*M + C*N + M*N) - 1
+ * with Mp, Np the padded sizes.  Host only.  Out-parameters may not be NULL. */
+int mg3m_padding_overhead(int M, int N, int C, int mt, int nt,
+                          double *flop_overhead, double *data_overhead);
+
+/* Fixed text for a status code (never NULL). */
+const char *mg3m_status_string(int status);
+
+/* Detail of the last error on the calling host thread ("" if none). */
+const char *mg3m_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MG3M_H */

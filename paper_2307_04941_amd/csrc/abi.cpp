@@ -1,0 +1,231 @@
+// The C ABI (include/mg3m.h): validation, planning and dispatch.
+//
+// Validation is synchronous and finishes before anything is launched, so a
+// rejected call writes nothing.  No exception crosses the interface.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <exception>
+#include <string>
+
+#include "mg3m.h"
+#include "mg3m_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+int shape_and_plan(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int layout,
+                   const char* plan, bool x16, bool w16, bool y16, mg3m::ConvShape* s,
+                   mg3m::Plan* p) {
+  std::string err;
+  int rc = mg3m::make_shape(N, C, H, W, K, R, S, stride, pad, layout, s, &err);
+  if (rc) return fail(rc, err);
+  rc = mg3m::make_plan(*s, plan, x16, w16, y16, p, &err);
+  if (rc) return fail(rc, err);
+  return MG3M_OK;
+}
+
+int run(const float* x, const float* w, float* y, int N, int C, int H, int W, int K, int R, int S,
+        int stride, int pad, int layout, void* workspace, size_t workspace_bytes, bool own_workspace,
+        const char* plan, void* stream) {
+  g_last_error.clear();
+  if (x == nullptr || w == nullptr || y == nullptr) return fail(MG3M_ERR_NULL, "x, w and y must be non-NULL");
+  if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4))
+    return fail(MG3M_ERR_ALIGN, "x, w and y must be 4-byte aligned");
+  mg3m::ConvShape s;
+  mg3m::Plan p;
+  int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, aligned(x, 16),
+                          aligned(w, 16), aligned(y, 16), &s, &p);
+  if (rc) return rc;
+  const size_t xb = 4ull * N * C * H * W, wb = 4ull * K * C * R * S;
+  const size_t yb = 4ull * (size_t)s.Mg * (size_t)s.Ng;
+  if (overlap(y, yb, x, xb) || overlap(y, yb, w, wb))
+    return fail(MG3M_ERR_ALIAS, "y overlaps x or w");
+
+  float* ws = nullptr;
+  if (p.split > 1) {
+    if (own_workspace) {
+      hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), p.ws_bytes,
+                                    static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return fail(MG3M_ERR_HIP, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+    } else {
+      if (workspace == nullptr || workspace_bytes < p.ws_bytes)
+        return fail(MG3M_ERR_WORKSPACE, "plan needs " + std::to_string(p.ws_bytes) + " workspace bytes");
+      if (!aligned(workspace, 16)) return fail(MG3M_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+      if (overlap(workspace, p.ws_bytes, x, xb) || overlap(workspace, p.ws_bytes, w, wb) ||
+          overlap(workspace, p.ws_bytes, y, yb))
+        return fail(MG3M_ERR_ALIAS, "workspace overlaps x, w or y");
+      ws = static_cast<float*>(workspace);
+    }
+  }
+
+  mg3m::KArgs a{};
+  a.x = x; a.w = w; a.out = p.split > 1 ? ws : y;
+  a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
+  a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
+  a.Mg = (int)s.Mg; a.Ng = (int)s.Ng; a.Kg = (int)s.Kg;
+  a.tiles_m = p.tiles_m; a.tiles_n = p.tiles_n; a.kps = p.kps; a.k_tiles = p.k_tiles;
+  a.a_mode = p.a_mode; a.e_mode = p.e_mode; a.xcd_remap = p.xcd_remap;
+  a.out_split_stride = s.Mg * s.Ng;
+
+  std::string err;
+  rc = mg3m::launch_conv(p, a, stream, &err);
+  if (rc == MG3M_OK && p.split > 1) {
+    const long long elems = s.Mg * s.Ng;
+    rc = mg3m::launch_splitk_reduce(ws, y, elems, p.split, elems % 4 == 0 && aligned(y, 16), stream, &err);
+  }
+  if (own_workspace && ws != nullptr) {
+    hipError_t e = hipFreeAsync(ws, static_cast<hipStream_t>(stream));
+    if (rc == MG3M_OK && e != hipSuccess) {
+      rc = MG3M_ERR_HIP;
+      err = std::string("hipFreeAsync: ") + hipGetErrorString(e);
+    }
+  }
+  if (rc) return fail(rc, err);
+  return MG3M_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int* Ho, int* Wo) {
+  g_last_error.clear();
+  if (Ho == nullptr || Wo == nullptr) return fail(MG3M_ERR_NULL, "Ho and Wo must be non-NULL");
+  mg3m::ConvShape s;
+  std::string err;
+  int rc = mg3m::make_shape(1, 1, H, W, 1, R, S, stride, pad, MG3M_LAYOUT_HWCN, &s, &err);
+  if (rc) return fail(rc, err);
+  *Ho = s.Ho;
+  *Wo = s.Wo;
+  return MG3M_OK;
+}
+
+int conv2d_fwd_f32(const float* x, const float* w, float* y, int N, int C, int H, int W, int K,
+                   int R, int S, int stride, int pad, int layout, void* stream) {
+  try {
+    return run(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, nullptr, 0, true, nullptr, stream);
+  } catch (const std::exception& e) {
+    return fail(MG3M_ERR_HIP, e.what());
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv2d_fwd_f32_ex(const float* x, const float* w, float* y, int N, int C, int H, int W, int K,
+                      int R, int S, int stride, int pad, int layout, void* workspace,
+                      size_t workspace_bytes, const char* plan, void* stream) {
+  try {
+    return run(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, workspace, workspace_bytes, false,
+               plan, stream);
+  } catch (const std::exception& e) {
+    return fail(MG3M_ERR_HIP, e.what());
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
+                                   int pad, int layout, const char* plan, size_t* bytes) {
+  try {
+    g_last_error.clear();
+    if (bytes == nullptr) return fail(MG3M_ERR_NULL, "bytes must be non-NULL");
+    mg3m::ConvShape s;
+    mg3m::Plan p;
+    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    if (rc) return rc;
+    *bytes = p.ws_bytes;
+    return MG3M_OK;
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                               int layout, const char* plan, char* buf, size_t len) {
+  try {
+    g_last_error.clear();
+    if (buf == nullptr) return fail(MG3M_ERR_NULL, "buf must be non-NULL");
+    mg3m::ConvShape s;
+    mg3m::Plan p;
+    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    if (rc) return rc;
+    std::string text = mg3m::plan_to_string(s, p);
+    if (len < text.size() + 1) return fail(MG3M_ERR_ARG, "buffer too short for the plan string");
+    std::memcpy(buf, text.c_str(), text.size() + 1);
+    return MG3M_OK;
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                             int layout, const char* plan, mg3m_plan_info* info) {
+  try {
+    g_last_error.clear();
+    if (info == nullptr) return fail(MG3M_ERR_NULL, "info must be non-NULL");
+    mg3m::ConvShape s;
+    mg3m::Plan p;
+    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    if (rc) return rc;
+    info->mt = p.t.mt; info->nt = p.t.nt; info->kt = p.t.kt;
+    info->waves_m = p.t.wm; info->waves_n = p.t.wn;
+    info->split = p.split; info->k_tiles = p.k_tiles; info->k_tiles_per_split = p.kps;
+    info->tiles_m = p.tiles_m; info->tiles_n = p.tiles_n; info->grid = p.grid;
+    info->Mg = s.Mg; info->Ng = s.Ng; info->Kg = s.Kg;
+    info->workspace_bytes = p.ws_bytes; info->lds_bytes = p.lds_bytes;
+    info->pad_efficiency = p.pad_eff; info->est_us = p.est_us;
+    return MG3M_OK;
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int mg3m_padding_overhead(int M, int N, int C, int mt, int nt, double* flop_overhead,
+                          double* data_overhead) {
+  g_last_error.clear();
+  if (flop_overhead == nullptr || data_overhead == nullptr)
+    return fail(MG3M_ERR_NULL, "out-parameters must be non-NULL");
+  if (M < 1 || N < 1 || C < 1 || mt < 1 || nt < 1) return fail(MG3M_ERR_SHAPE, "sizes must be >= 1");
+  const double Mp = (double)((M + mt - 1) / mt) * mt, Np = (double)((N + nt - 1) / nt) * nt;
+  *flop_overhead = Mp * Np / ((double)M * N) - 1.0;
+  *data_overhead = ((double)C * Mp + (double)C * Np + Mp * Np) /
+                       ((double)C * M + (double)C * N + (double)M * N) - 1.0;
+  return MG3M_OK;
+}
+
+const char* mg3m_status_string(int status) {
+  switch (status) {
+    case MG3M_OK: return "MG3M_OK: success";
+    case MG3M_ERR_NULL: return "MG3M_ERR_NULL: a required pointer is NULL";
+    case MG3M_ERR_SHAPE: return "MG3M_ERR_SHAPE: invalid dimensions, stride, pad or empty output";
+    case MG3M_ERR_LAYOUT: return "MG3M_ERR_LAYOUT: unknown layout";
+    case MG3M_ERR_TOO_LARGE: return "MG3M_ERR_TOO_LARGE: tensor too large for 32-bit indexing";
+    case MG3M_ERR_ALIAS: return "MG3M_ERR_ALIAS: output overlaps an input";
+    case MG3M_ERR_WORKSPACE: return "MG3M_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case MG3M_ERR_PLAN: return "MG3M_ERR_PLAN: invalid plan override";
+    case MG3M_ERR_HIP: return "MG3M_ERR_HIP: HIP runtime error";
+    case MG3M_ERR_ALIGN: return "MG3M_ERR_ALIGN: pointer not 4-byte aligned";
+    case MG3M_ERR_ARG: return "MG3M_ERR_ARG: bad auxiliary argument";
+    default: return "MG3M: unknown status";
+  }
+}
+
+const char* mg3m_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,268 @@
+// Per-shape plan selection: the MI355X counterpart of the multi-grained
+// thread-block mapping of MG3MConv (Sec. 4.1.2, Fig. 3; evaluated in Sec. 5.3,
+// Table 2).  The paper picks, per convolution scene, whether one MM_unit runs
+// on one CPE (TB(1,1)), a row of eight (TB(1,8)) or the whole 8x8 mesh
+// (TB(8,8)), because a coarse mapping starves the cores when B, IC and OC are
+// small, while a fine one repeats memory traffic when they are large.  Here the
+// same trade-off is a choice of work-group tile (how much of the output matrix
+// one work-group owns, and how many waves share its staged operands) and of a
+// split of the reduction, made by a small cost model over 256 compute units.
+//
+// Host only: no HIP call in this file.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "mg3m.h"
+#include "mg3m_internal.h"
+
+namespace mg3m {
+
+namespace {
+
+constexpr int kCUs = 256;                    // MI355X: 8 XCDs x 32 CUs
+constexpr double kClockHz = 2.4e9;
+constexpr double kFlopPerClkCU = 256.0;      // fp32 MFMA: 4 SIMDs x 64 flop/clk
+constexpr double kHbmBytesPerS = 8.0e12;
+constexpr int kLdsBytesPerCU = 160 * 1024;
+constexpr double kLaunchUs = 3.0;            // per kernel launch on the stream
+constexpr double kWgOverheadUs = 1.2;        // prologue + epilogue per work-group round
+
+long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+// Rough per-wave register use, to estimate work-groups resident per CU.
+int regs_per_lane(const TileDesc& t) {
+  const int T = t.wm * t.wn * 64;
+  const int acc = (t.mt / t.wm / 32) * (t.nt / t.wn / 32) * 16;
+  const int stage = (t.kt * t.mt + t.kt * t.nt) / T;
+  return acc + stage + 56;
+}
+
+int resident_wgs(const TileDesc& t) {
+  const int lds = lds_bytes_for(t);
+  const int by_lds = std::max(1, kLdsBytesPerCU / lds);
+  const int regs = (regs_per_lane(t) + 7) / 8 * 8;
+  const int waves_per_simd = std::max(1, std::min(8, 512 / regs));
+  const int by_regs = std::max(1, (4 * waves_per_simd) / (t.wm * t.wn));
+  return std::min(by_lds, by_regs);
+}
+
+// Fraction of MFMA peak a wave sustains with this register block, before
+// occupancy effects: larger blocks read fewer operands per MFMA.
+double block_efficiency(const TileDesc& t) {
+  const int wtm = t.mt / t.wm, wtn = t.nt / t.wn;
+  if (wtm >= 64 && wtn >= 64) return 0.80;
+  if (wtm >= 64 || wtn >= 64) return 0.65;
+  return 0.45;
+}
+
+struct Override {
+  int mt = 0, nt = 0, split = 0, xcd = -1;
+};
+
+int parse_override(const char* text, Override* o, std::string* err) {
+  if (text == nullptr || *text == 0) return MG3M_OK;
+  std::string s(text);
+  size_t pos = 0;
+  while (pos <= s.size()) {
+    size_t end = s.find(',', pos);
+    if (end == std::string::npos) end = s.size();
+    std::string item = s.substr(pos, end - pos);
+    pos = end + 1;
+    if (item.empty()) {
+      if (end == s.size()) break;
+      continue;
+    }
+    size_t eq = item.find('=');
+    if (eq == std::string::npos) {
+      *err = "plan override: expected key=value, got '" + item + "'";
+      return MG3M_ERR_PLAN;
+    }
+    std::string key = item.substr(0, eq), val = item.substr(eq + 1);
+    char* tail = nullptr;
+    if (key == "tile") {
+      size_t x = val.find('x');
+      if (x == std::string::npos) {
+        *err = "plan override: tile must be <MT>x<NT>";
+        return MG3M_ERR_PLAN;
+      }
+      o->mt = (int)std::strtol(val.substr(0, x).c_str(), &tail, 10);
+      o->nt = (int)std::strtol(val.substr(x + 1).c_str(), &tail, 10);
+      if (o->mt <= 0 || o->nt <= 0) {
+        *err = "plan override: bad tile '" + val + "'";
+        return MG3M_ERR_PLAN;
+      }
+    } else if (key == "split") {
+      long v = std::strtol(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || v < 1 || v > 64) {
+        *err = "plan override: split must be 1..64";
+        return MG3M_ERR_PLAN;
+      }
+      o->split = (int)v;
+    } else if (key == "xcd") {
+      if (val != "0" && val != "1") {
+        *err = "plan override: xcd must be 0 or 1";
+        return MG3M_ERR_PLAN;
+      }
+      o->xcd = val == "1";
+    } else {
+      *err = "plan override: unknown key '" + key + "'";
+      return MG3M_ERR_PLAN;
+    }
+    if (end == s.size()) break;
+  }
+  return MG3M_OK;
+}
+
+// Fill the shape-dependent parts of a plan for one (tile, split) choice.
+void shape_plan(const ConvShape& s, int tile, int split_req, Plan* p) {
+  const TileDesc& t = kTiles[tile];
+  p->layout = s.layout;
+  p->tile = tile;
+  p->t = t;
+  p->k_tiles = (int)cdiv(s.Kg, t.kt);
+  p->kps = (int)cdiv(p->k_tiles, std::max(1, std::min(split_req, p->k_tiles)));
+  p->split = (int)cdiv(p->k_tiles, p->kps);       // no empty split
+  p->tiles_m = (int)cdiv(s.Mg, t.mt);
+  p->tiles_n = (int)cdiv(s.Ng, t.nt);
+  p->grid = (long long)p->tiles_m * p->tiles_n * p->split;
+  p->lds_bytes = lds_bytes_for(t);
+  const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
+                        (double)p->k_tiles * t.kt;
+  p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
+  p->ws_bytes = p->split > 1 ? (size_t)p->split * (size_t)(s.Mg * s.Ng) * sizeof(float) : 0;
+
+  // Cost model.  The busiest CU runs ceil(grid / 256) work-groups; each costs
+  // its padded flops at the block efficiency, degraded when fewer than two
+  // waves per SIMD are resident to hide latency.
+  const double wg_flops = 2.0 * t.mt * t.nt * (double)t.kt * p->kps;
+  const long long per_cu = cdiv(p->grid, kCUs);
+  const int occ = resident_wgs(t);
+  const double waves_per_simd =
+      std::min<double>(occ, (double)per_cu) * t.wm * t.wn / 4.0;
+  const double lat = waves_per_simd >= 2.0 ? 1.0 : (waves_per_simd >= 1.0 ? 0.8 : 0.55);
+  const double eff = block_efficiency(t) * lat;
+  const double t_comp = per_cu * wg_flops / (kFlopPerClkCU * kClockHz * eff) * 1e6;
+  const double out_bytes = 4.0 * (double)s.Mg * s.Ng;
+  const double in_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
+  const double t_mem = (in_bytes + out_bytes) / kHbmBytesPerS * 1e6;
+  const double rounds = (double)cdiv(per_cu, occ);
+  double est = std::max(t_comp, t_mem) + kLaunchUs + rounds * kWgOverheadUs;
+  if (p->split > 1) est += (p->split + 1) * out_bytes / kHbmBytesPerS * 1e6 + kLaunchUs + 2.0;
+  p->est_us = est;
+}
+
+}  // namespace
+
+int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int layout,
+               ConvShape* s, std::string* err) {
+  if (layout != kHWCN && layout != kNCHW) {
+    *err = "unknown layout";
+    return MG3M_ERR_LAYOUT;
+  }
+  if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) {
+    *err = "dimensions and stride must be >= 1, pad >= 0";
+    return MG3M_ERR_SHAPE;
+  }
+  if (pad > (1 << 24) || H > (1 << 24) || W > (1 << 24) || R > (1 << 24) || S > (1 << 24)) {
+    *err = "a spatial size or pad exceeds 2^24";
+    return MG3M_ERR_TOO_LARGE;
+  }
+  const long long eh = (long long)H + 2LL * pad - R, ew = (long long)W + 2LL * pad - S;
+  if (eh < 0 || ew < 0) {
+    *err = "filter larger than the padded input: empty output";
+    return MG3M_ERR_SHAPE;
+  }
+  s->N = N; s->C = C; s->H = H; s->W = W; s->K = K; s->R = R; s->S = S;
+  s->sh = s->sw = stride;
+  s->ph = s->pw = pad;
+  s->Ho = (int)(eh / stride + 1);
+  s->Wo = (int)(ew / stride + 1);
+  s->layout = layout;
+  s->Mg = K;
+  s->Ng = (long long)N * s->Ho * s->Wo;
+  s->Kg = (long long)C * R * S;
+  // int32 index arithmetic in the kernels, with head-room for a tile past the end
+  const long long lim = 0x7fffffffLL - 1024;
+  const long long xe = (long long)N * C * H * W, we = (long long)K * C * R * S,
+                  ye = (long long)N * K * s->Ho * s->Wo;
+  if (xe >= lim || we >= lim || ye >= lim || s->Ng >= lim || s->Kg >= lim) {
+    *err = "a tensor has (about) 2^31 elements or more";
+    return MG3M_ERR_TOO_LARGE;
+  }
+  return MG3M_OK;
+}
+
+int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16, bool y16,
+              Plan* p, std::string* err) {
+  Override o;
+  int rc = parse_override(override_text, &o, err);
+  if (rc) return rc;
+
+  int best = -1;
+  Plan best_plan{};
+  const int splits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
+  for (int ti = 0; ti < kNumTiles; ++ti) {
+    if (o.mt && !(kTiles[ti].mt == o.mt && kTiles[ti].nt == o.nt)) continue;
+    for (int sp : splits) {
+      if (o.split && sp != 1) break;
+      Plan c{};
+      shape_plan(s, ti, o.split ? o.split : sp, &c);
+      if (!o.split && c.split != sp) continue;        // duplicate after clamping
+      bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
+                    (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
+                     (c.split < best_plan.split ||
+                      (c.split == best_plan.split && c.t.mt * c.t.nt > best_plan.t.mt * best_plan.t.nt)));
+      if (better) {
+        best = ti;
+        best_plan = c;
+      }
+    }
+  }
+  if (best < 0) {
+    *err = "plan override: no kernel tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt);
+    return MG3M_ERR_PLAN;
+  }
+  *p = best_plan;
+  p->xcd_remap = o.xcd < 0 ? 1 : o.xcd;
+
+  // Loader and epilogue modes.
+  if (s.layout == kHWCN) {
+    p->a_mode = (s.K % 4 == 0 && w16) ? kAVecM : kAScalar;
+    if (s.N % 4 == 0 && x16) p->b_mode = kBVecN;
+    else if (s.N == 1 && s.C % 4 == 0 && x16) p->b_mode = kBVecC;
+    else p->b_mode = kBScalar;
+  } else {
+    p->a_mode = (s.Kg % 4 == 0 && w16) ? kAVecK : kAScalar;
+    p->b_mode = kBScalar;
+  }
+  const bool out16 = p->split > 1 ? true : y16;   // the workspace is 256-byte aligned
+  if (s.layout == kHWCN) {
+    if (s.N % 4 == 0 && out16) p->e_mode = kEVecN;
+    else if (s.N == 1 && s.K % 4 == 0 && out16) p->e_mode = kEVecM;
+    else p->e_mode = kEScalar;
+  } else {
+    p->e_mode = ((long long)s.Ho * s.Wo % 4 == 0 && out16) ? kEVecN : kEScalar;
+  }
+  return MG3M_OK;
+}
+
+std::string plan_to_string(const ConvShape& s, const Plan& p) {
+  static const char* an[] = {"vec_m", "vec_k", "scalar"};
+  static const char* bn[] = {"vec_n", "vec_c", "scalar"};
+  static const char* en[] = {"vec_n", "vec_m", "scalar"};
+  char buf[512];
+  std::snprintf(buf, sizeof buf,
+                "tile=%dx%d,waves=%dx%d,kt=%d,split=%d,grid=%lld,tiles=%dx%d,k_tiles=%d,"
+                "a=%s,b=%s,e=%s,xcd=%d,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
+                "Mg=%lld,Ng=%lld,Kg=%lld",
+                p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.grid, p.tiles_m, p.tiles_n,
+                p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode], p.xcd_remap, p.lds_bytes,
+                p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
+  return buf;
+}
+
+}  // namespace mg3m

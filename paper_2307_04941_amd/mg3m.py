@@ -1,0 +1,211 @@
+"""Thin Python binding of the C ABI in include/mg3m.h (libmg3m.so).
+
+Functions carry the C names and only marshal arguments: every step of the
+convolution runs in the library's HIP kernels.  Device buffers are torch
+tensors (or raw device addresses as ints); torch provides device memory and
+the current stream, nothing else.  There is no fallback: if libmg3m.so is
+missing or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmg3m.so")
+
+HWCN = 0
+NCHW = 1
+LAYOUTS = {"HWCN": HWCN, "NCHW": NCHW}
+
+STATUS = {
+    0: "MG3M_OK", 1: "MG3M_ERR_NULL", 2: "MG3M_ERR_SHAPE", 3: "MG3M_ERR_LAYOUT",
+    4: "MG3M_ERR_TOO_LARGE", 5: "MG3M_ERR_ALIAS", 6: "MG3M_ERR_WORKSPACE", 7: "MG3M_ERR_PLAN",
+    8: "MG3M_ERR_HIP", 9: "MG3M_ERR_ALIGN", 10: "MG3M_ERR_ARG",
+}
+
+
+class Mg3mError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("mt", ctypes.c_int), ("nt", ctypes.c_int), ("kt", ctypes.c_int),
+        ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int),
+        ("split", ctypes.c_int), ("k_tiles", ctypes.c_int), ("k_tiles_per_split", ctypes.c_int),
+        ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
+        ("grid", ctypes.c_longlong), ("Mg", ctypes.c_longlong), ("Ng", ctypes.c_longlong),
+        ("Kg", ctypes.c_longlong), ("workspace_bytes", ctypes.c_size_t), ("lds_bytes", ctypes.c_int),
+        ("pad_efficiency", ctypes.c_double), ("est_us", ctypes.c_double),
+    ]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libmg3m.so (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2307_04941_amd.build`")
+    lib = ctypes.CDLL(path)
+    i, p, sz, cp = ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_char_p
+    shape = [i] * 10                     # N, C, H, W, K, R, S, stride, pad, layout
+    lib.conv2d_out_dims.argtypes = [i] * 6 + [ctypes.POINTER(i)] * 2
+    lib.conv2d_fwd_f32.argtypes = [p, p, p] + shape + [p]
+    lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
+    lib.conv2d_fwd_f32_workspace_bytes.argtypes = shape + [cp, ctypes.POINTER(sz)]
+    lib.conv2d_fwd_f32_plan_string.argtypes = shape + [cp, ctypes.c_char_p, sz]
+    lib.conv2d_fwd_f32_plan_info.argtypes = shape + [cp, ctypes.POINTER(PlanInfo)]
+    lib.mg3m_padding_overhead.argtypes = [i] * 5 + [ctypes.POINTER(ctypes.c_double)] * 2
+    lib.mg3m_status_string.argtypes = [i]
+    lib.mg3m_status_string.restype = ctypes.c_char_p
+    lib.mg3m_last_error.argtypes = []
+    lib.mg3m_last_error.restype = ctypes.c_char_p
+    for name in ("conv2d_out_dims", "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
+                 "conv2d_fwd_f32_workspace_bytes", "conv2d_fwd_f32_plan_string",
+                 "conv2d_fwd_f32_plan_info", "mg3m_padding_overhead"):
+        getattr(lib, name).restype = i
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise Mg3mError(rc, mg3m_last_error())
+
+
+def _layout(layout) -> int:
+    return LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+
+
+def _ptr(t) -> Optional[int]:
+    """Device address of a tensor (must be fp32, contiguous, on a GPU) or an int."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor or an int device address")
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if t.dtype != torch.float32:
+        raise TypeError("tensor must be float32")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _enc(plan):
+    return plan.encode() if isinstance(plan, str) else plan
+
+
+# ------------------------------------------------------------ C-named calls
+def mg3m_status_string(status: int) -> str:
+    return load_library().mg3m_status_string(status).decode()
+
+
+def mg3m_last_error() -> str:
+    return load_library().mg3m_last_error().decode()
+
+
+def conv2d_out_dims(H, W, R, S, stride, pad):
+    ho, wo = ctypes.c_int(), ctypes.c_int()
+    _check(load_library().conv2d_out_dims(H, W, R, S, stride, pad, ctypes.byref(ho), ctypes.byref(wo)))
+    return ho.value, wo.value
+
+
+def conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):
+    _check(load_library().conv2d_fwd_f32(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
+                                         stride, pad, _layout(layout), _stream(stream)))
+
+
+def conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, stride, pad, layout,
+                      workspace=None, workspace_bytes=0, plan=None, stream=None):
+    _check(load_library().conv2d_fwd_f32_ex(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
+                                            stride, pad, _layout(layout), _ptr(workspace),
+                                            workspace_bytes, _enc(plan), _stream(stream)))
+
+
+def conv2d_fwd_f32_workspace_bytes(N, C, H, W, K, R, S, stride, pad, layout, plan=None) -> int:
+    b = ctypes.c_size_t()
+    _check(load_library().conv2d_fwd_f32_workspace_bytes(N, C, H, W, K, R, S, stride, pad,
+                                                         _layout(layout), _enc(plan), ctypes.byref(b)))
+    return b.value
+
+
+def conv2d_fwd_f32_plan_string(N, C, H, W, K, R, S, stride, pad, layout, plan=None) -> str:
+    buf = ctypes.create_string_buffer(1024)
+    _check(load_library().conv2d_fwd_f32_plan_string(N, C, H, W, K, R, S, stride, pad,
+                                                     _layout(layout), _enc(plan), buf, len(buf)))
+    return buf.value.decode()
+
+
+def conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, stride, pad, layout, plan=None) -> dict:
+    info = PlanInfo()
+    _check(load_library().conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, stride, pad,
+                                                   _layout(layout), _enc(plan), ctypes.byref(info)))
+    return info.as_dict()
+
+
+def mg3m_padding_overhead(M, N, C, mt, nt):
+    f, d = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().mg3m_padding_overhead(M, N, C, mt, nt, ctypes.byref(f), ctypes.byref(d)))
+    return f.value, d.value
+
+
+# ------------------------------------------------------- tensor convenience
+def dims_of(x, w, layout):
+    """(N, C, H, W, K, R, S) from tensor shapes in `layout`."""
+    lay = _layout(layout)
+    if lay == HWCN:
+        H, W, C, N = x.shape
+        R, S, C2, K = w.shape
+    else:
+        N, C, H, W = x.shape
+        K, C2, R, S = w.shape
+    if C != C2:
+        raise ValueError("input and filter channel counts differ")
+    return N, C, H, W, K, R, S
+
+
+def conv2d_fwd(x, w, stride: int = 1, pad: int = 0, layout="HWCN", plan: Optional[str] = None,
+               out=None, workspace=None, stream=None):
+    """y = conv(x, w) for torch tensors on the GPU; allocates y unless `out`
+    is given.  With `plan` or `workspace` the _ex entry point is used."""
+    import torch
+    N, C, H, W, K, R, S = dims_of(x, w, layout)
+    Ho, Wo = conv2d_out_dims(H, W, R, S, stride, pad)
+    shape = (Ho, Wo, K, N) if _layout(layout) == HWCN else (N, K, Ho, Wo)
+    y = out if out is not None else torch.empty(shape, dtype=torch.float32, device=x.device)
+    if tuple(y.shape) != shape:
+        raise ValueError(f"out has shape {tuple(y.shape)}, expected {shape}")
+    if plan is None and workspace is None:
+        conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream)
+    else:
+        wsb = conv2d_fwd_f32_workspace_bytes(N, C, H, W, K, R, S, stride, pad, layout, plan)
+        if workspace is None and wsb > 0:
+            workspace = torch.empty((wsb + 3) // 4, dtype=torch.float32, device=x.device)
+        wsz = workspace.numel() * 4 if workspace is not None else 0
+        conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, stride, pad, layout,
+                          workspace, wsz, plan, stream)
+    return y

@@ -1,0 +1,176 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads and
+exports every function include/mg3m.h declares; validation rejects bad
+arguments with the documented status before anything reaches the GPU; the
+planner's plans cover the output and partition the reduction; the padding
+metric reproduces the paper's printed example."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from paper_2307_04941_amd import mg3m
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mg3m.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+# fake, never dereferenced device addresses: every call below fails validation
+X, Wp, Y = 0x100000, 0x200000, 0x300000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = mg3m.load_library()
+    names = declared_functions()
+    assert "conv2d_fwd_f32" in names and len(names) >= 9, names
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in mg3m.h but not exported"
+
+
+def test_status_strings():
+    for code in range(0, 11):
+        s = mg3m.mg3m_status_string(code)
+        assert s.startswith("MG3M_")
+    assert "unknown" in mg3m.mg3m_status_string(99)
+
+
+def _call(*shape, layout=0, x=X, w=Wp, y=Y):
+    lib = mg3m.load_library()
+    return lib.conv2d_fwd_f32(x, w, y, *shape, layout, None)
+
+
+GOOD = (2, 8, 10, 10, 16, 3, 3, 1, 1)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), 1), (dict(w=None), 1), (dict(y=None), 1),
+    (dict(x=X + 2), 9), (dict(y=Y + 1), 9),
+    (dict(layout=2), 3), (dict(layout=-1), 3),
+])
+def test_pointer_and_layout_errors(kw, status):
+    assert _call(*GOOD, **kw) == status
+    assert mg3m.mg3m_last_error() != ""
+
+
+@pytest.mark.parametrize("shape", [
+    (0, 8, 10, 10, 16, 3, 3, 1, 1), (2, 0, 10, 10, 16, 3, 3, 1, 1), (2, 8, 10, 10, 0, 3, 3, 1, 1),
+    (2, 8, 10, 10, 16, 3, 3, 0, 1), (2, 8, 10, 10, 16, 3, 3, 1, -1), (2, 8, 2, 2, 16, 5, 5, 1, 0),
+    (2, 8, 10, 10, 16, 0, 3, 1, 1),
+])
+def test_shape_errors(shape):
+    assert _call(*shape) == 2
+
+
+def test_too_large():
+    assert _call(1 << 16, 1 << 10, 64, 64, 16, 3, 3, 1, 1) == 4
+
+
+def test_alias():
+    # y placed inside x
+    assert _call(*GOOD, x=X, y=X + 64) == 5
+
+
+def test_workspace_and_plan_errors():
+    lib = mg3m.load_library()
+    shape = (4, 64, 14, 14, 96, 3, 3, 1, 1)
+    # forced split-K without a workspace
+    rc = lib.conv2d_fwd_f32_ex(X, Wp, Y, *shape, 0, None, 0, b"split=4", None)
+    assert rc == 6
+    for bad in (b"tile=7x7", b"split=0", b"split=x", b"bogus=1", b"tile=128", b"xcd=2"):
+        rc = lib.conv2d_fwd_f32_ex(X, Wp, Y, *shape, 0, None, 0, bad, None)
+        assert rc == 7, bad
+
+
+def test_out_dims_match_oracle():
+    rng = np.random.Generator(np.random.PCG64(1))
+    for _ in range(300):
+        H, W = (int(v) for v in rng.integers(1, 40, 2))
+        R = int(rng.integers(1, 8))
+        st, pd = int(rng.integers(1, 5)), int(rng.integers(0, 5))
+        if H + 2 * pd < R or W + 2 * pd < R:
+            with pytest.raises(mg3m.Mg3mError):
+                mg3m.conv2d_out_dims(H, W, R, R, st, pd)
+            continue
+        assert mg3m.conv2d_out_dims(H, W, R, R, st, pd) == oracle.out_dims(H, W, R, R, st, pd)
+
+
+def _check_plan(shape, layout, plan=None):
+    N, C, H, W, K, R, S, st, pd = shape
+    p = mg3m.conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, st, pd, layout, plan)
+    Ho, Wo = mg3m.conv2d_out_dims(H, W, R, S, st, pd)
+    Mg, Ng, Kg = K, N * Ho * Wo, C * R * S
+    assert (p["Mg"], p["Ng"], p["Kg"]) == (Mg, Ng, Kg)
+    # tiles cover the output exactly once
+    assert (p["tiles_m"] - 1) * p["mt"] < Mg <= p["tiles_m"] * p["mt"]
+    assert (p["tiles_n"] - 1) * p["nt"] < Ng <= p["tiles_n"] * p["nt"]
+    # splits partition the k-tiles, none empty
+    kt = p["k_tiles"]
+    assert kt == -(-Kg // p["kt"])
+    assert (p["split"] - 1) * p["k_tiles_per_split"] < kt <= p["split"] * p["k_tiles_per_split"]
+    assert p["grid"] == p["tiles_m"] * p["tiles_n"] * p["split"] <= 2**31 - 1
+    assert p["workspace_bytes"] == (4 * p["split"] * Mg * Ng if p["split"] > 1 else 0)
+    assert 0 < p["lds_bytes"] <= 160 * 1024
+    assert 0 < p["pad_efficiency"] <= 1.0
+    assert p["est_us"] > 0
+    return p
+
+
+def test_plans_for_every_catalogue_layer():
+    for wl, (_, layers) in workloads.WORKLOADS.items():
+        for L in layers:
+            for layout in ("HWCN", "NCHW"):
+                _check_plan((L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad), layout)
+
+
+def test_plans_random_grid_and_overrides():
+    rng = np.random.Generator(np.random.PCG64(2))
+    tiles = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x128", "32x64",
+             "128x32", "64x32"]
+    for _ in range(200):
+        N = int(rng.integers(1, 65))
+        C, K = (int(v) for v in rng.integers(1, 600, 2))
+        H = int(rng.integers(1, 60))
+        R = int(rng.choice([1, 3, 5, 7]))
+        st, pd = int(rng.integers(1, 4)), int(rng.integers(0, 4))
+        if H + 2 * pd < R:
+            continue
+        shape = (N, C, H, H, K, R, R, st, pd)
+        _check_plan(shape, "HWCN")
+        t = str(rng.choice(tiles))
+        sp = int(rng.integers(1, 20))
+        p = _check_plan(shape, "NCHW", f"tile={t},split={sp}")
+        assert f"{p['mt']}x{p['nt']}" == t
+        assert p["split"] <= sp
+
+
+def test_plan_string_roundtrip():
+    s = mg3m.conv2d_fwd_f32_plan_string(64, 512, 28, 28, 512, 3, 3, 1, 1, "HWCN", "tile=128x128,split=2")
+    assert s.startswith("tile=128x128,") and "split=2" in s
+    lib = mg3m.load_library()
+    import ctypes
+    buf = ctypes.create_string_buffer(8)
+    assert lib.conv2d_fwd_f32_plan_string(64, 512, 28, 28, 512, 3, 3, 1, 1, 0, None, buf, 8) == 10
+
+
+def test_padding_overhead_reproduces_paper_example():
+    g = json.load(open(os.path.join(GOLDEN, "paper_arithmetic.json")))["padding_overhead"]
+    f, d = mg3m.mg3m_padding_overhead(g["K"], g["N"], g["C"], g["Kr"], g["Nr"])
+    assert round(100 * f, g["printed_decimals"]) == g["extra_compute_pct"]
+    assert round(100 * d, g["printed_decimals"]) == g["extra_data_pct"]
+    f0, d0 = mg3m.mg3m_padding_overhead(32, 48, 16, 4, 16)
+    assert f0 == 0.0 and d0 == 0.0
+
+
+def test_inception_5x5_layer_matches_paper_mm_unit():
+    g = json.load(open(os.path.join(GOLDEN, "paper_arithmetic.json")))["inception3a_5x5_mm_unit"]
+    L = [l for l in workloads.workload("alexnet_inception_n128") if l.name == "incep3a_5x5"][0]
+    assert (L.K, L.N, L.C) == (g["M_oc"], g["N_batch"], g["K_ic"])

@@ -1,0 +1,176 @@
+"""GPU parity: the HIP implicit-GEMM convolution (through the C ABI) against
+the fp64 oracle, element by element, |gpu - oracle| <= 1e-5 * sum|x*w|
+(and bit-exact on small-integer data, where every partial sum is an integer
+below 2^24 and fp32 is exact in any order)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from paper_2307_04941_amd import mg3m
+from tests.gpu_util import assert_parity, make, run_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+TILES = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x128", "32x64",
+         "128x32", "64x32"]
+
+
+def _small_grid():
+    rng = np.random.Generator(np.random.PCG64(20230704))
+    cases = []
+    while len(cases) < 36:
+        N = int(rng.choice([1, 2, 3, 4, 5, 8]))
+        C = int(rng.choice([1, 3, 4, 5, 8, 16, 20]))
+        K = int(rng.choice([1, 3, 16, 17, 30, 33, 64, 96]))
+        H, W = (int(v) for v in rng.integers(1, 15, 2))
+        R, S = (int(v) for v in rng.choice([1, 2, 3, 5], 2))
+        st = int(rng.integers(1, 4))
+        pd = int(rng.integers(0, 4))
+        if H + 2 * pd < R or W + 2 * pd < S:
+            continue
+        cases.append((N, C, H, W, K, R, S, st, pd))
+    return cases
+
+
+SMALL = _small_grid()
+
+
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_grid(case, layout):
+    shape = SMALL[case]
+    say(f"small grid {case} {layout} shape={shape}")
+    x, w, st, pd = make(shape, 1000 + case, layout)
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    y = run_gpu(x, w, st, pd, layout)
+    assert_parity(y, acc, mag, f"{shape} {layout}")
+
+
+# One ragged shape (every GEMM dimension has a tail) forced through every tile
+# and several split-K factors, in each loader mode.
+FORCED_SHAPES = {
+    "vec_n": (4, 20, 13, 11, 70, 3, 3, 1, 1),     # N % 4 == 0: batch-vector gather
+    "vec_c": (1, 24, 17, 15, 70, 3, 3, 2, 1),     # N == 1, C % 4 == 0: channel-vector gather
+    "scalar": (3, 5, 12, 13, 45, 3, 2, 1, 2),     # element-wise gather
+}
+
+
+@pytest.mark.parametrize("mode", sorted(FORCED_SHAPES))
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_and_split(tile, mode):
+    shape = FORCED_SHAPES[mode]
+    x, w, st, pd = make(shape, 77, "HWCN")
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    for split in (1, 2, 5):
+        plan = f"tile={tile},split={split}"
+        say(f"forced {mode} {plan} shape={shape}")
+        y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+        assert_parity(y, acc, mag, f"{shape} {plan}")
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_nchw(tile):
+    shape = (2, 6, 11, 9, 37, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 78, "NCHW")
+    acc, mag = oracle.conv2d(x, w, st, pd, "NCHW")
+    for split in (1, 3):
+        plan = f"tile={tile},split={split}"
+        say(f"forced NCHW {plan}")
+        y = run_gpu(x, w, st, pd, "NCHW", plan=plan)
+        assert_parity(y, acc, mag, f"{shape} {plan}")
+
+
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+def test_misaligned_pointers(layout):
+    """4-byte but not 16-byte aligned buffers take the element-wise paths."""
+    shape = (4, 8, 9, 9, 32, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 79, layout)
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    y = run_gpu(x, w, st, pd, layout, misalign=1)
+    assert_parity(y, acc, mag, "misaligned")
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 16, 32, 32, 16, 3, 3, 1, 1),        # the single-layer case
+    (2, 32, 14, 14, 64, 3, 3, 1, 1),
+    (1, 64, 9, 9, 128, 3, 3, 2, 1),
+    (4, 12, 8, 8, 24, 5, 5, 1, 2),
+])
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+def test_small_integer_bit_exact(shape, layout):
+    x, w, st, pd = make(shape, 80, layout, dist="int")
+    acc, _ = oracle.conv2d(x, w, st, pd, layout)
+    for plan in (None, "split=3"):
+        y = run_gpu(x, w, st, pd, layout, plan=plan)
+        assert np.array_equal(y.astype(np.float64), acc), f"{shape} {layout} {plan}: not bit-exact"
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 1, 1, 1, 1, 1, 1, 1, 0),            # everything 1
+    (1, 2, 3, 3, 2, 2, 2, 1, 3),            # pad >= R: all-zero border outputs
+    (2, 3, 7, 7, 5, 2, 2, 4, 0),            # stride > R: skipped input pixels
+    (1, 3, 1, 17, 4, 1, 5, 1, 2),           # one input row
+    (3, 1, 6, 6, 1, 3, 3, 1, 1),            # C == K == 1
+    (1, 4, 5, 5, 200, 1, 1, 1, 0),          # Mg spans several tiles, Ng tiny
+])
+def test_degenerate_shapes(shape):
+    for layout in ("HWCN", "NCHW"):
+        x, w, st, pd = make(shape, 81, layout)
+        acc, mag = oracle.conv2d(x, w, st, pd, layout)
+        y = run_gpu(x, w, st, pd, layout)
+        assert_parity(y, acc, mag, f"{shape} {layout}")
+
+
+def test_guard_bands_and_determinism():
+    """Nothing outside y is written; split-K results repeat bit for bit."""
+    import torch
+    shape = (4, 64, 14, 14, 96, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 82, "HWCN")
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    Ho, Wo = mg3m.conv2d_out_dims(14, 14, 3, 3, 1, 1)
+    n = Ho * Wo * 96 * 4
+    pad = 4096
+    outs = []
+    for _ in range(2):
+        buf = torch.full((n + 2 * pad,), float("nan"), device="cuda")
+        y = buf[pad:pad + n].view(Ho, Wo, 96, 4)
+        mg3m.conv2d_fwd(xd, wd, st, pd, "HWCN", plan="split=4", out=y)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.isnan(b[:pad]).all() and np.isnan(b[pad + n:]).all(), "write outside y"
+        outs.append(b[pad:pad + n].copy())
+    assert np.array_equal(outs[0], outs[1])
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    assert_parity(outs[0].reshape(Ho, Wo, 96, 4), acc, mag, "guard")
+
+
+def test_non_default_stream():
+    import torch
+    shape = (8, 32, 16, 16, 64, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 83, "HWCN")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+        y = mg3m.conv2d_fwd(xd, wd, st, pd, "HWCN")
+        host = torch.empty(y.shape, dtype=torch.float32, pin_memory=True)
+        host.copy_(y, non_blocking=True)
+    s.synchronize()
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    assert_parity(host.numpy(), acc, mag, "stream")
+
+
+def test_caller_workspace_too_small_is_rejected():
+    import torch
+    shape = (4, 64, 14, 14, 96, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 84, "HWCN")
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = torch.full((14, 14, 96, 4), 7.0, device="cuda")
+    need = mg3m.conv2d_fwd_f32_workspace_bytes(4, 64, 14, 14, 96, 3, 3, 1, 1, "HWCN", "split=4")
+    ws = torch.empty(need // 4 - 1, device="cuda")
+    with pytest.raises(mg3m.Mg3mError) as e:
+        mg3m.conv2d_fwd_f32_ex(xd, wd, y, 4, 64, 14, 14, 96, 3, 3, 1, 1, "HWCN",
+                               ws, ws.numel() * 4, "split=4")
+    assert e.value.status == 6
+    torch.cuda.synchronize()
+    assert (y == 7.0).all().item(), "a rejected call wrote to y"

@@ -1,0 +1,45 @@
+"""GPU parity at full layer sizes, in the launch configuration the benchmark
+times (the selector's plan, HWCN): every layer of every catalogue workload.
+The oracle computes a seeded sample of outputs one by one (all outputs of
+the corner pixels, which see the padding, plus random ones); every output is
+also checked to be finite."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from paper_2307_04941_amd import mg3m
+from tests.gpu_util import RTOL, say
+
+pytestmark = pytest.mark.gpu
+
+LAYERS = [(wl, i) for wl, (_, layers) in workloads.WORKLOADS.items() for i in range(len(layers))]
+
+
+@pytest.mark.parametrize("wl,index", LAYERS, ids=[f"{wl}-{i}" for wl, i in LAYERS])
+def test_layer_sampled(wl, index):
+    import torch
+    layer, x, w = workloads.layer_tensors(wl, index, "HWCN")
+    say(f"layer {wl}/{layer.name} N={layer.N} C={layer.C} HW={layer.H} K={layer.K} "
+        f"RS={layer.R} s={layer.stride} p={layer.pad}: "
+        + mg3m.conv2d_fwd_f32_plan_string(layer.N, layer.C, layer.H, layer.W, layer.K, layer.R,
+                                          layer.S, layer.stride, layer.pad, "HWCN"))
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = mg3m.conv2d_fwd(xd, wd, layer.stride, layer.pad, "HWCN")
+    torch.cuda.synchronize()
+    assert torch.isfinite(y).all().item(), "non-finite output"
+    Ho, Wo, K, N = y.shape
+    per_pix = K * N
+    rng = np.random.Generator(np.random.PCG64(4242 + index))
+    idx = np.concatenate([
+        np.arange(0, per_pix),                                    # pixel (0, 0)
+        np.arange((Ho * Wo - 1) * per_pix, Ho * Wo * per_pix),    # pixel (Ho-1, Wo-1)
+        rng.integers(0, y.numel(), 8192),
+    ]).astype(np.int64)
+    got = y.view(-1)[torch.from_numpy(idx).cuda()].cpu().numpy().astype(np.float64)
+    acc, mag = oracle.conv2d_points(x, w, idx, layer.stride, layer.pad, "HWCN")
+    err = np.abs(got - acc)
+    bad = ~(err <= RTOL * mag)
+    worst = float(np.max(np.where(mag > 0, err / (RTOL * np.where(mag > 0, mag, 1)), 0)))
+    say(f"  sampled {idx.size} outputs, worst ratio {worst:.3g}")
+    assert not bad.any(), f"{int(bad.sum())} sampled outputs outside tolerance (worst {worst:.3g})"
