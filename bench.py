@@ -29,10 +29,13 @@ METRIC = "fp32 conv TFLOPS and % of MI355X fp32 MFMA peak per layer, 1 GPU"
 
 
 def kernel_source_digest() -> str:
+    """Digest of every library source: profile figures taken on other sources
+    are not reused."""
     h = hashlib.sha256()
-    for f in ("conv_igemm.hip", "plan.cpp", "abi.cpp", "mg3m_internal.h"):
-        with open(os.path.join(ROOT, "paper_2307_04941_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2307_04941_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
@@ -94,6 +97,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU work budget of the oracle baseline (0 = skip)")
     ap.add_argument("--plan", default=None, help="plan override for every layer (diagnostics)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="before the warm-up, copy a buffer of this many MiB once (a plain copy "
+                         "kernel of known size, to scale the HBM byte counters of a profile run)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -128,6 +134,15 @@ def main():
 
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
+
+    if args.copy_mib > 0:
+        n = args.copy_mib * (1 << 20) // 4
+        src = torch.zeros(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def one_step(evs=None):
         for j, ((L, Ho, Wo), (xd, wd, yd)) in enumerate(zip(layers, dev_bufs)):

@@ -35,8 +35,9 @@
  * synchronous and happens before anything is launched, so a rejected call
  * writes nothing.  Checked: dimensions >= 1, stride >= 1, pad >= 0, a
  * non-empty output, non-NULL pointers, 4-byte aligned pointers, every tensor
- * below 2^31 elements, y not overlapping x or w, a known layout, a large
- * enough workspace, a valid plan override.  HIP launch failures return
+ * at most 4 GiB - 64 bytes (the kernels use 32-bit byte offsets), y not
+ * overlapping x or w, a known layout, a large enough workspace, a valid plan
+ * override.  HIP launch failures return
  * MG3M_ERR_HIP with the HIP error text in mg3m_last_error().  No C++
  * exception crosses this interface.  Calls on different streams may run
  * concurrently from different host threads.
@@ -60,7 +61,7 @@ enum mg3m_status {
     MG3M_ERR_NULL = 1,        /* a required pointer is NULL */
     MG3M_ERR_SHAPE = 2,       /* a dimension < 1, stride < 1, pad < 0 or empty output */
     MG3M_ERR_LAYOUT = 3,      /* unknown layout */
-    MG3M_ERR_TOO_LARGE = 4,   /* a tensor has 2^31 elements or more */
+    MG3M_ERR_TOO_LARGE = 4,   /* a tensor is larger than 4 GiB - 64 bytes */
     MG3M_ERR_ALIAS = 5,       /* y overlaps x or w */
     MG3M_ERR_WORKSPACE = 6,   /* workspace missing or too small for the plan */
     MG3M_ERR_PLAN = 7,        /* malformed or inapplicable plan override */
@@ -94,9 +95,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  * conv2d_fwd_f32_workspace_bytes() long otherwise) and an optional plan
  * override.  Override syntax: comma-separated key=value pairs,
  *   tile=<MT>x<NT>   one of the kernel tile shapes (e.g. 128x128, 64x256)
+ *   kt=16|32         reduction depth staged per step (default 16 with a tile)
  *   split=<n>        split-K factor (1..64; clamped so no split is empty)
- *   xcd=0|1          XCD-aware work-group order (default 1)
- * e.g. "tile=128x128,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
+ *   xcd=0|1          XCD-aware work-group order (default 0)
+ * e.g. "tile=128x128,kt=32,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
 int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
                       int N, int C, int H, int W, int K, int R, int S,
                       int stride, int pad, int layout,

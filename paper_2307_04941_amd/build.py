@@ -17,7 +17,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmg3m.so")
-SOURCES = ["conv_igemm.hip", "plan.cpp", "abi.cpp"]
+SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn.hip", "conv_hwcn_vecc.hip", "conv_hwcn_veca.hip", "conv_hwcn_scalar.hip",
+           "conv_nchw.hip", "conv_launch.hip", "plan.cpp", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

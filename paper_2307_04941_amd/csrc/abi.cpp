@@ -76,11 +76,13 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
 
   mg3m::KArgs a{};
   a.x = x; a.w = w; a.out = p.split > 1 ? ws : y;
+  a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb;
   a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
   a.Mg = (int)s.Mg; a.Ng = (int)s.Ng; a.Kg = (int)s.Kg;
   a.tiles_m = p.tiles_m; a.tiles_n = p.tiles_n; a.kps = p.kps; a.k_tiles = p.k_tiles;
-  a.a_mode = p.a_mode; a.e_mode = p.e_mode; a.xcd_remap = p.xcd_remap;
+  a.e_mode = p.e_mode; a.xcd_remap = p.xcd_remap;
+  a.mstride = s.layout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
   a.out_split_stride = s.Mg * s.Ng;
 
   std::string err;

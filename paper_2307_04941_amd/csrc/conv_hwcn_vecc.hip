@@ -1,0 +1,9 @@
+// Instantiations of the implicit-GEMM kernel for the HWCN layout with the
+// kAVecM filter loader and the kBVecC input-patch loader, one per tile shape.
+#include "conv_kernel.h"
+
+namespace mg3m {
+
+KernelFn conv_kernel_hwcn_vecc(int tile) { return kernel_for_tile<kHWCN, kAVecM, kBVecC>(tile); }
+
+}  // namespace mg3m

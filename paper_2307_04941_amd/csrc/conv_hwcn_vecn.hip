@@ -1,0 +1,9 @@
+// Instantiations of the implicit-GEMM kernel for the HWCN layout with the
+// kAVecM filter loader and the kBVecN input-patch loader, one per tile shape.
+#include "conv_kernel.h"
+
+namespace mg3m {
+
+KernelFn conv_kernel_hwcn_vecn(int tile) { return kernel_for_tile<kHWCN, kAVecM, kBVecN>(tile); }
+
+}  // namespace mg3m

@@ -1,0 +1,607 @@
+// Implicit-GEMM forward convolution on fp32 MFMA for gfx950 (MI355X): the
+// device template.  Included by the instantiation files (conv_hwcn_*.hip,
+// conv_nchw.hip); not part of the public interface.
+//
+// The convolution of Eq. 1 (Sec. 2.1) is computed as the matrix product of
+// Eq. 2 / Alg. 1 (Sec. 4.1.1), without materialising the patch matrix:
+//
+//   OUT[m][n] = sum_k A[m][k] * B[k][n]
+//   m = output channel                  (Mg = OC)
+//   n = (output pixel, image)           (Ng = B*outH*outW)
+//   k = (filter tap, input channel)     (Kg = IC*fltH*fltW)
+//
+// In the paper's HWCN storage (Sec. 4.1.1) the filter is already the dense
+// Kg x OC matrix A^T (each FLT_mtx of Alg. 1 is one IC x OC slab of it, k
+// ordered (fh, fw, ic)), and column n of B at row k is one element of the
+// IN_mtx at pixel (ih, iw), so a k-slab of B is a gather of contiguous IN_mtx
+// rows.  In NCHW the reduction runs in (ic, fh, fw) order.
+//
+// How the paper's design maps onto CDNA4:
+//  * Multi-grained mapping (Sec. 4.1.2): the work-group tile (mt x nt) and the
+//    split of the reduction are chosen per shape by the host planner; small
+//    tiles play the role of TB(1,1), tiles whose waves share one operand that
+//    of TB(1,8), 2-D wave grids that of TB(8,8).
+//  * On-chip sharing (Sec. 4.2, Eq. 4/5): the waves of a work-group share the
+//    staged A and B tiles through LDS instead of register broadcasts.
+//  * Filter reuse (Alg. 2): one staged A tile serves all nt columns.
+//  * Double buffering (Alg. 3): two LDS stages; the next tile's global loads
+//    are in flight while the MFMAs consume the current stage.
+//  * Register blocking (Sec. 4.4.1, Eq. 9): each wave holds a (mt/wm) x
+//    (nt/wn) accumulator block as 32x32 MFMA blocks in AccVGPRs; each lane
+//    reads one A and one B value from LDS per 4096-flop MFMA.
+//  * Remainders (Sec. 4.4.2): instead of sixteen remainder kernels, edge
+//    tiles and padding taps are zero-filled by the buffer hardware (an
+//    out-of-range offset reads as 0) and stores are masked.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "mg3m_internal.h"
+
+namespace mg3m {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Byte offset that is past the end of every buffer the kernels read (tensors
+// are limited to kMaxTensorBytes): a raw buffer load there returns zero.
+constexpr unsigned kOOB = 0xFFFFFFC0u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* p, unsigned bytes) {
+  // stride 0 (raw buffer), num_records = bytes, 32-bit data format.
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ f32x4 bload4(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ void st4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+
+template <int MT, int NT, int KT, int WM, int WN>
+struct Cfg {
+  static constexpr int T = WM * WN * 64;        // threads per work-group
+  static constexpr int WTM = MT / WM;           // wave tile rows
+  static constexpr int WTN = NT / WN;           // wave tile columns
+  static constexpr int TM = WTM / 32;           // 32x32 MFMA blocks per wave, rows
+  static constexpr int TN = WTN / 32;           // ... columns
+  static constexpr int AS = lds_row_stride(MT);
+  static constexpr int BS = lds_row_stride(NT);
+  static constexpr int A_STAGE = KT * AS;
+  static constexpr int B_STAGE = KT * BS;
+  static constexpr int LDS_FLOATS = 2 * A_STAGE + 2 * B_STAGE;
+  static constexpr int A_ELEMS = KT * MT / T;    // A elements each thread loads per stage
+  static constexpr int B_ELEMS = KT * NT / T;
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
+  static_assert(KT % 2 == 0, "the 32x32x2 MFMA consumes two reduction rows");
+  static_assert(LDS_FLOATS * 4 == lds_bytes_for(TileDesc{MT, NT, KT, WM, WN, 0, 0.0}), "LDS size model");
+};
+
+// Reduction index k -> (filter row r, filter column s, input channel c).
+template <int LAYOUT>
+__device__ __forceinline__ void split_k(const KArgs& a, int k, int& r, int& s, int& c) {
+  if constexpr (LAYOUT == kHWCN) {           // k = (r*S + s)*C + c
+    c = k % a.C; int rs = k / a.C; s = rs % a.S; r = rs / a.S;
+  } else {                                   // k = (c*R + r)*S + s
+    s = k % a.S; int cr = k / a.S; r = cr % a.R; c = cr / a.R;
+  }
+}
+
+// Move (r, s, c) forward by `step` reduction rows, HWCN order (c fastest).
+__device__ __forceinline__ void step_rsc(const KArgs& a, int step, int& r, int& s, int& c) {
+  c += step;
+  while (c >= a.C) {
+    c -= a.C;
+    if (++s == a.S) { s = 0; ++r; }
+  }
+}
+
+// ------------------------------------------------------------ A (filter)
+// HWCN filter w[R][S][C][K] is A^T[k][m] (OC contiguous): each thread owns a
+// 4-wide OC vector and NV rows of the KT x MT tile.  Element offsets advance
+// by KT*K per stage.
+template <class C, int MT, int KT>
+struct AVecM {
+  static constexpr int MC4 = MT / 4;
+  static constexpr int RSTEP = C::T / MC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % MC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::A_ELEMS, "A vec-M split");
+  int m4, kr0, k0, off0;
+  bool m_ok;
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs& a, int t, int m0, int kbeg) {
+    m4 = t % MC4;
+    kr0 = t / MC4;
+    const int m = m0 + m4 * 4;
+    m_ok = m < a.Mg;
+    k0 = kbeg + kr0;
+    off0 = k0 * a.K + m;
+  }
+  __device__ void advance(const KArgs& a) {
+    k0 += KT;
+    off0 += KT * a.K;
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t wr) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const bool ok = m_ok & (k0 + i * RSTEP < a.Kg);
+      const unsigned off = (unsigned)(off0 + i * RSTEP * a.K) * 4u;
+      v[i] = bload4(wr, ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* As) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + m4 * 4, v[i]);
+  }
+};
+
+// NCHW filter w[K][C][R][S] is A[m][k] (Kg contiguous): 4-wide k vectors,
+// transposed into the k-major LDS tile.
+template <class C, int MT, int KT>
+struct AVecK {
+  static constexpr int KV = KT / 4;
+  static constexpr int MSTEP = C::T / KV;
+  static constexpr int NV = MT / MSTEP;
+  static_assert(C::T % KV == 0 && MT % MSTEP == 0 && NV * 4 == C::A_ELEMS, "A vec-K split");
+  int k4, mr0, k, m_base;
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs&, int t, int m0, int kbeg) {
+    k4 = t % KV;
+    mr0 = t / KV;
+    k = kbeg + 4 * k4;
+    m_base = m0;
+  }
+  __device__ void advance(const KArgs&) { k += KT; }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t wr) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int m = m_base + mr0 + i * MSTEP;
+      const bool ok = (m < a.Mg) & (k < a.Kg);
+      const unsigned off = (unsigned)(m * a.Kg + k) * 4u;
+      v[i] = bload4(wr, ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* As) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int mm = mr0 + i * MSTEP;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) As[(4 * k4 + e) * C::AS + mm] = v[i][e];
+    }
+  }
+};
+
+// Any layout, any alignment: single elements, coalesced along the
+// contiguous axis of the filter (m for HWCN, k for NCHW).
+template <int LAYOUT, class C, int MT, int KT>
+struct AScalar {
+  static constexpr int NE = C::A_ELEMS;
+  int t_, m0_, kbase;
+  float v[NE];
+
+  __device__ void init(const KArgs&, int t, int m0, int kbeg) { t_ = t; m0_ = m0; kbase = kbeg; }
+  __device__ void advance(const KArgs&) { kbase += KT; }
+  __device__ static void coords(int e, int& m, int& kr) {
+    if constexpr (LAYOUT == kHWCN) { m = e % MT; kr = e / MT; }
+    else { kr = e % KT; m = e / KT; }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t wr) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      int m, kr;
+      coords(t_ + i * C::T, m, kr);
+      const int mg = m0_ + m, k = kbase + kr;
+      const bool ok = (mg < a.Mg) & (k < a.Kg);
+      const int idx = (LAYOUT == kHWCN) ? k * a.K + mg : mg * a.Kg + k;
+      v[i] = bload1(wr, ok ? (unsigned)idx * 4u : kOOB);
+    }
+  }
+  __device__ void store(float* As) const {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      int m, kr;
+      coords(t_ + i * C::T, m, kr);
+      As[kr * C::AS + m] = v[i];
+    }
+  }
+};
+
+// ------------------------------------------------------ B (input patches)
+// HWCN, N % 4 == 0, C % KT == 0: a KT-row slab of the reduction then lies
+// inside one filter tap (r, s) -- the per-pixel IN_mtx of Alg. 1 -- so the tap
+// is the same for the whole work-group and kept in scalar registers; each
+// thread tests its column against the padding once per stage and its NV rows
+// are consecutive channel offsets of one input pixel.
+template <class C, int NT, int KT>
+struct BVecNTap {
+  static constexpr int NC4 = NT / 4;
+  static constexpr int RSTEP = C::T / NC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % NC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::B_ELEMS, "B vec-N split");
+  int n4, kr0, ih0, iw0, base;
+  bool col_ok;
+  int r, s, c0;            // uniform: tap and first channel of the slab
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    n4 = t % NC4;
+    kr0 = t / NC4;
+    const int n = n0 + n4 * 4;
+    col_ok = n < a.Ng;
+    const int pix = n / a.N;
+    const int b = n - pix * a.N;
+    const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+    ih0 = ho * a.sh - a.ph;
+    iw0 = wo * a.sw - a.pw;
+    // element offset of (ih0, iw0, channel kr0, image b); only used when the
+    // tap lands inside the input
+    base = ((ih0 * a.W + iw0) * a.C + kr0) * a.N + b;
+    const int tap = kbeg / a.C;
+    c0 = kbeg - tap * a.C;
+    s = tap % a.S;
+    r = tap / a.S;
+  }
+  __device__ void advance(const KArgs& a) {
+    c0 += KT;
+    if (c0 == a.C) {
+      c0 = 0;
+      if (++s == a.S) { s = 0; ++r; }
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+    const bool ok = col_ok & ((unsigned)(ih0 + r) < (unsigned)a.H) &
+                    ((unsigned)(iw0 + s) < (unsigned)a.W);
+    const int o = base + ((r * a.W + s) * a.C + c0) * a.N;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const unsigned off = (unsigned)(o + i * RSTEP * a.N) * 4u;
+      v[i] = bload4(xr, ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + n4 * 4, v[i]);
+  }
+};
+
+// HWCN, N % 4 == 0: each thread owns one 4-wide batch vector of one output
+// pixel (a fixed column group) and NV rows of the KT x NT tile.
+template <class C, int NT, int KT>
+struct BVecN {
+  static constexpr int NC4 = NT / 4;
+  static constexpr int RSTEP = C::T / NC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % NC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::B_ELEMS, "B vec-N split");
+  int n4, kr0, ih0, iw0, b;
+  bool col_ok;
+  int k[NV], r[NV], s[NV], c[NV];
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    n4 = t % NC4;
+    kr0 = t / NC4;
+    const int n = n0 + n4 * 4;
+    col_ok = n < a.Ng;
+    const int pix = n / a.N;
+    b = n - pix * a.N;
+    const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+    ih0 = ho * a.sh - a.ph;
+    iw0 = wo * a.sw - a.pw;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      k[i] = kbeg + kr0 + i * RSTEP;
+      split_k<kHWCN>(a, k[i], r[i], s[i], c[i]);
+    }
+  }
+  __device__ void advance(const KArgs& a) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      k[i] += KT;
+      step_rsc(a, KT, r[i], s[i], c[i]);
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int ih = ih0 + r[i], iw = iw0 + s[i];
+      const bool ok = col_ok & (k[i] < a.Kg) & ((unsigned)ih < (unsigned)a.H) &
+                      ((unsigned)iw < (unsigned)a.W);
+      const unsigned off = (unsigned)(((ih * a.W + iw) * a.C + c[i]) * a.N + b) * 4u;
+      v[i] = bload4(xr, ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + n4 * 4, v[i]);
+  }
+};
+
+// HWCN, N == 1, C % 4 == 0: each thread owns one 4-deep channel vector of
+// one filter tap (a fixed row group) and NV output pixels.
+template <class C, int NT, int KT>
+struct BVecC {
+  static constexpr int KV = KT / 4;
+  static constexpr int NSTEP = C::T / KV;
+  static constexpr int NV = NT / NSTEP;
+  static_assert(C::T % KV == 0 && NT % NSTEP == 0 && NV * 4 == C::B_ELEMS, "B vec-C split");
+  int k4, nc0, k, r, s, c;
+  int ih0[NV], iw0[NV];
+  bool col_ok[NV];
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    k4 = t % KV;
+    nc0 = t / KV;
+    k = kbeg + 4 * k4;
+    split_k<kHWCN>(a, k, r, s, c);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int n = n0 + nc0 + i * NSTEP;          // N == 1: n is the output pixel
+      col_ok[i] = n < a.Ng;
+      const int ho = n / a.Wo, wo = n - ho * a.Wo;
+      ih0[i] = ho * a.sh - a.ph;
+      iw0[i] = wo * a.sw - a.pw;
+    }
+  }
+  __device__ void advance(const KArgs& a) {
+    k += KT;
+    step_rsc(a, KT, r, s, c);
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int ih = ih0[i] + r, iw = iw0[i] + s;
+      const bool ok = col_ok[i] & (k < a.Kg) & ((unsigned)ih < (unsigned)a.H) &
+                      ((unsigned)iw < (unsigned)a.W);
+      const unsigned off = (unsigned)((ih * a.W + iw) * a.C + c) * 4u;
+      v[i] = bload4(xr, ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int n = nc0 + i * NSTEP;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Bs[(4 * k4 + e) * C::BS + n] = v[i][e];
+    }
+  }
+};
+
+// Any layout, any alignment: single elements, indices decomposed per stage.
+template <int LAYOUT, class C, int NT, int KT>
+struct BScalar {
+  static constexpr int NE = C::B_ELEMS;
+  int t_, n0_, kbase;
+  float v[NE];
+
+  __device__ void init(const KArgs&, int t, int n0, int kbeg) { t_ = t; n0_ = n0; kbase = kbeg; }
+  __device__ void advance(const KArgs&) { kbase += KT; }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int e = t_ + i * C::T;
+      const int n = n0_ + e % NT, k = kbase + e / NT;
+      unsigned off = kOOB;
+      if (n < a.Ng && k < a.Kg) {
+        int r, s, c;
+        split_k<LAYOUT>(a, k, r, s, c);
+        int b, pix;
+        if constexpr (LAYOUT == kHWCN) { pix = n / a.N; b = n - pix * a.N; }
+        else { const int hw = a.Ho * a.Wo; b = n / hw; pix = n - b * hw; }
+        const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+        const int ih = ho * a.sh - a.ph + r, iw = wo * a.sw - a.pw + s;
+        if ((unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W) {
+          const int idx = (LAYOUT == kHWCN) ? ((ih * a.W + iw) * a.C + c) * a.N + b
+                                            : ((b * a.C + c) * a.H + ih) * a.W + iw;
+          off = (unsigned)idx * 4u;
+        }
+      }
+      v[i] = bload1(xr, off);
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int e = t_ + i * C::T;
+      Bs[(e / NT) * C::BS + e % NT] = v[i];
+    }
+  }
+};
+
+template <int LAYOUT, int AM, class C, int MT, int KT>
+struct ASel;
+template <class C, int MT, int KT>
+struct ASel<kHWCN, kAVecM, C, MT, KT> { using type = AVecM<C, MT, KT>; };
+template <class C, int MT, int KT>
+struct ASel<kNCHW, kAVecK, C, MT, KT> { using type = AVecK<C, MT, KT>; };
+template <int LAYOUT, class C, int MT, int KT>
+struct ASel<LAYOUT, kAScalar, C, MT, KT> { using type = AScalar<LAYOUT, C, MT, KT>; };
+
+template <int LAYOUT, int BM, class C, int NT, int KT>
+struct BSel;
+template <class C, int NT, int KT>
+struct BSel<kHWCN, kBVecN, C, NT, KT> { using type = BVecN<C, NT, KT>; };
+template <class C, int NT, int KT>
+struct BSel<kHWCN, kBVecNTap, C, NT, KT> { using type = BVecNTap<C, NT, KT>; };
+template <class C, int NT, int KT>
+struct BSel<kHWCN, kBVecC, C, NT, KT> { using type = BVecC<C, NT, KT>; };
+template <int LAYOUT, class C, int NT, int KT>
+struct BSel<LAYOUT, kBScalar, C, NT, KT> { using type = BScalar<LAYOUT, C, NT, KT>; };
+
+// --------------------------------------------------------- MFMA on a stage
+// 32x32x2 fp32 MFMA operand layout: lane (hh, q) = (lane / 32, lane % 32)
+// supplies A[row q][k = hh] and B[k = hh][column q].
+template <class C, int KT>
+__device__ __forceinline__ void mma_stage(floatx16 (&acc)[C::TM][C::TN], const float* As,
+                                          const float* Bs, int wm, int wn, int hh, int q) {
+  const float* Ac = As + wm * C::WTM + q;
+  const float* Bc = Bs + wn * C::WTN + q;
+  float av[KT / 2][C::TM], bv[KT / 2][C::TN];
+#pragma unroll
+  for (int kk = 0; kk < KT / 2; ++kk) {
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) av[kk][i] = Ac[(2 * kk + hh) * C::AS + i * 32];
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) bv[kk][j] = Bc[(2 * kk + hh) * C::BS + j * 32];
+  }
+#pragma unroll
+  for (int kk = 0; kk < KT / 2; ++kk)
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
+}
+
+// ------------------------------------------------------------------ kernel
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_f32(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  const int t = threadIdx.x;
+
+  // Work-group -> tile.  Consecutive hardware work-group ids go to different
+  // XCDs (round robin over 8); remap so that each XCD receives a contiguous
+  // run of tiles, which share filter and halo input rows in its L2.
+  int L = blockIdx.x;
+  if (a.xcd_remap) {
+    const int G = gridDim.x, q8 = G >> 3, r8 = G & 7, xcd = L & 7, loc = L >> 3;
+    L = (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
+  }
+  const int tm = L % a.tiles_m;
+  const int rest = L / a.tiles_m;
+  const int tn = rest % a.tiles_n;
+  const int ks = rest / a.tiles_n;
+  const int m0 = tm * MT, n0 = tn * NT;
+  const int kt0 = ks * a.kps;
+  const int nk = min(a.kps, a.k_tiles - kt0);
+  const int kbeg = kt0 * KT;
+
+  float* const As0 = lds;
+  float* const Bs0 = lds + 2 * C::A_STAGE;
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+
+  typename ASel<LAYOUT, AM, C, MT, KT>::type al;
+  typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
+  al.init(a, t, m0, kbeg);
+  bl.init(a, t, n0, kbeg);
+
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave % WM, wn = wave / WM;
+  const int hh = lane >> 5, q = lane & 31;
+
+  floatx16 acc[C::TM][C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  if (nk > 0) {
+    al.load(a, wr);
+    bl.load(a, xr);
+    al.store(As0);
+    bl.store(Bs0);
+    __syncthreads();
+    // Steady state: the loads of stage it+1 are issued before the MFMAs of
+    // stage it and land in the other LDS buffer after them; one barrier per
+    // stage.  Buffer cur^1 was last read in iteration it-1, which every wave
+    // finished before the barrier that ended it.  Stages alternate between
+    // the two buffers, so the loop is unrolled by two to make the buffer
+    // offsets compile-time constants.
+    auto step = [&](auto cur_c) {
+      constexpr int CUR = decltype(cur_c)::value;
+      al.advance(a);
+      bl.advance(a);
+      al.load(a, wr);
+      bl.load(a, xr);
+      // keep the global loads ahead of the MFMAs (the scheduler would
+      // otherwise sink them next to their LDS stores and expose their latency)
+      __builtin_amdgcn_sched_barrier(0);
+      mma_stage<C, KT>(acc, As0 + CUR * C::A_STAGE, Bs0 + CUR * C::B_STAGE, wm, wn, hh, q);
+      __builtin_amdgcn_sched_barrier(0);
+      al.store(As0 + (CUR ^ 1) * C::A_STAGE);
+      bl.store(Bs0 + (CUR ^ 1) * C::B_STAGE);
+      __syncthreads();
+    };
+    using B0 = std::integral_constant<int, 0>;
+    using B1 = std::integral_constant<int, 1>;
+    int it = 0;
+    for (; it + 2 <= nk - 1; it += 2) {
+      step(B0{});
+      step(B1{});
+    }
+    if (it < nk - 1) {
+      step(B0{});
+      ++it;
+    }
+    const int last = it & 1;
+    mma_stage<C, KT>(acc, As0 + last * C::A_STAGE, Bs0 + last * C::B_STAGE, wm, wn, hh, q);
+  }
+
+  // Epilogue, straight from the accumulators.  32x32 accumulator layout:
+  // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
+  // Output element (m, n) sits at colbase(n) + m*mstride in either layout.
+  float* const out = a.out + (long long)ks * a.out_split_stride;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int n = n0 + wn * C::WTN + j * 32 + q;
+    if (n >= a.Ng) continue;
+    int colbase;
+    if constexpr (LAYOUT == kHWCN) {
+      const int pix = n / a.N, b = n - pix * a.N;
+      colbase = pix * a.K * a.N + b;
+    } else {
+      const int hw = a.Ho * a.Wo, b = n / hw, pix = n - b * hw;
+      colbase = b * a.K * hw + pix;
+    }
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
+        if (a.e_mode == kEVecM) {
+          // four consecutive output channels, contiguous when mstride == 1
+          if (row0 < a.Mg)
+            st4(out + colbase + row0,
+                f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]});
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (row0 + e < a.Mg) out[colbase + (row0 + e) * a.mstride] = acc[i][j][4 * g + e];
+        }
+      }
+  }
+}
+
+template <int LAYOUT, int AM, int BM, int TI>
+constexpr KernelFn kernel_at() {
+  constexpr TileDesc d = kTiles[TI];
+  return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn>;
+}
+
+template <int LAYOUT, int AM, int BM, int... TI>
+KernelFn pick_tile(int tile, std::integer_sequence<int, TI...>) {
+  KernelFn fn = nullptr;
+  ((fn = (tile == TI ? kernel_at<LAYOUT, AM, BM, TI>() : fn)), ...);
+  return fn;
+}
+
+template <int LAYOUT, int AM, int BM>
+KernelFn kernel_for_tile(int tile) {
+  if (tile < 0 || tile >= kNumTiles) return nullptr;
+  return pick_tile<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles>{});
+}
+
+}  // namespace mg3m

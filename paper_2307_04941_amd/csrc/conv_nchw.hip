@@ -1,0 +1,14 @@
+// Instantiations of the implicit-GEMM kernel for the NCHW layout (Eq. 1's
+// index order): vectorised or element-wise filter loads, element-wise
+// input-patch gathers, one per tile shape.
+#include "conv_kernel.h"
+
+namespace mg3m {
+
+KernelFn conv_kernel_nchw(int variant, int tile) {
+  if (variant == kVarNchwVecA) return kernel_for_tile<kNCHW, kAVecK, kBScalar>(tile);
+  if (variant == kVarNchwScalar) return kernel_for_tile<kNCHW, kAScalar, kBScalar>(tile);
+  return nullptr;
+}
+
+}  // namespace mg3m

@@ -10,16 +10,32 @@ namespace mg3m {
 
 enum Layout : int { kHWCN = 0, kNCHW = 1 };
 
-// Filter (A operand) loader: 16-byte vectors along OC (HWCN, K % 4 == 0),
-// along the reduction axis (NCHW, Kg % 4 == 0), or single elements.
+// Operand loader variants.  Each is a separate kernel instantiation, so the
+// main loop carries no run-time branch on the mode.
+//   A (filter):        kAVecM   16-byte vectors along OC   (HWCN, K % 4 == 0)
+//                      kAVecK   16-byte vectors along Kg   (NCHW, Kg % 4 == 0)
+//                      kAScalar single elements            (any)
+//   B (input patches): kBVecNTap 16-byte vectors along the batch, one filter tap
+//                               per staged slab (HWCN, N % 4 == 0, C % kt == 0)
+//                      kBVecN   16-byte vectors along the batch (HWCN, N % 4 == 0)
+//                      kBVecC   16-byte vectors along channels  (HWCN, N == 1, C % 4 == 0)
+//                      kBScalar single elements                 (any)
 enum AMode : int { kAVecM = 0, kAVecK = 1, kAScalar = 2 };
-// Input-patch (B operand) gather: 16-byte vectors along the batch
-// (HWCN, N % 4 == 0), along channels (HWCN, N == 1, C % 4 == 0), or single
-// elements (any layout).
-enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kNumBModes = 3 };
-// Epilogue store: 16-byte vectors along Ng (contiguous output runs of 4),
-// along OC (HWCN, N == 1, K % 4 == 0), or single elements.
-enum EMode : int { kEVecN = 0, kEVecM = 1, kEScalar = 2 };
+enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3 };
+// The loader pairs that are instantiated.
+enum Variant : int {
+  kVarHwcnVecN = 0,     // HWCN, A vec-M, B vec-N
+  kVarHwcnVecC = 1,     // HWCN, A vec-M, B vec-C
+  kVarHwcnVecA = 2,     // HWCN, A vec-M, B scalar
+  kVarHwcnScalar = 3,   // HWCN, A scalar, B scalar
+  kVarNchwVecA = 4,     // NCHW, A vec-K, B scalar
+  kVarNchwScalar = 5,   // NCHW, A scalar, B scalar
+  kVarHwcnVecNTap = 6,  // HWCN, A vec-M, B vec-N with one tap per slab (the tuned path)
+  kNumVariants = 7
+};
+// Epilogue store: single elements, or 16-byte vectors of four consecutive
+// output channels (HWCN with N == 1 and K % 4 == 0, where they are contiguous).
+enum EMode : int { kEElem = 0, kEVecM = 1 };
 
 struct ConvShape {
   int N, C, H, W, K, R, S;
@@ -31,37 +47,48 @@ struct ConvShape {
 
 // A kernel tile shape: one work-group computes an mt x nt block of the
 // output matrix, stepping the reduction kt at a time, with wm x wn waves.
+// regs and eff feed the planner's cost model: regs is the per-lane register
+// count (VGPR + AGPR) of the tuned loader variant as compiled for gfx950, eff
+// the fraction of the fp32 MFMA peak the tile sustains on MI355X when a layer
+// keeps every CU full (measured over the VGG-16, ResNet-50 and AlexNet layer
+// catalogues; 75th percentile over layers with at least 12 rounds of
+// work-groups).
 struct TileDesc {
   int mt, nt, kt, wm, wn;
+  int regs;
+  double eff;
 };
 
-// The tile menu.  Every entry is instantiated for each layout / loader mode.
-constexpr int kNumTiles = 10;
+// The tile menu.  Every entry is instantiated for every loader variant.
+constexpr int kNumTiles = 13;
 inline constexpr TileDesc kTiles[kNumTiles] = {
-    {128, 128, 16, 2, 2},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4},    // 1: four waves sharing one filter tile (TB(1,8)-like)
-    {256, 64, 16, 4, 1},    // 2: four waves sharing one patch tile
-    {64, 128, 16, 1, 2},    // 3
-    {128, 64, 16, 2, 1},    // 4
-    {64, 64, 16, 1, 1},     // 5: one wave per work-group (TB(1,1)-like)
-    {32, 128, 16, 1, 2},    // 6
-    {32, 64, 16, 1, 1},     // 7
-    {128, 32, 16, 2, 1},    // 8
-    {64, 32, 16, 1, 1},     // 9
+    {128, 128, 16, 2, 2, 136, 0.704},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
+    {64, 256, 16, 1, 4, 136, 0.797},    // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {256, 64, 16, 4, 1, 144, 0.837},    // 2: four waves sharing one patch tile
+    {64, 128, 16, 1, 2, 144, 0.639},    // 3
+    {128, 64, 16, 2, 1, 144, 0.642},    // 4
+    {64, 64, 16, 1, 1, 146, 0.653},     // 5: one wave per work-group (TB(1,1)-like)
+    {32, 128, 16, 1, 2, 104, 0.708},    // 6
+    {32, 64, 16, 1, 1, 104, 0.650},     // 7
+    {128, 32, 16, 2, 1, 104, 0.736},    // 8
+    {64, 32, 16, 1, 1, 104, 0.662},     // 9
+    {256, 128, 16, 4, 2, 130, 0.790},   // 10: eight waves
+    {128, 256, 16, 2, 4, 130, 0.770},   // 11: eight waves
+    {128, 128, 32, 2, 2, 192, 0.799},   // 12: deeper reduction step
 };
 
 // LDS row strides (floats) of the staged operand tiles.  The two half-waves of
 // an MFMA operand read hit rows k and k+1; a stride of 32 (mod 64) floats keeps
 // them on disjoint banks.
 constexpr int lds_row_stride(int dim) { return dim % 64 == 0 ? dim + 32 : dim; }
-constexpr int lds_c_stride(int nt) { return nt + 8; }   // epilogue staging
-// LDS bytes per work-group: two stages of A and B tiles, reused for the
-// epilogue's output tile.
+// LDS bytes per work-group: two stages of the A and B tiles.
 constexpr int lds_bytes_for(const TileDesc& t) {
-  const int ab = 2 * t.kt * lds_row_stride(t.mt) + 2 * t.kt * lds_row_stride(t.nt);
-  const int c = t.mt * lds_c_stride(t.nt);
-  return 4 * (ab > c ? ab : c);
+  return 4 * (2 * t.kt * lds_row_stride(t.mt) + 2 * t.kt * lds_row_stride(t.nt));
 }
+
+// Largest tensor the kernels address: byte offsets are 32-bit and 0xFFFFFFC0
+// is reserved as the out-of-range offset that reads as zero.
+constexpr long long kMaxTensorBytes = 0xFFFFFFC0LL;
 
 struct Plan {
   int layout;
@@ -73,6 +100,7 @@ struct Plan {
   int tiles_m, tiles_n;
   long long grid;
   int a_mode, b_mode, e_mode;
+  int variant;
   int xcd_remap;
   size_t ws_bytes;
   int lds_bytes;
@@ -85,11 +113,13 @@ struct KArgs {
   const float* x;
   const float* w;
   float* out;               // y, or the split-K workspace
+  unsigned x_bytes, w_bytes;
   int N, C, H, W, K, R, S;
   int sh, sw, ph, pw, Ho, Wo;
   int Mg, Ng, Kg;
   int tiles_m, tiles_n, kps, k_tiles;
-  int a_mode, e_mode, xcd_remap;
+  int e_mode, xcd_remap;
+  int mstride;              // output elements between output channels m and m+1
   long long out_split_stride;   // elements between split-K partials
 };
 
@@ -101,7 +131,16 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
               Plan* p, std::string* err);
 std::string plan_to_string(const ConvShape& s, const Plan& p);
 
-// Kernel launchers (conv_igemm.hip).
+// Kernel entry points by (variant, tile): conv_hwcn_*.hip, conv_nchw.hip.
+using KernelFn = void (*)(KArgs);
+KernelFn conv_kernel_hwcn_vecn(int tile);
+KernelFn conv_kernel_hwcn_vecn_tap(int tile);
+KernelFn conv_kernel_hwcn_vecc(int tile);
+KernelFn conv_kernel_hwcn_veca(int tile);
+KernelFn conv_kernel_hwcn_scalar(int tile);
+KernelFn conv_kernel_nchw(int variant, int tile);
+
+// Kernel launchers (conv_launch.hip).
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
 int launch_splitk_reduce(const float* ws, float* y, long long elems, int split, bool vec4,
                          void* stream, std::string* err);

@@ -26,41 +26,42 @@ namespace {
 constexpr int kCUs = 256;                    // MI355X: 8 XCDs x 32 CUs
 constexpr double kClockHz = 2.4e9;
 constexpr double kFlopPerClkCU = 256.0;      // fp32 MFMA: 4 SIMDs x 64 flop/clk
-constexpr double kHbmBytesPerS = 8.0e12;
 constexpr int kLdsBytesPerCU = 160 * 1024;
-constexpr double kLaunchUs = 3.0;            // per kernel launch on the stream
-constexpr double kWgOverheadUs = 1.2;        // prologue + epilogue per work-group round
+constexpr int kRegsPerLane = 512;            // unified VGPR + AGPR file per SIMD lane
+constexpr int kMaxWavesPerSimd = 8;
+// Constants fitted to kernel timings on MI355X (see the tile menu): a layer's
+// streaming rate, the cost of one kernel launch on the stream, the fixed cost
+// of each round of resident work-groups (prologue loads, epilogue stores), and
+// how MFMA utilisation falls when fewer than ~2 waves per SIMD are resident.
+constexpr double kStreamBytesPerS = 5.0e12;
+constexpr double kLaunchUs = 4.0;
+constexpr double kRoundUs = 2.0;
+constexpr double kUtilBase = 0.4, kUtilPerWave = 0.3;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
-// Rough per-wave register use, to estimate work-groups resident per CU.
-int regs_per_lane(const TileDesc& t) {
-  const int T = t.wm * t.wn * 64;
-  const int acc = (t.mt / t.wm / 32) * (t.nt / t.wn / 32) * 16;
-  const int stage = (t.kt * t.mt + t.kt * t.nt) / T;
-  return acc + stage + 56;
-}
-
+// Work-groups of this tile resident on one CU, limited by LDS and registers.
 int resident_wgs(const TileDesc& t) {
-  const int lds = lds_bytes_for(t);
-  const int by_lds = std::max(1, kLdsBytesPerCU / lds);
-  const int regs = (regs_per_lane(t) + 7) / 8 * 8;
-  const int waves_per_simd = std::max(1, std::min(8, 512 / regs));
-  const int by_regs = std::max(1, (4 * waves_per_simd) / (t.wm * t.wn));
-  return std::min(by_lds, by_regs);
+  const int waves = t.wm * t.wn;
+  const int regs = (t.regs + 7) / 8 * 8;
+  const int waves_per_simd = std::min(kMaxWavesPerSimd, kRegsPerLane / regs);
+  const int by_regs = std::max(1, 4 * waves_per_simd / waves);
+  const int by_lds = std::max(1, kLdsBytesPerCU / lds_bytes_for(t));
+  return std::min(by_regs, by_lds);
 }
 
-// Fraction of MFMA peak a wave sustains with this register block, before
-// occupancy effects: larger blocks read fewer operands per MFMA.
-double block_efficiency(const TileDesc& t) {
-  const int wtm = t.mt / t.wm, wtn = t.nt / t.wn;
-  if (wtm >= 64 && wtn >= 64) return 0.80;
-  if (wtm >= 64 || wtn >= 64) return 0.65;
-  return 0.45;
+// Relative speed of the loader variants against the tuned one.
+double variant_factor(int variant) {
+  switch (variant) {
+    case kVarHwcnVecNTap: return 1.0;
+    case kVarHwcnVecN: return 0.85;
+    case kVarHwcnVecC: case kVarHwcnVecA: case kVarNchwVecA: return 0.7;
+    default: return 0.5;
+  }
 }
 
 struct Override {
-  int mt = 0, nt = 0, split = 0, xcd = -1;
+  int mt = 0, nt = 0, kt = 0, split = 0, xcd = -1;
 };
 
 int parse_override(const char* text, Override* o, std::string* err) {
@@ -102,6 +103,13 @@ int parse_override(const char* text, Override* o, std::string* err) {
         return MG3M_ERR_PLAN;
       }
       o->split = (int)v;
+    } else if (key == "kt") {
+      long v = std::strtol(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || (v != 16 && v != 32)) {
+        *err = "plan override: kt must be 16 or 32";
+        return MG3M_ERR_PLAN;
+      }
+      o->kt = (int)v;
     } else if (key == "xcd") {
       if (val != "0" && val != "1") {
         *err = "plan override: xcd must be 0 or 1";
@@ -135,24 +143,31 @@ void shape_plan(const ConvShape& s, int tile, int split_req, Plan* p) {
   p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
   p->ws_bytes = p->split > 1 ? (size_t)p->split * (size_t)(s.Mg * s.Ng) * sizeof(float) : 0;
 
-  // Cost model.  The busiest CU runs ceil(grid / 256) work-groups; each costs
-  // its padded flops at the block efficiency, degraded when fewer than two
-  // waves per SIMD are resident to hide latency.
-  const double wg_flops = 2.0 * t.mt * t.nt * (double)t.kt * p->kps;
-  const long long per_cu = cdiv(p->grid, kCUs);
+  p->est_us = 0.0;
+}
+
+// The selector's predicted time for a plan (microseconds).  The busiest CU
+// runs ceil(grid / 256) work-groups, each costing its padded MFMA flops at
+// the tile's measured efficiency, scaled down when that CU holds too few
+// waves to hide latency, plus a fixed cost per round of resident
+// work-groups; a layer cannot beat streaming its tensors once; split-K adds
+// its partials' traffic and a second launch.
+double predict_us(const ConvShape& s, const Plan& p) {
+  const TileDesc& t = p.t;
+  const long long per_cu = cdiv(p.grid, kCUs);
   const int occ = resident_wgs(t);
-  const double waves_per_simd =
-      std::min<double>(occ, (double)per_cu) * t.wm * t.wn / 4.0;
-  const double lat = waves_per_simd >= 2.0 ? 1.0 : (waves_per_simd >= 1.0 ? 0.8 : 0.55);
-  const double eff = block_efficiency(t) * lat;
-  const double t_comp = per_cu * wg_flops / (kFlopPerClkCU * kClockHz * eff) * 1e6;
-  const double out_bytes = 4.0 * (double)s.Mg * s.Ng;
-  const double in_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
-  const double t_mem = (in_bytes + out_bytes) / kHbmBytesPerS * 1e6;
-  const double rounds = (double)cdiv(per_cu, occ);
-  double est = std::max(t_comp, t_mem) + kLaunchUs + rounds * kWgOverheadUs;
-  if (p->split > 1) est += (p->split + 1) * out_bytes / kHbmBytesPerS * 1e6 + kLaunchUs + 2.0;
-  p->est_us = est;
+  const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
+  const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
+  const double eff = t.eff * variant_factor(p.variant) * util;
+  const double wg_flops = 2.0 * t.mt * t.nt * (double)t.kt * p.kps;
+  const double t_comp = (double)per_cu * wg_flops / (kFlopPerClkCU * kClockHz * eff) * 1e6 +
+                        (double)cdiv(per_cu, occ) * kRoundUs;
+  const double y_bytes = 4.0 * (double)s.Mg * (double)s.Ng;
+  const double xw_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
+  const double t_mem = (xw_bytes + y_bytes * p.split) / kStreamBytesPerS * 1e6;
+  double est = std::max(t_comp, t_mem) + kLaunchUs;
+  if (p.split > 1) est += (p.split + 1) * y_bytes / kStreamBytesPerS * 1e6 + kLaunchUs;
+  return est;
 }
 
 }  // namespace
@@ -186,14 +201,40 @@ int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride, int 
   s->Ng = (long long)N * s->Ho * s->Wo;
   s->Kg = (long long)C * R * S;
   // int32 index arithmetic in the kernels, with head-room for a tile past the end
-  const long long lim = 0x7fffffffLL - 1024;
+  // 32-bit byte offsets in the kernels' buffer loads
+  const long long lim = kMaxTensorBytes / 4;
   const long long xe = (long long)N * C * H * W, we = (long long)K * C * R * S,
                   ye = (long long)N * K * s->Ho * s->Wo;
-  if (xe >= lim || we >= lim || ye >= lim || s->Ng >= lim || s->Kg >= lim) {
-    *err = "a tensor has (about) 2^31 elements or more";
+  if (xe > lim || we > lim || ye > lim) {
+    *err = "a tensor is larger than 4 GiB - 64 bytes (the kernels use 32-bit byte offsets)";
     return MG3M_ERR_TOO_LARGE;
   }
   return MG3M_OK;
+}
+
+// Loader variant and epilogue mode for a plan whose tile is already set.
+void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
+  if (s.layout == kHWCN) {
+    if (s.K % 4 == 0 && w16) {
+      p->a_mode = kAVecM;
+      if (s.N % 4 == 0 && x16 && s.C % p->t.kt == 0) p->b_mode = kBVecNTap, p->variant = kVarHwcnVecNTap;
+      else if (s.N % 4 == 0 && x16) p->b_mode = kBVecN, p->variant = kVarHwcnVecN;
+      else if (s.N == 1 && s.C % 4 == 0 && x16) p->b_mode = kBVecC, p->variant = kVarHwcnVecC;
+      else p->b_mode = kBScalar, p->variant = kVarHwcnVecA;
+    } else {
+      p->a_mode = kAScalar;
+      p->b_mode = kBScalar;
+      p->variant = kVarHwcnScalar;
+    }
+  } else {
+    p->b_mode = kBScalar;
+    if (s.Kg % 4 == 0 && w16) p->a_mode = kAVecK, p->variant = kVarNchwVecA;
+    else p->a_mode = kAScalar, p->variant = kVarNchwScalar;
+  }
+  // Four consecutive output channels are contiguous only in HWCN with N == 1;
+  // the split-K workspace is 256-byte aligned and has the output's layout.
+  const bool out16 = p->split > 1 ? true : y16;
+  p->e_mode = (s.layout == kHWCN && s.N == 1 && s.K % 4 == 0 && out16) ? kEVecM : kEElem;
 }
 
 int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16, bool y16,
@@ -207,11 +248,16 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
   const int splits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
   for (int ti = 0; ti < kNumTiles; ++ti) {
     if (o.mt && !(kTiles[ti].mt == o.mt && kTiles[ti].nt == o.nt)) continue;
+    // a forced tile without a depth means the default depth of 16
+    if ((o.kt || o.mt) && kTiles[ti].kt != (o.kt ? o.kt : 16)) continue;
     for (int sp : splits) {
       if (o.split && sp != 1) break;
       Plan c{};
       shape_plan(s, ti, o.split ? o.split : sp, &c);
       if (!o.split && c.split != sp) continue;        // duplicate after clamping
+      choose_modes(s, x16, w16, y16, &c);
+      c.est_us = predict_us(s, c);
+      // ties: fewer splits (less traffic), then the larger tile
       bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
                     (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
                      (c.split < best_plan.split ||
@@ -223,37 +269,21 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
     }
   }
   if (best < 0) {
-    *err = "plan override: no kernel tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt);
+    *err = "plan override: no kernel tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
+           (o.kt ? " with kt=" + std::to_string(o.kt) : std::string());
     return MG3M_ERR_PLAN;
   }
   *p = best_plan;
-  p->xcd_remap = o.xcd < 0 ? 1 : o.xcd;
-
-  // Loader and epilogue modes.
-  if (s.layout == kHWCN) {
-    p->a_mode = (s.K % 4 == 0 && w16) ? kAVecM : kAScalar;
-    if (s.N % 4 == 0 && x16) p->b_mode = kBVecN;
-    else if (s.N == 1 && s.C % 4 == 0 && x16) p->b_mode = kBVecC;
-    else p->b_mode = kBScalar;
-  } else {
-    p->a_mode = (s.Kg % 4 == 0 && w16) ? kAVecK : kAScalar;
-    p->b_mode = kBScalar;
-  }
-  const bool out16 = p->split > 1 ? true : y16;   // the workspace is 256-byte aligned
-  if (s.layout == kHWCN) {
-    if (s.N % 4 == 0 && out16) p->e_mode = kEVecN;
-    else if (s.N == 1 && s.K % 4 == 0 && out16) p->e_mode = kEVecM;
-    else p->e_mode = kEScalar;
-  } else {
-    p->e_mode = ((long long)s.Ho * s.Wo % 4 == 0 && out16) ? kEVecN : kEScalar;
-  }
+  // Measured on MI355X: grouping tiles per XCD never helped these shapes and
+  // cost up to 5% with 64-row tiles, so it is off unless asked for.
+  p->xcd_remap = o.xcd < 0 ? 0 : o.xcd;
   return MG3M_OK;
 }
 
 std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* an[] = {"vec_m", "vec_k", "scalar"};
-  static const char* bn[] = {"vec_n", "vec_c", "scalar"};
-  static const char* en[] = {"vec_n", "vec_m", "scalar"};
+  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap"};
+  static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
                 "tile=%dx%d,waves=%dx%d,kt=%d,split=%d,grid=%lld,tiles=%dx%d,k_tiles=%d,"

@@ -134,7 +134,7 @@ def test_plans_for_every_catalogue_layer():
 def test_plans_random_grid_and_overrides():
     rng = np.random.Generator(np.random.PCG64(2))
     tiles = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x128", "32x64",
-             "128x32", "64x32"]
+             "128x32", "64x32", "256x128", "128x256", "128x128,kt=32"]
     for _ in range(200):
         N = int(rng.integers(1, 65))
         C, K = (int(v) for v in rng.integers(1, 600, 2))
@@ -148,7 +148,8 @@ def test_plans_random_grid_and_overrides():
         t = str(rng.choice(tiles))
         sp = int(rng.integers(1, 20))
         p = _check_plan(shape, "NCHW", f"tile={t},split={sp}")
-        assert f"{p['mt']}x{p['nt']}" == t
+        assert f"{p['mt']}x{p['nt']}" == t.split(",")[0]
+        assert p["kt"] == (32 if "kt=32" in t else 16)
         assert p["split"] <= sp
 
 
