@@ -39,6 +39,14 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+def kernel_name(plan) -> str:
+    """The main kernel's symbol as rocprofv3 prints it (its template arguments:
+    layout, filter loader, patch loader, tile rows, columns, depth, waves)."""
+    return (f"void mg3m::conv_igemm_f32<{plan['layout']}, {plan['a_mode']}, {plan['b_mode']}, "
+            f"{plan['mt']}, {plan['nt']}, {plan['kt']}, {plan['waves_m']}, {plan['waves_n']}>"
+            f"(mg3m::KArgs)")
+
+
 def layer_flops(L, Ho, Wo) -> float:
     return 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo
 
@@ -144,10 +152,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    def new_event():
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(stream)            # creates the underlying hipEvent_t
+        return ev
+
     def one_step(evs=None):
         for j, ((L, Ho, Wo), (xd, wd, yd)) in enumerate(zip(layers, dev_bufs)):
             if evs is not None:
                 evs[j][0].record(stream)
+                mg3m.mg3m_time_next_kernel(evs[j][2], evs[j][3])
             if args.plan:
                 mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", plan=args.plan, out=yd)
             else:
@@ -160,9 +174,10 @@ def main():
         one_step()
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly K steps
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in layers] for _ in range(args.steps)]
+    # ---- timed region: exactly K steps.  Per layer and step: events around
+    # the C-ABI call, and (through mg3m_time_next_kernel) around its main
+    # convolution kernel alone, recorded on the stream the kernel runs on.
+    evs = [[tuple(new_event() for _ in range(4)) for _ in layers] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -176,6 +191,7 @@ def main():
     per_layer = []
     for j, (L, Ho, Wo) in enumerate(layers):
         us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j][1]) for k in range(args.steps)])) * 1e3
+        kus = float(np.mean([evs[k][j][2].elapsed_time(evs[k][j][3]) for k in range(args.steps)])) * 1e3
         fl = layer_flops(L, Ho, Wo)
         by = layer_alg_bytes(L, Ho, Wo)
         plan = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad,
@@ -184,35 +200,38 @@ def main():
         attainable = min(PEAK_TFLOPS, ai * HBM_GBS / 1e3)
         per_layer.append({
             "layer": L.name, "N": L.N, "C": L.C, "H": L.H, "K": L.K, "R": L.R, "stride": L.stride,
-            "pad": L.pad, "us": round(us, 2), "tflops": round(fl / us / 1e6, 2),
+            "pad": L.pad, "us": round(us, 2), "kernel_us": round(kus, 2),
+            "tflops": round(fl / us / 1e6, 2),
             "pct_peak": round(100 * fl / us / 1e6 / PEAK_TFLOPS, 1),
             "pct_roofline": round(100 * fl / us / 1e6 / attainable, 1),
             "bound": "mfma" if ai * HBM_GBS / 1e3 >= PEAK_TFLOPS else "hbm",
-            "tile": f"{plan['mt']}x{plan['nt']}", "split": plan["split"], "grid": plan["grid"],
+            "tile": f"{plan['mt']}x{plan['nt']}x{plan['kt']}", "split": plan["split"],
+            "grid": plan["grid"], "kernel": kernel_name(plan),
             "flops": fl, "alg_bytes": by,
         })
 
-    # dominant kernel: the (tile, split) plan with the largest share of step time
+    # dominant kernel: the instantiation with the largest share of kernel time
     groups = {}
     for r in per_layer:
-        key = (r["tile"], r["split"])
-        g = groups.setdefault(key, {"us": 0.0, "flops": 0.0, "n": 0})
-        g["us"] += r["us"]
+        g = groups.setdefault(r["kernel"], {"us": 0.0, "flops": 0.0, "n": 0, "layers": []})
+        g["us"] += r["kernel_us"]
         g["flops"] += r["flops"]
         g["n"] += 1
-    (dtile, dsplit), dg = max(groups.items(), key=lambda kv: kv[1]["us"])
+        g["layers"].append(r["layer"])
+    dname, dg = max(groups.items(), key=lambda kv: kv[1]["us"])
     achieved = dg["flops"] / dg["us"] / 1e6
     traffic = None
-    prof = os.path.join(ROOT, "profiles", "traffic_vgg16_n64.json")
-    if os.path.exists(prof) and args.workload == "vgg16_n64" and not args.plan:
+    prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    if os.path.exists(prof) and not args.plan:
         with open(prof) as f:
             t = json.load(f)
-        if t.get("kernel_digest") == kernel_source_digest() and t.get("tile") == dtile:
+        if t.get("kernel_digest") == kernel_source_digest() and t.get("kernel") == dname:
             traffic = t.get("hbm_bytes_per_launch")
     roofline = {
         "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
         "frac": round(achieved / PEAK_TFLOPS, 4), "traffic": traffic,
-        "kernel": f"conv_igemm_f32 tile {dtile} split {dsplit}",
+        "kernel": dname,
+        "layers": dg["layers"],
         "launches_per_step": dg["n"],
         "alg_flops_per_launch": dg["flops"] / dg["n"],
         "avg_launch_us": round(dg["us"] / dg["n"], 2),

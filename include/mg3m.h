@@ -127,11 +127,24 @@ typedef struct mg3m_plan_info {
     int lds_bytes;            /* LDS per work-group */
     double pad_efficiency;    /* Mg*Ng*Kg / (padded tile volume), in (0, 1] */
     double est_us;            /* the selector's predicted time */
+    int layout;               /* MG3M_LAYOUT_* */
+    int a_mode, b_mode;       /* operand loader variant of the main kernel (its template arguments) */
+    int e_mode;               /* epilogue store mode */
 } mg3m_plan_info;
 
 int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,
                              int stride, int pad, int layout, const char *plan,
                              mg3m_plan_info *info);
+
+/* Measurement hook for timing the main convolution kernel alone with HIP
+ * events on the stream it runs on.  start and stop are hipEvent_t handles
+ * created by the caller (both non-NULL), or both NULL to clear the hook.  The
+ * next compute call (conv2d_fwd_f32 / _ex) made on the calling host thread
+ * records start on its stream immediately before launching its main kernel
+ * and stop immediately after it -- before any split-K reduction -- and then
+ * clears the hook; a call rejected by validation leaves it set.  Returns
+ * MG3M_OK, or MG3M_ERR_ARG if exactly one handle is NULL. */
+int mg3m_time_next_kernel(void *start, void *stop);
 
 /* Padding overhead of computing an M x N (x C deep) product in whole
  * mt x nt register blocks, as in the remainder analysis of Sec. 4.4.2:

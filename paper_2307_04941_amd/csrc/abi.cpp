@@ -16,6 +16,8 @@
 namespace {
 
 thread_local std::string g_last_error;
+// one-shot kernel timing events (mg3m_time_next_kernel)
+thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
 
 int fail(int status, const std::string& msg) {
   g_last_error = msg;
@@ -86,7 +88,17 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
   a.out_split_stride = s.Mg * s.Ng;
 
   std::string err;
-  rc = mg3m::launch_conv(p, a, stream, &err);
+  hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
+  g_ev_start = g_ev_stop = nullptr;
+  if (ev0 != nullptr) {
+    hipError_t e = hipEventRecord(ev0, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) err = std::string("hipEventRecord: ") + hipGetErrorString(e), rc = MG3M_ERR_HIP;
+  }
+  if (rc == MG3M_OK) rc = mg3m::launch_conv(p, a, stream, &err);
+  if (rc == MG3M_OK && ev1 != nullptr) {
+    hipError_t e = hipEventRecord(ev1, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) err = std::string("hipEventRecord: ") + hipGetErrorString(e), rc = MG3M_ERR_HIP;
+  }
   if (rc == MG3M_OK && p.split > 1) {
     const long long elems = s.Mg * s.Ng;
     rc = mg3m::launch_splitk_reduce(ws, y, elems, p.split, elems % 4 == 0 && aligned(y, 16), stream, &err);
@@ -192,10 +204,20 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     info->Mg = s.Mg; info->Ng = s.Ng; info->Kg = s.Kg;
     info->workspace_bytes = p.ws_bytes; info->lds_bytes = p.lds_bytes;
     info->pad_efficiency = p.pad_eff; info->est_us = p.est_us;
+    info->layout = p.layout; info->a_mode = p.a_mode; info->b_mode = p.b_mode;
+    info->e_mode = p.e_mode;
     return MG3M_OK;
   } catch (...) {
     return fail(MG3M_ERR_HIP, "unknown exception");
   }
+}
+
+int mg3m_time_next_kernel(void* start, void* stop) {
+  g_last_error.clear();
+  if ((start == nullptr) != (stop == nullptr)) return fail(MG3M_ERR_ARG, "give both events or neither");
+  g_ev_start = static_cast<hipEvent_t>(start);
+  g_ev_stop = static_cast<hipEvent_t>(stop);
+  return MG3M_OK;
 }
 
 int mg3m_padding_overhead(int M, int N, int C, int mt, int nt, double* flop_overhead,

@@ -41,6 +41,8 @@ class PlanInfo(ctypes.Structure):
         ("grid", ctypes.c_longlong), ("Mg", ctypes.c_longlong), ("Ng", ctypes.c_longlong),
         ("Kg", ctypes.c_longlong), ("workspace_bytes", ctypes.c_size_t), ("lds_bytes", ctypes.c_int),
         ("pad_efficiency", ctypes.c_double), ("est_us", ctypes.c_double),
+        ("layout", ctypes.c_int), ("a_mode", ctypes.c_int), ("b_mode", ctypes.c_int),
+        ("e_mode", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -67,13 +69,14 @@ def load_library(path: str = LIB_PATH):
     lib.conv2d_fwd_f32_plan_string.argtypes = shape + [cp, ctypes.c_char_p, sz]
     lib.conv2d_fwd_f32_plan_info.argtypes = shape + [cp, ctypes.POINTER(PlanInfo)]
     lib.mg3m_padding_overhead.argtypes = [i] * 5 + [ctypes.POINTER(ctypes.c_double)] * 2
+    lib.mg3m_time_next_kernel.argtypes = [p, p]
     lib.mg3m_status_string.argtypes = [i]
     lib.mg3m_status_string.restype = ctypes.c_char_p
     lib.mg3m_last_error.argtypes = []
     lib.mg3m_last_error.restype = ctypes.c_char_p
     for name in ("conv2d_out_dims", "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
                  "conv2d_fwd_f32_workspace_bytes", "conv2d_fwd_f32_plan_string",
-                 "conv2d_fwd_f32_plan_info", "mg3m_padding_overhead"):
+                 "conv2d_fwd_f32_plan_info", "mg3m_padding_overhead", "mg3m_time_next_kernel"):
         getattr(lib, name).restype = i
     _lib = lib
     return lib
@@ -165,6 +168,16 @@ def conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, stride, pad, layout, plan=None
     _check(load_library().conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, stride, pad,
                                                    _layout(layout), _enc(plan), ctypes.byref(info)))
     return info.as_dict()
+
+
+def mg3m_time_next_kernel(start, stop):
+    """start/stop: torch.cuda.Event objects (already recorded once, so that
+    they exist), raw hipEvent_t handles as ints, or None, None."""
+    def h(e):
+        if e is None or isinstance(e, int):
+            return e
+        return e.cuda_event
+    _check(load_library().mg3m_time_next_kernel(h(start), h(stop)))
 
 
 def mg3m_padding_overhead(M, N, C, mt, nt):

@@ -1,0 +1,153 @@
+"""Summarise rocprofv3 output of a benchmark run into short text files.
+
+    python -m paper_2307_04941_amd.rocprof_summary --workload vgg16_n64 \\
+        --trace DIR --fetch DIR --write DIR --bench-log FILE --copy-mib 1024 --out DIR \\
+        --command-trace "..." --command-fetch "..." --command-write "..."
+
+--trace is a ``rocprofv3 --kernel-trace --stats -f csv`` directory, --fetch and
+--write are ``rocprofv3 --pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` directories of
+runs that also copied --copy-mib MiB once with a plain copy kernel (bench.py
+--copy-mib).  The dominant kernel is the one named in the benchmark's JSON
+line (--bench-log).  HBM bytes per launch of that kernel are its FETCH_SIZE and
+WRITE_SIZE (KiB per dispatch, averaged over its dispatches), each scaled by
+the ratio of the copy's known size to what the same counter read for the copy.
+
+Writes <out>/<kernel tag>_<workload>_kernel_stats.txt,
+<out>/<kernel tag>_<workload>_traffic.txt and <out>/traffic_<workload>.json
+(the figure bench.py reports as roofline.traffic while the library sources
+are unchanged).
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import os
+import sys
+
+
+def _csv(directory: str, suffix: str):
+    files = glob.glob(os.path.join(directory, "**", f"*{suffix}"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no *{suffix} under {directory}")
+    with open(files[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def per_dispatch(directory: str, counter: str):
+    """[(dispatch id, kernel name, value)] for one counter (summed over
+    the instances rocprofv3 reports for a dispatch)."""
+    acc = {}
+    for r in _csv(directory, "counter_collection.csv"):
+        if r["Counter_Name"] != counter:
+            continue
+        key = int(r["Dispatch_Id"])
+        name, val = r["Kernel_Name"], float(r["Counter_Value"])
+        if key in acc:
+            acc[key] = (name, acc[key][1] + val)
+        else:
+            acc[key] = (name, val)
+    return [(k, v[0], v[1]) for k, v in sorted(acc.items())]
+
+
+def copy_scale(rows, known_kib: float):
+    """Known size / counter reading of the plain copy: the largest copy-kernel
+    dispatch of the run (the calibration copy dwarfs the input uploads)."""
+    copies = [v for _, n, v in rows if "copyBuffer" in n and v > 0]
+    if not copies:
+        raise ValueError("no copy kernel dispatch in the counter run")
+    v = max(copies)
+    return known_kib / v, v
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--bench-log", required=True)
+    ap.add_argument("--copy-mib", type=float, required=True)
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--command-trace", default="")
+    ap.add_argument("--command-fetch", default="")
+    ap.add_argument("--command-write", default="")
+    a = ap.parse_args(argv)
+
+    with open(a.bench_log) as f:
+        bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
+    kernel = bench["roofline"]["kernel"]
+    tmpl = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").replace(",", "_")
+    tag = f"conv_igemm_{tmpl}"
+    os.makedirs(a.out, exist_ok=True)
+
+    # ---- kernel statistics
+    stats = _csv(a.trace, "kernel_stats.csv")
+    lines = [f"rocprofv3 kernel statistics, workload {a.workload}",
+             f"command: {a.command_trace}", "",
+             f"{'calls':>6} {'avg_us':>10} {'total_ms':>10} {'pct':>6}  kernel"]
+    dom = None
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.2f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:10.3f} {float(r['Percentage']):6.2f}  {r['Name']}")
+        if r["Name"] == kernel:
+            dom = r
+    roof = bench["roofline"]
+    lines += ["", f"dominant kernel (bench.py): {kernel}",
+              f"  bench.py HIP-event average per launch: {roof['avg_launch_us']} us over its "
+              f"{roof['launches_per_step']} launches per step ({', '.join(roof['layers'])})"]
+    if dom is not None:
+        lines.append(f"  rocprofv3 average per launch:          {float(dom['AverageNs']) / 1e3:.2f} us "
+                     f"over {dom['Calls']} calls (warm-up included)")
+    lines += [f"  achieved {roof['achieved']} TFLOP/s of {roof['peak']} ({100 * roof['frac']:.1f}%)",
+              f"bench.py value: {bench['value']} {bench['unit']} ({bench.get('pct_peak')}% of peak), "
+              f"{bench['ms_per_step']} ms per step, kernel digest {bench['kernel_digest']}"]
+    with open(os.path.join(a.out, f"{tag}_{a.workload}_kernel_stats.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+    # ---- HBM traffic of the dominant kernel
+    known_kib = a.copy_mib * 1024.0
+    fetch = per_dispatch(a.fetch, "FETCH_SIZE")
+    write = per_dispatch(a.write, "WRITE_SIZE")
+    fscale, fcopy = copy_scale(fetch, known_kib)
+    wscale, wcopy = copy_scale(write, known_kib)
+    fk = [v for _, n, v in fetch if n == kernel]
+    wk = [v for _, n, v in write if n == kernel]
+    if not fk or not wk:
+        raise ValueError(f"no dispatch of {kernel} in the counter runs")
+    fetch_b = sum(fk) / len(fk) * fscale * 1024.0
+    write_b = sum(wk) / len(wk) * wscale * 1024.0
+    alg_flops = roof["alg_flops_per_launch"]
+    layers = [r for r in bench["layers"] if r["kernel"] == kernel]
+    alg_bytes = sum(r["alg_bytes"] for r in layers) / len(layers)
+    out = {
+        "workload": a.workload, "kernel": kernel, "kernel_digest": bench["kernel_digest"],
+        "hbm_bytes_per_launch": round(fetch_b + write_b),
+        "fetch_bytes_per_launch": round(fetch_b), "write_bytes_per_launch": round(write_b),
+        "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
+        "copy_bytes": round(known_kib * 1024), "copy_fetch_kib": fcopy, "copy_write_kib": wcopy,
+        "dispatches": len(fk), "alg_bytes_per_launch": round(alg_bytes),
+        "alg_flops_per_launch": alg_flops,
+        "command_fetch": a.command_fetch, "command_write": a.command_write,
+    }
+    with open(os.path.join(a.out, f"traffic_{a.workload}.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    txt = [f"HBM traffic of {kernel}, workload {a.workload}",
+           f"FETCH_SIZE run: {a.command_fetch}", f"WRITE_SIZE run: {a.command_write}", "",
+           f"plain copy of {a.copy_mib:.0f} MiB: FETCH_SIZE read {fcopy:.0f} KiB (scale {fscale:.4f}), "
+           f"WRITE_SIZE read {wcopy:.0f} KiB (scale {wscale:.4f})",
+           f"dominant kernel, {len(fk)} dispatches: FETCH {fetch_b / 1e6:.1f} MB + WRITE {write_b / 1e6:.1f} MB "
+           f"per launch (scaled) = {(fetch_b + write_b) / 1e6:.1f} MB",
+           f"algorithmic bytes per launch (each tensor once): {alg_bytes / 1e6:.1f} MB; "
+           f"measured / algorithmic = {(fetch_b + write_b) / alg_bytes:.2f}",
+           "", "per dispatch (KiB, unscaled): FETCH_SIZE / WRITE_SIZE"]
+    for (d, _, fv), (_, _, wv) in zip([x for x in fetch if x[1] == kernel], [x for x in write if x[1] == kernel]):
+        txt.append(f"  dispatch {d}: {fv:.0f} / {wv:.0f}")
+    with open(os.path.join(a.out, f"{tag}_{a.workload}_traffic.txt"), "w") as f:
+        f.write("\n".join(txt) + "\n")
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    sys.exit(main())
