@@ -62,19 +62,19 @@ struct TileDesc {
 // The tile menu.  Every entry is instantiated for every loader variant.
 constexpr int kNumTiles = 13;
 inline constexpr TileDesc kTiles[kNumTiles] = {
-    {128, 128, 16, 2, 2, 136, 0.704},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 136, 0.797},    // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {128, 128, 16, 2, 2, 136, 0.708},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
+    {64, 256, 16, 1, 4, 136, 0.802},    // 1: four waves sharing one filter tile (TB(1,8)-like)
     {256, 64, 16, 4, 1, 144, 0.837},    // 2: four waves sharing one patch tile
-    {64, 128, 16, 1, 2, 144, 0.639},    // 3
-    {128, 64, 16, 2, 1, 144, 0.642},    // 4
-    {64, 64, 16, 1, 1, 146, 0.653},     // 5: one wave per work-group (TB(1,1)-like)
-    {32, 128, 16, 1, 2, 104, 0.708},    // 6
-    {32, 64, 16, 1, 1, 104, 0.650},     // 7
-    {128, 32, 16, 2, 1, 104, 0.736},    // 8
-    {64, 32, 16, 1, 1, 104, 0.662},     // 9
+    {64, 128, 16, 1, 2, 144, 0.636},    // 3
+    {128, 64, 16, 2, 1, 144, 0.641},    // 4
+    {64, 64, 16, 1, 1, 146, 0.654},     // 5: one wave per work-group (TB(1,1)-like)
+    {32, 128, 16, 1, 2, 104, 0.703},    // 6
+    {32, 64, 16, 1, 1, 104, 0.649},     // 7
+    {128, 32, 16, 2, 1, 104, 0.730},    // 8
+    {64, 32, 16, 1, 1, 104, 0.658},     // 9
     {256, 128, 16, 4, 2, 130, 0.790},   // 10: eight waves
-    {128, 256, 16, 2, 4, 130, 0.770},   // 11: eight waves
-    {128, 128, 32, 2, 2, 192, 0.799},   // 12: deeper reduction step
+    {128, 256, 16, 2, 4, 130, 0.765},   // 11: eight waves
+    {128, 128, 32, 2, 2, 192, 0.795},   // 12: deeper reduction step
 };
 
 // LDS row strides (floats) of the staged operand tiles.  The two half-waves of

@@ -34,9 +34,9 @@ constexpr int kMaxWavesPerSimd = 8;
 // of each round of resident work-groups (prologue loads, epilogue stores), and
 // how MFMA utilisation falls when fewer than ~2 waves per SIMD are resident.
 constexpr double kStreamBytesPerS = 5.0e12;
-constexpr double kLaunchUs = 4.0;
+constexpr double kLaunchUs = 2.0;
 constexpr double kRoundUs = 2.0;
-constexpr double kUtilBase = 0.4, kUtilPerWave = 0.3;
+constexpr double kUtilBase = 0.6, kUtilPerWave = 0.2;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
@@ -245,7 +245,8 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
 
   int best = -1;
   Plan best_plan{};
-  const int splits[] = {1, 2, 3, 4, 6, 8, 12, 16, 24, 32};
+  // the split factors the cost model was calibrated on
+  const int splits[] = {1, 2, 3, 4, 6, 8, 16};
   for (int ti = 0; ti < kNumTiles; ++ti) {
     if (o.mt && !(kTiles[ti].mt == o.mt && kTiles[ti].nt == o.nt)) continue;
     // a forced tile without a depth means the default depth of 16
