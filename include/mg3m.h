@@ -75,15 +75,17 @@ enum mg3m_status {
 int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, int *Wo);
 
 /* y = conv(x, w) in `layout`.  Plan chosen by the per-shape selector.  When
- * the plan splits the Kg reduction (split-K), the partial sums go to a
- * workspace that this call takes from HIP's stream-ordered allocator
- * (hipMallocAsync / hipFreeAsync on `stream`); the splits are summed in a
- * fixed order, so results are deterministic run to run. */
+ * the plan splits the Kg reduction of some output tiles into chunks (all
+ * tiles, or only those left over after whole rounds of work-groups), the
+ * chunks' partial sums go to a workspace that this call takes from HIP's
+ * stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`) and a
+ * second kernel sums them in chunk order, so results are deterministic run
+ * to run. */
 int conv2d_fwd_f32(const float *x, const float *w, float *y,
                    int N, int C, int H, int W, int K, int R, int S,
                    int stride, int pad, int layout, void *stream);
 
-/* Bytes of workspace the plan for this shape needs (0 without split-K).
+/* Bytes of workspace the plan for this shape needs (0 when no tile is split).
  * plan: NULL for the selector's choice, or an override string (below).
  * bytes: host out-parameter. */
 int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S,
@@ -96,8 +98,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  * override.  Override syntax: comma-separated key=value pairs,
  *   tile=<MT>x<NT>   one of the kernel tile shapes (e.g. 128x128, 64x256)
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
- *   split=<n>        split-K factor (1..64; clamped so no split is empty)
- *   xcd=0|1          XCD-aware work-group order (default 0)
+ *   split=<n>        split every tile's reduction into n chunks (1..64, clamped so
+ *                    no chunk is empty; 1 = no split)
+ *   tail=<n>         split only the tiles left over after whole rounds of resident
+ *                    work-groups, into n chunks (2..64); the other tiles run whole
  * e.g. "tile=128x128,kt=32,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
 int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
                       int N, int C, int H, int W, int K, int R, int S,
@@ -117,9 +121,11 @@ int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S,
 typedef struct mg3m_plan_info {
     int mt, nt, kt;           /* work-group tile: rows (OC), columns (B*outH*outW), depth step */
     int waves_m, waves_n;     /* waves per work-group along rows / columns */
-    int split;                /* split-K factor actually used */
+    int split;                /* reduction chunks per split tile (1 = none) */
     int k_tiles;              /* ceil(Kg / kt) */
-    int k_tiles_per_split;
+    int k_tiles_per_split;    /* k-tiles per chunk */
+    int dp_tiles;             /* tiles computed whole */
+    int tail_tiles;           /* tiles split into `split` chunks */
     int tiles_m, tiles_n;     /* ceil(Mg / mt), ceil(Ng / nt) */
     long long grid;           /* work-groups launched by the main kernel */
     long long Mg, Ng, Kg;     /* implicit-GEMM sizes */

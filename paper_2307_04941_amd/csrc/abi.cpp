@@ -60,7 +60,7 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
     return fail(MG3M_ERR_ALIAS, "y overlaps x or w");
 
   float* ws = nullptr;
-  if (p.split > 1) {
+  if (p.tail_tiles > 0) {
     if (own_workspace) {
       hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), p.ws_bytes,
                                     static_cast<hipStream_t>(stream));
@@ -77,15 +77,15 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
   }
 
   mg3m::KArgs a{};
-  a.x = x; a.w = w; a.out = p.split > 1 ? ws : y;
+  a.x = x; a.w = w; a.y = y; a.ws = ws;
   a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb;
   a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
   a.Mg = (int)s.Mg; a.Ng = (int)s.Ng; a.Kg = (int)s.Kg;
-  a.tiles_m = p.tiles_m; a.tiles_n = p.tiles_n; a.kps = p.kps; a.k_tiles = p.k_tiles;
-  a.e_mode = p.e_mode; a.xcd_remap = p.xcd_remap;
+  a.tiles_m = p.tiles_m; a.k_tiles = p.k_tiles;
+  a.dp_tiles = p.dp_tiles; a.tail_tiles = p.tail_tiles > 0 ? p.tail_tiles : 1; a.kps = p.kps;
+  a.e_mode = p.e_mode;
   a.mstride = s.layout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
-  a.out_split_stride = s.Mg * s.Ng;
 
   std::string err;
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
@@ -99,9 +99,15 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
     hipError_t e = hipEventRecord(ev1, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) err = std::string("hipEventRecord: ") + hipGetErrorString(e), rc = MG3M_ERR_HIP;
   }
-  if (rc == MG3M_OK && p.split > 1) {
-    const long long elems = s.Mg * s.Ng;
-    rc = mg3m::launch_splitk_reduce(ws, y, elems, p.split, elems % 4 == 0 && aligned(y, 16), stream, &err);
+  if (rc == MG3M_OK && p.tail_tiles > 0) {
+    mg3m::RArgs r{};
+    r.ws = ws; r.y = y; r.mt = p.t.mt; r.nt = p.t.nt;
+    r.tiles_m = p.tiles_m; r.dp_tiles = p.dp_tiles; r.tail_tiles = p.tail_tiles; r.split = p.split;
+    r.layout = s.layout; r.N = s.N; r.K = s.K; r.HoWo = s.Ho * s.Wo;
+    r.Mg = (int)s.Mg; r.Ng = (int)s.Ng;
+    const bool contiguous4 = s.layout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
+    r.vec4 = contiguous4 && aligned(y, 16);
+    rc = mg3m::launch_tail_reduce(r, stream, &err);
   }
   if (own_workspace && ws != nullptr) {
     hipError_t e = hipFreeAsync(ws, static_cast<hipStream_t>(stream));
@@ -200,6 +206,7 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     info->mt = p.t.mt; info->nt = p.t.nt; info->kt = p.t.kt;
     info->waves_m = p.t.wm; info->waves_n = p.t.wn;
     info->split = p.split; info->k_tiles = p.k_tiles; info->k_tiles_per_split = p.kps;
+    info->dp_tiles = p.dp_tiles; info->tail_tiles = p.tail_tiles;
     info->tiles_m = p.tiles_m; info->tiles_n = p.tiles_n; info->grid = p.grid;
     info->Mg = s.Mg; info->Ng = s.Ng; info->Kg = s.Kg;
     info->workspace_bytes = p.ws_bytes; info->lds_bytes = p.lds_bytes;

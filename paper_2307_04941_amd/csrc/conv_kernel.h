@@ -468,21 +468,27 @@ void conv_igemm_f32(KArgs a) {
 
   const int t = threadIdx.x;
 
-  // Work-group -> tile.  Consecutive hardware work-group ids go to different
-  // XCDs (round robin over 8); remap so that each XCD receives a contiguous
-  // run of tiles, which share filter and halo input rows in its L2.
-  int L = blockIdx.x;
-  if (a.xcd_remap) {
-    const int G = gridDim.x, q8 = G >> 3, r8 = G & 7, xcd = L & 7, loc = L >> 3;
-    L = (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
+  // Work-group -> (tile, range of k-tiles).  Work-groups [0, dp_tiles) each
+  // compute one whole tile; the rest compute one chunk of kps k-tiles of a
+  // tail tile, consecutive work-groups taking different tiles of the same
+  // chunk.
+  const int L = blockIdx.x;
+  int tile, kt0, nk, chunk = 0;
+  const bool partial = L >= a.dp_tiles;
+  if (!partial) {
+    tile = L;
+    kt0 = 0;
+    nk = a.k_tiles;
+  } else {
+    const int j = L - a.dp_tiles;
+    chunk = j / a.tail_tiles;
+    tile = a.dp_tiles + (j - chunk * a.tail_tiles);
+    kt0 = chunk * a.kps;
+    nk = min(a.kps, a.k_tiles - kt0);
   }
-  const int tm = L % a.tiles_m;
-  const int rest = L / a.tiles_m;
-  const int tn = rest % a.tiles_n;
-  const int ks = rest / a.tiles_n;
+  const int tm = tile % a.tiles_m;
+  const int tn = tile / a.tiles_m;
   const int m0 = tm * MT, n0 = tn * NT;
-  const int kt0 = ks * a.kps;
-  const int nk = min(a.kps, a.k_tiles - kt0);
   const int kbeg = kt0 * KT;
 
   float* const As0 = lds;
@@ -552,8 +558,24 @@ void conv_igemm_f32(KArgs a) {
 
   // Epilogue, straight from the accumulators.  32x32 accumulator layout:
   // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
+  if (partial) {
+    // tile-local partial sums, row-major mt x nt, chunk-major over the tail
+    float* const part = a.ws + ((long long)chunk * a.tail_tiles + (tile - a.dp_tiles)) * (MT * NT);
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int col = wn * C::WTN + j * 32 + q;
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = wm * C::WTM + i * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+          part[row * NT + col] = acc[i][j][e];
+        }
+    }
+    return;
+  }
   // Output element (m, n) sits at colbase(n) + m*mstride in either layout.
-  float* const out = a.out + (long long)ks * a.out_split_stride;
+  float* const out = a.y;
 #pragma unroll
   for (int j = 0; j < C::TN; ++j) {
     const int n = n0 + wn * C::WTN + j * 32 + q;

@@ -11,23 +11,41 @@ namespace mg3m {
 
 typedef float f32x4r __attribute__((ext_vector_type(4)));
 
-// Split-K reduction: y = sum over splits of the partials, in split order, so
-// the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void splitk_reduce_f32(const float* __restrict__ ws,
-                                                         float* __restrict__ y, long long elems,
-                                                         int split, int vec4) {
+// Tail reduction: for every element of every tail tile, y = sum of the
+// tile's chunk partials in chunk order 0, 1, ..., split-1, so the result does
+// not depend on scheduling.  One thread per four consecutive columns of one
+// tile row; rows and columns past the output are skipped.
+__global__ __launch_bounds__(256) void tail_reduce_f32(RArgs r) {
+  const long long tile_elems = (long long)r.mt * r.nt;
+  const long long per_tile4 = tile_elems / 4;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (vec4) {
-    const long long e = i * 4;
-    if (e >= elems) return;
-    f32x4r s = *reinterpret_cast<const f32x4r*>(ws + e);
-    for (int p = 1; p < split; ++p) s += *reinterpret_cast<const f32x4r*>(ws + (long long)p * elems + e);
-    *reinterpret_cast<f32x4r*>(y + e) = s;
+  if (i >= per_tile4 * r.tail_tiles) return;
+  const int t = (int)(i / per_tile4);
+  const int e = (int)(i - (long long)t * per_tile4) * 4;
+  const int row = e / r.nt, col = e - row * r.nt;
+  const float* p = r.ws + (long long)t * tile_elems + e;
+  const long long chunk_stride = (long long)r.tail_tiles * tile_elems;
+  f32x4r sum = *reinterpret_cast<const f32x4r*>(p);
+  for (int c = 1; c < r.split; ++c) sum += *reinterpret_cast<const f32x4r*>(p + c * chunk_stride);
+  const int tile = r.dp_tiles + t;
+  const int tm = tile % r.tiles_m, tn = tile / r.tiles_m;
+  const int m = tm * r.mt + row;
+  if (m >= r.Mg) return;
+  const int n0 = tn * r.nt + col;
+  auto index = [&](int n) -> long long {
+    if (r.layout == kHWCN) {                 // y[Ho][Wo][K][N], n = pix*N + b
+      const int pix = n / r.N, b = n - pix * r.N;
+      return ((long long)pix * r.K + m) * r.N + b;
+    }
+    const int b = n / r.HoWo, pix = n - b * r.HoWo;   // y[N][K][Ho][Wo]
+    return ((long long)b * r.K + m) * r.HoWo + pix;
+  };
+  if (r.vec4 && n0 + 3 < r.Ng) {
+    *reinterpret_cast<f32x4r*>(r.y + index(n0)) = sum;
   } else {
-    if (i >= elems) return;
-    float s = ws[i];
-    for (int p = 1; p < split; ++p) s += ws[(long long)p * elems + i];
-    y[i] = s;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (n0 + q < r.Ng) r.y[index(n0 + q)] = sum[q];
   }
 }
 
@@ -64,19 +82,17 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
   return MG3M_OK;
 }
 
-int launch_splitk_reduce(const float* ws, float* y, long long elems, int split, bool vec4,
-                         void* stream, std::string* err) {
-  const long long threads = vec4 ? (elems + 3) / 4 : elems;
+int launch_tail_reduce(const RArgs& r, void* stream, std::string* err) {
+  const long long threads = (long long)r.mt * r.nt / 4 * r.tail_tiles;
   const long long blocks = (threads + 255) / 256;
-  if (blocks < 1 || blocks > 0x7fffffffLL) {
-    *err = "internal: reduction grid out of range";
+  if (r.mt % 4 || r.nt % 4 || blocks < 1 || blocks > 0x7fffffffLL) {
+    *err = "internal: tail reduction shape out of range";
     return MG3M_ERR_PLAN;
   }
-  hipLaunchKernelGGL(splitk_reduce_f32, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
-                     ws, y, elems, split, vec4 ? 1 : 0);
+  hipLaunchKernelGGL(tail_reduce_f32, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, r);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
-    *err = std::string("split-K reduction launch: ") + hipGetErrorString(e);
+    *err = std::string("tail reduction launch: ") + hipGetErrorString(e);
     return MG3M_ERR_HIP;
   }
   return MG3M_OK;

@@ -62,19 +62,19 @@ struct TileDesc {
 // The tile menu.  Every entry is instantiated for every loader variant.
 constexpr int kNumTiles = 13;
 inline constexpr TileDesc kTiles[kNumTiles] = {
-    {128, 128, 16, 2, 2, 136, 0.708},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 136, 0.802},    // 1: four waves sharing one filter tile (TB(1,8)-like)
-    {256, 64, 16, 4, 1, 144, 0.837},    // 2: four waves sharing one patch tile
-    {64, 128, 16, 1, 2, 144, 0.636},    // 3
-    {128, 64, 16, 2, 1, 144, 0.641},    // 4
-    {64, 64, 16, 1, 1, 146, 0.654},     // 5: one wave per work-group (TB(1,1)-like)
-    {32, 128, 16, 1, 2, 104, 0.703},    // 6
-    {32, 64, 16, 1, 1, 104, 0.649},     // 7
-    {128, 32, 16, 2, 1, 104, 0.730},    // 8
-    {64, 32, 16, 1, 1, 104, 0.658},     // 9
+    {128, 128, 16, 2, 2, 136, 0.824},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
+    {64, 256, 16, 1, 4, 136, 0.803},    // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {256, 64, 16, 4, 1, 144, 0.843},    // 2: four waves sharing one patch tile
+    {64, 128, 16, 1, 2, 144, 0.648},    // 3
+    {128, 64, 16, 2, 1, 144, 0.647},    // 4
+    {64, 64, 16, 1, 1, 146, 0.657},     // 5: one wave per work-group (TB(1,1)-like)
+    {32, 128, 16, 1, 2, 104, 0.698},    // 6
+    {32, 64, 16, 1, 1, 104, 0.645},     // 7
+    {128, 32, 16, 2, 1, 104, 0.741},    // 8
+    {64, 32, 16, 1, 1, 104, 0.660},     // 9
     {256, 128, 16, 4, 2, 130, 0.790},   // 10: eight waves
-    {128, 256, 16, 2, 4, 130, 0.765},   // 11: eight waves
-    {128, 128, 32, 2, 2, 192, 0.795},   // 12: deeper reduction step
+    {128, 256, 16, 2, 4, 130, 0.763},   // 11: eight waves
+    {128, 128, 32, 2, 2, 192, 0.799},   // 12: deeper reduction step
 };
 
 // LDS row strides (floats) of the staged operand tiles.  The two half-waves of
@@ -90,19 +90,29 @@ constexpr int lds_bytes_for(const TileDesc& t) {
 // is reserved as the out-of-range offset that reads as zero.
 constexpr long long kMaxTensorBytes = 0xFFFFFFC0LL;
 
+// How the output tiles are scheduled.  Tiles are numbered tm + tiles_m * tn.
+// The first dp_tiles tiles are computed whole, one work-group each, and
+// written to y.  The remaining tail_tiles tiles are split along the reduction
+// into `split` chunks of k_tiles_per_split k-tiles, one work-group each;
+// those write tile-local partials to the workspace and a second kernel sums
+// each tile's chunks in chunk order into y (deterministic).  Pure data
+// parallel: tail_tiles = 0.  Classic split-K: dp_tiles = 0.  Hybrid: dp_tiles
+// is a whole number of rounds of resident work-groups and only the leftover
+// tiles are split, so the last round is filled with short chunks instead of
+// running mostly empty.
 struct Plan {
   int layout;
   int tile;                 // index into kTiles
   TileDesc t;
-  int split;                // split-K factor
-  int kps;                  // k-tiles per split
-  int k_tiles;              // total k-tiles
+  int k_tiles;              // ceil(Kg / kt)
   int tiles_m, tiles_n;
-  long long grid;
+  int dp_tiles, tail_tiles;
+  int split;                // chunks per tail tile (1 when there is no tail)
+  int kps;                  // k-tiles per chunk
+  long long grid;           // dp_tiles + tail_tiles * split
   int a_mode, b_mode, e_mode;
   int variant;
-  int xcd_remap;
-  size_t ws_bytes;
+  size_t ws_bytes;          // tail_tiles * split * mt * nt floats
   int lds_bytes;
   double pad_eff;
   double est_us;
@@ -112,15 +122,26 @@ struct Plan {
 struct KArgs {
   const float* x;
   const float* w;
-  float* out;               // y, or the split-K workspace
+  float* y;
+  float* ws;                // tile-local partials of the tail tiles
   unsigned x_bytes, w_bytes;
   int N, C, H, W, K, R, S;
   int sh, sw, ph, pw, Ho, Wo;
   int Mg, Ng, Kg;
-  int tiles_m, tiles_n, kps, k_tiles;
-  int e_mode, xcd_remap;
+  int tiles_m, k_tiles;
+  int dp_tiles, tail_tiles, kps;
+  int e_mode;
   int mstride;              // output elements between output channels m and m+1
-  long long out_split_stride;   // elements between split-K partials
+};
+
+// Arguments of the tail reduction.
+struct RArgs {
+  const float* ws;
+  float* y;
+  int mt, nt;               // tile shape
+  int tiles_m, dp_tiles, tail_tiles, split;
+  int layout, N, K, HoWo, Mg, Ng;
+  int vec4;                 // four consecutive columns are contiguous in y
 };
 
 // Planner (host only, no HIP calls).  Returns 0 or an mg3m_status code and
@@ -142,7 +163,6 @@ KernelFn conv_kernel_nchw(int variant, int tile);
 
 // Kernel launchers (conv_launch.hip).
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
-int launch_splitk_reduce(const float* ws, float* y, long long elems, int split, bool vec4,
-                         void* stream, std::string* err);
+int launch_tail_reduce(const RArgs& r, void* stream, std::string* err);
 
 }  // namespace mg3m

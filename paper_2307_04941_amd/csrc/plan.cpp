@@ -34,9 +34,9 @@ constexpr int kMaxWavesPerSimd = 8;
 // of each round of resident work-groups (prologue loads, epilogue stores), and
 // how MFMA utilisation falls when fewer than ~2 waves per SIMD are resident.
 constexpr double kStreamBytesPerS = 5.0e12;
-constexpr double kLaunchUs = 2.0;
-constexpr double kRoundUs = 2.0;
-constexpr double kUtilBase = 0.6, kUtilPerWave = 0.2;
+constexpr double kLaunchUs = 4.0;
+constexpr double kRoundUs = 3.0;
+constexpr double kUtilBase = 0.4, kUtilPerWave = 0.2;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
@@ -61,7 +61,7 @@ double variant_factor(int variant) {
 }
 
 struct Override {
-  int mt = 0, nt = 0, kt = 0, split = 0, xcd = -1;
+  int mt = 0, nt = 0, kt = 0, split = 0, tail = 0;
 };
 
 int parse_override(const char* text, Override* o, std::string* err) {
@@ -110,12 +110,13 @@ int parse_override(const char* text, Override* o, std::string* err) {
         return MG3M_ERR_PLAN;
       }
       o->kt = (int)v;
-    } else if (key == "xcd") {
-      if (val != "0" && val != "1") {
-        *err = "plan override: xcd must be 0 or 1";
+    } else if (key == "tail") {
+      long v = std::strtol(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || v < 2 || v > 64) {
+        *err = "plan override: tail must be 2..64";
         return MG3M_ERR_PLAN;
       }
-      o->xcd = val == "1";
+      o->tail = (int)v;
     } else {
       *err = "plan override: unknown key '" + key + "'";
       return MG3M_ERR_PLAN;
@@ -125,48 +126,87 @@ int parse_override(const char* text, Override* o, std::string* err) {
   return MG3M_OK;
 }
 
-// Fill the shape-dependent parts of a plan for one (tile, split) choice.
-void shape_plan(const ConvShape& s, int tile, int split_req, Plan* p) {
+// How a candidate schedules its tiles (see Plan).
+enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2 };
+
+// Fill the shape-dependent parts of a plan for one (tile, schedule, split)
+// choice.  Returns false when the tile count does not fit a launch.
+bool shape_plan(const ConvShape& s, int tile, int sched, int split_req, Plan* p) {
   const TileDesc& t = kTiles[tile];
   p->layout = s.layout;
   p->tile = tile;
   p->t = t;
   p->k_tiles = (int)cdiv(s.Kg, t.kt);
-  p->kps = (int)cdiv(p->k_tiles, std::max(1, std::min(split_req, p->k_tiles)));
-  p->split = (int)cdiv(p->k_tiles, p->kps);       // no empty split
   p->tiles_m = (int)cdiv(s.Mg, t.mt);
   p->tiles_n = (int)cdiv(s.Ng, t.nt);
-  p->grid = (long long)p->tiles_m * p->tiles_n * p->split;
+  const long long tiles = (long long)p->tiles_m * p->tiles_n;
+  if (tiles > 0x7fffffffLL) return false;
+  if (sched == kDataParallel || split_req <= 1) {
+    p->dp_tiles = (int)tiles;
+    p->tail_tiles = 0;
+  } else if (sched == kSplitAll) {
+    p->dp_tiles = 0;
+    p->tail_tiles = (int)tiles;
+  } else {
+    // whole rounds of resident work-groups run unsplit (none if the tiles do
+    // not fill one round: then every tile is split)
+    const long long slots = (long long)kCUs * resident_wgs(t);
+    const long long dp = tiles / slots * slots;
+    p->dp_tiles = (int)dp;
+    p->tail_tiles = (int)(tiles - dp);
+  }
+  p->kps = p->k_tiles;
+  p->split = 1;
+  if (p->tail_tiles > 0) {
+    p->kps = (int)cdiv(p->k_tiles, std::max(1, std::min(split_req, p->k_tiles)));
+    p->split = (int)cdiv(p->k_tiles, p->kps);       // no empty chunk
+    if (p->split < 2) {                              // too short to split: run whole
+      p->dp_tiles = (int)tiles;
+      p->tail_tiles = 0;
+      p->kps = p->k_tiles;
+      p->split = 1;
+    }
+  }
+  p->grid = (long long)p->dp_tiles + (long long)p->tail_tiles * p->split;
   p->lds_bytes = lds_bytes_for(t);
   const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
                         (double)p->k_tiles * t.kt;
   p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
-  p->ws_bytes = p->split > 1 ? (size_t)p->split * (size_t)(s.Mg * s.Ng) * sizeof(float) : 0;
-
+  p->ws_bytes = (size_t)p->tail_tiles * p->split * t.mt * t.nt * sizeof(float);
   p->est_us = 0.0;
+  return true;
 }
 
-// The selector's predicted time for a plan (microseconds).  The busiest CU
-// runs ceil(grid / 256) work-groups, each costing its padded MFMA flops at
-// the tile's measured efficiency, scaled down when that CU holds too few
-// waves to hide latency, plus a fixed cost per round of resident
-// work-groups; a layer cannot beat streaming its tensors once; split-K adds
-// its partials' traffic and a second launch.
+// The selector's predicted time for a plan (microseconds).  Work-groups are
+// dispatched in order, whole tiles first and tail chunks after them.  In each
+// phase the busiest CU runs ceil(work-groups / 256) of them, each costing its
+// padded MFMA flops at the tile's measured efficiency, scaled down when that
+// CU holds too few waves to hide latency, plus a fixed cost per round of
+// resident work-groups.  A layer cannot beat streaming its tensors (and the
+// partials) once; the tail reduction adds its traffic and a second launch.
 double predict_us(const ConvShape& s, const Plan& p) {
   const TileDesc& t = p.t;
-  const long long per_cu = cdiv(p.grid, kCUs);
   const int occ = resident_wgs(t);
-  const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
-  const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
-  const double eff = t.eff * variant_factor(p.variant) * util;
-  const double wg_flops = 2.0 * t.mt * t.nt * (double)t.kt * p.kps;
-  const double t_comp = (double)per_cu * wg_flops / (kFlopPerClkCU * kClockHz * eff) * 1e6 +
-                        (double)cdiv(per_cu, occ) * kRoundUs;
+  const double tile_flops = 2.0 * t.mt * t.nt * (double)t.kt;
+  auto phase = [&](long long wgs, int k_tiles) {
+    if (wgs <= 0) return 0.0;
+    const long long per_cu = cdiv(wgs, kCUs);
+    const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
+    const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
+    const double eff = t.eff * variant_factor(p.variant) * util;
+    return (double)per_cu * tile_flops * k_tiles / (kFlopPerClkCU * kClockHz * eff) * 1e6 +
+           (double)cdiv(per_cu, occ) * kRoundUs;
+  };
+  const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase((long long)p.tail_tiles * p.split, p.kps);
   const double y_bytes = 4.0 * (double)s.Mg * (double)s.Ng;
   const double xw_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
-  const double t_mem = (xw_bytes + y_bytes * p.split) / kStreamBytesPerS * 1e6;
+  const double part_bytes = (double)p.ws_bytes;
+  const double t_mem = (xw_bytes + y_bytes + part_bytes) / kStreamBytesPerS * 1e6;
   double est = std::max(t_comp, t_mem) + kLaunchUs;
-  if (p.split > 1) est += (p.split + 1) * y_bytes / kStreamBytesPerS * 1e6 + kLaunchUs;
+  if (p.tail_tiles > 0) {
+    const double tail_out = 4.0 * (double)p.tail_tiles * t.mt * t.nt;
+    est += (part_bytes + tail_out) / kStreamBytesPerS * 1e6 + kLaunchUs;
+  }
   return est;
 }
 
@@ -246,38 +286,45 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
   int best = -1;
   Plan best_plan{};
   // the split factors the cost model was calibrated on
-  const int splits[] = {1, 2, 3, 4, 6, 8, 16};
+  const int splits[] = {2, 3, 4, 6, 8, 16};
+  auto consider = [&](int ti, int sched, int sp) {
+    Plan c{};
+    if (!shape_plan(s, ti, sched, sp, &c)) return;
+    choose_modes(s, x16, w16, y16, &c);
+    c.est_us = predict_us(s, c);
+    // ties: less workspace traffic, then the larger tile
+    const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
+                        (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
+                         (c.ws_bytes < best_plan.ws_bytes ||
+                          (c.ws_bytes == best_plan.ws_bytes && c.t.mt * c.t.nt > best_plan.t.mt * best_plan.t.nt)));
+    if (better) {
+      best = ti;
+      best_plan = c;
+    }
+  };
   for (int ti = 0; ti < kNumTiles; ++ti) {
     if (o.mt && !(kTiles[ti].mt == o.mt && kTiles[ti].nt == o.nt)) continue;
     // a forced tile without a depth means the default depth of 16
     if ((o.kt || o.mt) && kTiles[ti].kt != (o.kt ? o.kt : 16)) continue;
-    for (int sp : splits) {
-      if (o.split && sp != 1) break;
-      Plan c{};
-      shape_plan(s, ti, o.split ? o.split : sp, &c);
-      if (!o.split && c.split != sp) continue;        // duplicate after clamping
-      choose_modes(s, x16, w16, y16, &c);
-      c.est_us = predict_us(s, c);
-      // ties: fewer splits (less traffic), then the larger tile
-      bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
-                    (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
-                     (c.split < best_plan.split ||
-                      (c.split == best_plan.split && c.t.mt * c.t.nt > best_plan.t.mt * best_plan.t.nt)));
-      if (better) {
-        best = ti;
-        best_plan = c;
+    if (o.split) {
+      consider(ti, o.split > 1 ? kSplitAll : kDataParallel, o.split);
+    } else if (o.tail) {
+      consider(ti, kSplitTail, o.tail);
+    } else {
+      consider(ti, kDataParallel, 1);
+      for (int sp : splits) {
+        consider(ti, kSplitAll, sp);
+        consider(ti, kSplitTail, sp);
       }
     }
   }
   if (best < 0) {
-    *err = "plan override: no kernel tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
-           (o.kt ? " with kt=" + std::to_string(o.kt) : std::string());
+    *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
+           (o.kt ? " kt=" + std::to_string(o.kt) : std::string()) +
+           (o.tail ? " tail=" + std::to_string(o.tail) : std::string());
     return MG3M_ERR_PLAN;
   }
   *p = best_plan;
-  // Measured on MI355X: grouping tiles per XCD never helped these shapes and
-  // cost up to 5% with 64-row tiles, so it is off unless asked for.
-  p->xcd_remap = o.xcd < 0 ? 0 : o.xcd;
   return MG3M_OK;
 }
 
@@ -287,12 +334,12 @@ std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
-                "tile=%dx%d,waves=%dx%d,kt=%d,split=%d,grid=%lld,tiles=%dx%d,k_tiles=%d,"
-                "a=%s,b=%s,e=%s,xcd=%d,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
+                "tile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,grid=%lld,"
+                "tiles=%dx%d,k_tiles=%d,a=%s,b=%s,e=%s,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
                 "Mg=%lld,Ng=%lld,Kg=%lld",
-                p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.grid, p.tiles_m, p.tiles_n,
-                p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode], p.xcd_remap, p.lds_bytes,
-                p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
+                p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.grid,
+                p.tiles_m, p.tiles_n, p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode],
+                p.lds_bytes, p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
   return buf;
 }
 

@@ -37,6 +37,7 @@ class PlanInfo(ctypes.Structure):
         ("mt", ctypes.c_int), ("nt", ctypes.c_int), ("kt", ctypes.c_int),
         ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int),
         ("split", ctypes.c_int), ("k_tiles", ctypes.c_int), ("k_tiles_per_split", ctypes.c_int),
+        ("dp_tiles", ctypes.c_int), ("tail_tiles", ctypes.c_int),
         ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
         ("grid", ctypes.c_longlong), ("Mg", ctypes.c_longlong), ("Ng", ctypes.c_longlong),
         ("Kg", ctypes.c_longlong), ("workspace_bytes", ctypes.c_size_t), ("lds_bytes", ctypes.c_int),

@@ -85,7 +85,7 @@ def test_workspace_and_plan_errors():
     # forced split-K without a workspace
     rc = lib.conv2d_fwd_f32_ex(X, Wp, Y, *shape, 0, None, 0, b"split=4", None)
     assert rc == 6
-    for bad in (b"tile=7x7", b"split=0", b"split=x", b"bogus=1", b"tile=128", b"xcd=2"):
+    for bad in (b"tile=7x7", b"split=0", b"split=x", b"bogus=1", b"tile=128", b"xcd=1", b"tail=1", b"tail=x"):
         rc = lib.conv2d_fwd_f32_ex(X, Wp, Y, *shape, 0, None, 0, bad, None)
         assert rc == 7, bad
 
@@ -112,12 +112,19 @@ def _check_plan(shape, layout, plan=None):
     # tiles cover the output exactly once
     assert (p["tiles_m"] - 1) * p["mt"] < Mg <= p["tiles_m"] * p["mt"]
     assert (p["tiles_n"] - 1) * p["nt"] < Ng <= p["tiles_n"] * p["nt"]
-    # splits partition the k-tiles, none empty
+    # whole tiles and split tail tiles partition the tiles; chunks partition
+    # the k-tiles, none empty
     kt = p["k_tiles"]
     assert kt == -(-Kg // p["kt"])
-    assert (p["split"] - 1) * p["k_tiles_per_split"] < kt <= p["split"] * p["k_tiles_per_split"]
-    assert p["grid"] == p["tiles_m"] * p["tiles_n"] * p["split"] <= 2**31 - 1
-    assert p["workspace_bytes"] == (4 * p["split"] * Mg * Ng if p["split"] > 1 else 0)
+    tiles = p["tiles_m"] * p["tiles_n"]
+    assert p["dp_tiles"] + p["tail_tiles"] == tiles
+    if p["tail_tiles"]:
+        assert p["split"] >= 2
+        assert (p["split"] - 1) * p["k_tiles_per_split"] < kt <= p["split"] * p["k_tiles_per_split"]
+    else:
+        assert p["split"] == 1 and p["k_tiles_per_split"] == kt
+    assert p["grid"] == p["dp_tiles"] + p["tail_tiles"] * p["split"] <= 2**31 - 1
+    assert p["workspace_bytes"] == 4 * p["tail_tiles"] * p["split"] * p["mt"] * p["nt"]
     assert 0 < p["lds_bytes"] <= 160 * 1024
     assert 0 < p["pad_efficiency"] <= 1.0
     assert p["est_us"] > 0

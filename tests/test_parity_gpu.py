@@ -81,6 +81,34 @@ def test_every_tile_nchw(tile):
         assert_parity(y, acc, mag, f"{shape} {plan}")
 
 
+# Enough output tiles for more than one round of resident work-groups, so that
+# tail=n splits only the leftover tiles (e.g. 256x64 tiles: 3081 tiles against
+# 768 resident work-groups -> 3072 whole, 9 split).
+TAIL_SHAPE = (16, 16, 111, 111, 32, 3, 3, 1, 1)
+
+
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+@pytest.mark.parametrize("plan", ["tile=256x64,tail=2", "tile=256x64,tail=3", "tile=256x64,tail=5",
+                                  "tile=64x256,tail=4", "tile=128x128,kt=32,tail=2"])
+def test_tail_split(plan, layout):
+    x, w, st, pd = make(TAIL_SHAPE, 85, layout)
+    info = mg3m.conv2d_fwd_f32_plan_info(*TAIL_SHAPE, layout, plan)
+    say(f"tail split {plan} {layout}: dp_tiles {info['dp_tiles']} tail_tiles {info['tail_tiles']} "
+        f"split {info['split']}")
+    assert info["dp_tiles"] > 0 and info["tail_tiles"] > 0
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    y = run_gpu(x, w, st, pd, layout, plan=plan)
+    assert_parity(y, acc, mag, f"{TAIL_SHAPE} {plan} {layout}")
+
+
+def test_tail_split_bit_exact():
+    x, w, st, pd = make(TAIL_SHAPE, 86, "HWCN", dist="int")
+    acc, _ = oracle.conv2d(x, w, st, pd, "HWCN")
+    for plan in ("tile=256x64,tail=3", "tile=256x64,split=4"):
+        y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+        assert np.array_equal(y.astype(np.float64), acc), f"{plan}: not bit-exact"
+
+
 @pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
 def test_misaligned_pointers(layout):
     """4-byte but not 16-byte aligned buffers take the element-wise paths."""
