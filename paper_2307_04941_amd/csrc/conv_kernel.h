@@ -140,6 +140,51 @@ struct AVecM {
   }
 };
 
+// HWCN filter for the one-tap-per-slab path: rows of a stage are channels
+// c0..c0+KT-1 of tap (r, s), in the same stage order as the patch loader.
+template <class C, int MT, int KT>
+struct AVecMTap {
+  static constexpr int MC4 = MT / 4;
+  static constexpr int RSTEP = C::T / MC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % MC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::A_ELEMS, "A vec-M split");
+  int m4, kr0, base;
+  bool m_ok;
+  int r, s, c0;
+  f32x4 v[NV];
+
+  __device__ void init(const KArgs& a, int t, int m0, int kbeg) {
+    m4 = t % MC4;
+    kr0 = t / MC4;
+    const int m = m0 + m4 * 4;
+    m_ok = m < a.Mg;
+    base = kr0 * a.K + m;
+    const int t0 = kbeg / KT, rs = a.R * a.S;
+    const int slab = t0 / rs, tap = t0 - slab * rs;
+    c0 = slab * KT;
+    r = tap / a.S;
+    s = tap - r * a.S;
+  }
+  __device__ void advance(const KArgs& a) {
+    if (++s == a.S) {
+      s = 0;
+      if (++r == a.R) { r = 0; c0 += KT; }
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t wr) {
+    const int o = base + ((r * a.S + s) * a.C + c0) * a.K;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const unsigned off = (unsigned)(o + i * RSTEP * a.K) * 4u;
+      v[i] = bload4(wr, m_ok ? off : kOOB);
+    }
+  }
+  __device__ void store(float* As) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + m4 * 4, v[i]);
+  }
+};
+
 // NCHW filter w[K][C][R][S] is A[m][k] (Kg contiguous): 4-wide k vectors,
 // transposed into the k-major LDS tile.
 template <class C, int MT, int KT>
@@ -217,7 +262,10 @@ struct AScalar {
 // inside one filter tap (r, s) -- the per-pixel IN_mtx of Alg. 1 -- so the tap
 // is the same for the whole work-group and kept in scalar registers; each
 // thread tests its column against the padding once per stage and its NV rows
-// are consecutive channel offsets of one input pixel.
+// are consecutive channel offsets of one input pixel.  Stages run the taps
+// inside each channel slab (Alg. 1's fh, fw loops inside the IC blocks), so
+// a neighbouring output pixel's shifted reuse of an input pixel comes one
+// stage later and still hits in L2.
 template <class C, int NT, int KT>
 struct BVecNTap {
   static constexpr int NC4 = NT / 4;
@@ -242,16 +290,18 @@ struct BVecNTap {
     // element offset of (ih0, iw0, channel kr0, image b); only used when the
     // tap lands inside the input
     base = ((ih0 * a.W + iw0) * a.C + kr0) * a.N + b;
-    const int tap = kbeg / a.C;
-    c0 = kbeg - tap * a.C;
-    s = tap % a.S;
+    // stage t covers channels c0..c0+KT-1 of tap (r, s); stages run taps
+    // inner, channel slabs outer: t = (c0 / KT) * R*S + r*S + s
+    const int t0 = kbeg / KT, rs = a.R * a.S;
+    const int slab = t0 / rs, tap = t0 - slab * rs;
+    c0 = slab * KT;
     r = tap / a.S;
+    s = tap - r * a.S;
   }
   __device__ void advance(const KArgs& a) {
-    c0 += KT;
-    if (c0 == a.C) {
-      c0 = 0;
-      if (++s == a.S) { s = 0; ++r; }
+    if (++s == a.S) {
+      s = 0;
+      if (++r == a.R) { r = 0; c0 += KT; }
     }
   }
   __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
@@ -414,14 +464,16 @@ struct BScalar {
   }
 };
 
-template <int LAYOUT, int AM, class C, int MT, int KT>
+template <int LAYOUT, int AM, class C, int MT, int KT, int BM = -1>
 struct ASel;
+template <class C, int MT, int KT, int BM>
+struct ASel<kHWCN, kAVecM, C, MT, KT, BM> { using type = AVecM<C, MT, KT>; };
 template <class C, int MT, int KT>
-struct ASel<kHWCN, kAVecM, C, MT, KT> { using type = AVecM<C, MT, KT>; };
-template <class C, int MT, int KT>
-struct ASel<kNCHW, kAVecK, C, MT, KT> { using type = AVecK<C, MT, KT>; };
-template <int LAYOUT, class C, int MT, int KT>
-struct ASel<LAYOUT, kAScalar, C, MT, KT> { using type = AScalar<LAYOUT, C, MT, KT>; };
+struct ASel<kHWCN, kAVecM, C, MT, KT, kBVecNTap> { using type = AVecMTap<C, MT, KT>; };
+template <class C, int MT, int KT, int BM>
+struct ASel<kNCHW, kAVecK, C, MT, KT, BM> { using type = AVecK<C, MT, KT>; };
+template <int LAYOUT, class C, int MT, int KT, int BM>
+struct ASel<LAYOUT, kAScalar, C, MT, KT, BM> { using type = AScalar<LAYOUT, C, MT, KT>; };
 
 template <int LAYOUT, int BM, class C, int NT, int KT>
 struct BSel;
@@ -471,8 +523,18 @@ void conv_igemm_f32(KArgs a) {
   // Work-group -> (tile, range of k-tiles).  Work-groups [0, dp_tiles) each
   // compute one whole tile; the rest compute one chunk of kps k-tiles of a
   // tail tile, consecutive work-groups taking different tiles of the same
-  // chunk.
-  const int L = blockIdx.x;
+  // chunk.  The whole tiles are regrouped so that each XCD gets a contiguous
+  // run of them (tiles sharing a patch tile or halo rows then share one L2);
+  // the tail chunks keep their place at the end of the dispatch order.
+  int L = blockIdx.x;
+  if (L < a.dp_tiles) {
+    // XCD grouping of the whole tiles only (tail chunks keep their place at
+    // the end of the dispatch order): work-group i runs on XCD i % 8, so give
+    // each XCD a contiguous run of tiles.  dp_tiles is a multiple of 8
+    // whenever there is a tail; otherwise the runs differ by one.
+    const int G = a.dp_tiles, q8 = G >> 3, r8 = G & 7, xcd = L & 7, loc = L >> 3;
+    L = (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
+  }
   int tile, kt0, nk, chunk = 0;
   const bool partial = L >= a.dp_tiles;
   if (!partial) {
@@ -497,7 +559,7 @@ void conv_igemm_f32(KArgs a) {
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
 
-  typename ASel<LAYOUT, AM, C, MT, KT>::type al;
+  typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
   typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
   al.init(a, t, m0, kbeg);
   bl.init(a, t, n0, kbeg);
