@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""The paper's scene experiments, measured on one MI355X.
+
+    python experiments.py adaptability [--workloads W,...] [--reps R] [--out FILE]
+    python experiments.py ablation [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
+
+adaptability -- Sec. 5.1: the channel-scale scenes (5.1.1), the batch sweep
+    (5.1.2), the filter-size sweep (5.1.3) and the padding/stride sweep
+    (5.1.4).  Per scene: fp32 TFLOPS of the C-ABI call with the selector's
+    plan, and the hardware efficiency the paper uses (runtime performance /
+    theoretical peak; here the 157.3 TFLOPS fp32 MFMA peak).  Group averages
+    follow the paper's groupings.
+ablation -- Sec. 5.3, Table 2: one fixed work-group mapping for every scene
+    (by default the 128x128 tile, a 2-D wave grid sharing both operands like
+    TB(8,8), and the one-wave 32x64 tile, like TB(1,1)), against the per-shape
+    selector, on the batch-sweep scenes (B in {64, 128, 256}, IC = OC from 16 to
+    1024); average efficiency per B, and the tile the selector picked per scene
+    (the analogue of Fig. 14's best-grained map).
+
+Inputs are the seeded synthetic tensors of ``workloads`` (HWCN, resident on
+the GPU before timing).  Each scene is warmed up for ~100 ms, then timed over
+R calls with HIP events on the calling stream.  One JSON line per scene and
+one summary line are printed (and written to --out).  Correctness of every
+scene at full size is checked by tests/test_parity_layers_gpu.py.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = 157.3
+
+
+def _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache):
+    """Mean microseconds per call of one plan (None = the selector)."""
+    args = (L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
+    need = mg3m.conv2d_fwd_f32_workspace_bytes(*args, plan)
+    if need > ws_cache["bytes"]:
+        ws_cache["t"] = None
+        torch.cuda.empty_cache()
+        ws_cache["t"] = torch.empty((need + 3) // 4, dtype=torch.float32, device="cuda")
+        ws_cache["bytes"] = need
+
+    def call():
+        if plan is None:
+            mg3m.conv2d_fwd_f32(xd, wd, yd, *args)
+        else:
+            ws = ws_cache["t"] if need else None
+            mg3m.conv2d_fwd_f32_ex(xd, wd, yd, *args, ws, need, plan)
+
+    call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def run_scenes(workload_names, plans, reps, emit):
+    """Time every scene of the workloads with the selector and the given
+    fixed plans; emit one record per scene."""
+    import torch
+
+    import workloads
+    from paper_2307_04941_amd import mg3m
+
+    mg3m.load_library()
+    torch.cuda.set_device(0)
+    records = []
+    ws_cache = {"t": None, "bytes": 0}
+    for wl in workload_names:
+        for i, L in enumerate(workloads.workload(wl)):
+            _, x, w = workloads.layer_tensors(wl, i, "HWCN")
+            xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+            Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
+            yd = torch.empty((Ho, Wo, L.K, L.N), dtype=torch.float32, device="cuda")
+            flops = 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo
+            t_end = time.perf_counter() + 0.1          # clocks up before timing
+            while time.perf_counter() < t_end:
+                mg3m.conv2d_fwd_f32(xd, wd, yd, L.N, L.C, L.H, L.W, L.K, L.R, L.S,
+                                    L.stride, L.pad, "HWCN")
+                torch.cuda.synchronize()
+            info = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S,
+                                                 L.stride, L.pad, "HWCN")
+            rec = {"workload": wl, "scene": L.name, "N": L.N, "C": L.C, "K": L.K, "H": L.H,
+                   "R": L.R, "stride": L.stride, "pad": L.pad, "gflop": flops / 1e9,
+                   "selector_plan": f"tile={info['mt']}x{info['nt']}x{info['kt']},"
+                                    f"dp={info['dp_tiles']},tail={info['tail_tiles']}x{info['split']}"}
+            for plan in [None] + list(plans):
+                us = _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache)
+                key = plan or "selector"
+                rec[key] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 2),
+                            "pct_peak": round(100 * flops / us / 1e6 / PEAK_TFLOPS, 2)}
+            records.append(rec)
+            emit(rec)
+            del xd, wd, yd
+            torch.cuda.empty_cache()
+    return records
+
+
+def _mean(v):
+    return round(sum(v) / len(v), 2) if v else None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("mode", choices=["adaptability", "ablation"])
+    ap.add_argument("--workloads", default=None)
+    ap.add_argument("--fixed", default="tile=128x128,split=1;tile=32x64,split=1",
+                    help="ablation: fixed plans separated by ';'")
+    ap.add_argument("--reps", type=int, default=10)
+    ap.add_argument("--out", default=None)
+    a = ap.parse_args()
+
+    out = open(a.out, "w") if a.out else None
+
+    def emit(obj):
+        line = json.dumps(obj)
+        print(line, flush=True)
+        if out:
+            out.write(line + "\n")
+            out.flush()
+
+    if a.mode == "adaptability":
+        names = (a.workloads.split(",") if a.workloads else
+                 ["channel_scenes_n128", "batch_sweep", "filter_sweep_n128", "padstride_sweep_n128"])
+        recs = run_scenes(names, [], a.reps, emit)
+        groups = collections.defaultdict(list)
+        for r in recs:
+            pct = r["selector"]["pct_peak"]
+            if r["workload"] == "channel_scenes_n128":
+                groups["channels_" + r["scene"].split("_")[0]].append(pct)
+            elif r["workload"] == "batch_sweep":
+                groups[f"batch_B{r['N']}"].append(pct)
+            elif r["workload"] == "filter_sweep_n128":
+                groups[f"filter_{r['R']}x{r['R']}"].append(pct)
+            elif r["workload"] == "padstride_sweep_n128":
+                groups[f"pad{r['pad']}_stride{r['stride']}"].append(pct)
+            else:
+                groups[r["workload"]].append(pct)
+        emit({"summary": "adaptability", "metric": "mean % of the fp32 MFMA peak per group",
+              "groups": {g: _mean(v) for g, v in groups.items()},
+              "max_pct_peak": max(r["selector"]["pct_peak"] for r in recs)})
+    else:
+        fixed = [p for p in a.fixed.split(";") if p]
+        names = a.workloads.split(",") if a.workloads else ["batch_sweep"]
+        recs = run_scenes(names, fixed, a.reps, emit)
+        per_b = collections.defaultdict(lambda: collections.defaultdict(list))
+        tiles = collections.defaultdict(dict)
+        for r in recs:
+            for key in ["selector"] + fixed:
+                per_b[r["N"]][key].append(r[key]["pct_peak"])
+            tiles[r["N"]][r["C"]] = r["selector_plan"]
+        emit({"summary": "ablation", "metric": "mean % of the fp32 MFMA peak per batch size",
+              "per_batch": {str(b): {k: _mean(v) for k, v in d.items()} for b, d in sorted(per_b.items())},
+              # the paper's Table 2 comparison: mean efficiency of the selector
+              # over that of each fixed mapping, minus one
+              "selector_gain_pct": {str(b): {k: round(100 * (sum(d["selector"]) / sum(d[k]) - 1), 1)
+                                             for k in fixed}
+                                    for b, d in sorted(per_b.items())},
+              "selector_plans": {str(b): v for b, v in sorted(tiles.items())}})
+    if out:
+        out.close()
+
+
+if __name__ == "__main__":
+    main()

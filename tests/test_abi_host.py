@@ -182,3 +182,20 @@ def test_inception_5x5_layer_matches_paper_mm_unit():
     g = json.load(open(os.path.join(GOLDEN, "paper_arithmetic.json")))["inception3a_5x5_mm_unit"]
     L = [l for l in workloads.workload("alexnet_inception_n128") if l.name == "incep3a_5x5"][0]
     assert (L.K, L.N, L.C) == (g["M_oc"], g["N_batch"], g["K_ic"])
+
+
+def test_time_next_kernel_arguments():
+    lib = mg3m.load_library()
+    assert lib.mg3m_time_next_kernel(None, None) == 0
+    assert lib.mg3m_time_next_kernel(0x1000, None) == 10       # MG3M_ERR_ARG: one event only
+    assert lib.mg3m_time_next_kernel(None, 0x1000) == 10
+    assert lib.mg3m_time_next_kernel(None, None) == 0          # cleared again
+
+
+def test_bench_refuses_more_than_one_gpu():
+    import subprocess
+    import sys
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert p.returncode == 2
+    assert "one GPU" in p.stderr

@@ -273,17 +273,33 @@ def test_points_match_full(layout):
 
 
 def test_output_sizes_golden():
-    """Output sizes of every catalogue layer against hand-computed values."""
+    """Output sizes of every layer of the benchmark configurations against
+    hand-computed values."""
     with open(os.path.join(GOLDEN, "output_sizes.json")) as f:
         gold = json.load(f)["sizes"]
     seen = 0
-    for wl_name, (_, layers) in workloads.WORKLOADS.items():
-        for L in layers:
+    for wl_name in workloads.CONFIG_WORKLOADS:
+        for L in workloads.workload(wl_name):
             key = f"{wl_name}/{L.name}"
             ho, wo = oracle.out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
             assert [ho, wo] == gold[key], key
             seen += 1
     assert seen == len(gold)
+
+
+def test_output_sizes_of_sweep_layers_by_counting_windows():
+    """The Sec. 5.1 sweep layers: output sizes against a count of the window
+    positions that fit in the padded input (no floor formula)."""
+    def count(size, pad, k, stride):
+        n, start = 0, 0
+        while start + k <= size + 2 * pad:
+            n += 1
+            start += stride
+        return n
+    for wl_name in workloads.SWEEP_WORKLOADS:
+        for L in workloads.workload(wl_name):
+            expect = (count(L.H, L.pad, L.R, L.stride), count(L.W, L.pad, L.S, L.stride))
+            assert oracle.out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad) == expect, L
 
 
 def test_invalid_shapes_rejected():

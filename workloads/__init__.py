@@ -9,19 +9,25 @@ Inputs stand in for the paper's workloads (Sec. 5): the paper's CNN
 experiments use only layer shapes, so seeded uniform / He-normal tensors of
 those shapes replace real activations and trained weights.
 
-Random recipe (numpy ``Generator(PCG64(seed))``):
-  * x ~ uniform[-1, 1): ``rng.random(n, float32) * 2 - 1``, drawn in logical
+Random recipe (numpy PCG64): a tensor of n elements, in logical order, is
+cut into chunks of 2^22 elements and chunk i is drawn from the stream
+``PCG64(seed).jumped(i)`` (chunks are drawn in parallel threads; the values do
+not depend on the thread count):
+  * x ~ uniform[-1, 1): ``random(float32) * 2 - 1``, drawn in logical
     (N, C, H, W) order, then permuted to the requested layout;
   * w ~ He-normal ``standard_normal(float32) * sqrt(2 / (C*R*S))`` or uniform
     [-1, 1), drawn in logical (K, C, R, S) order, then permuted;
   * small-integer data: x, w drawn uniformly from {-2, ..., 2};
   * seed(x) = 230704941 + 10000 * workload_id + 10 * layer_index,
     seed(w) = seed(x) + 1.
-Both layouts of one seed are the same logical tensors.
+Both layouts of one seed are the same logical tensors.  Layout permutations
+are done by torch on the CPU (multi-threaded data movement only).
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field, asdict
+import concurrent.futures
+import os
+from dataclasses import dataclass, asdict
 from typing import List
 
 import numpy as np
@@ -110,6 +116,52 @@ def _alexnet_inception(n=128) -> List[Layer]:
     ]
 
 
+# ------------------------------------------------ the paper's scene sweeps
+# Sec. 5.1 varies one convolution parameter group at a time; the paper does
+# not state the spatial size, the batch of the channel / filter / pad-stride
+# sweeps, nor the padding of the filter sweep.  Readings used here: input
+# 56x56 when both channel counts are <= 64, else 28x28; B = 128 where B is
+# not the swept parameter; 3x3 filters with pad 1 and stride 1 unless swept;
+# "same" padding (pad = fltH // 2) in the filter sweep.
+CHANNEL_GROUPS = {"small": (16, 32, 48, 64), "medium": (64, 128, 192, 256),
+                  "big": (256, 512, 768, 1024)}
+IC_EQ_OC = (16, 32, 48, 64, 128, 192, 256, 512, 768, 1024)
+
+
+def _hw(c, k):
+    return 56 if max(c, k) <= 64 else 28
+
+
+def _channel_scenes(n=128) -> List[Layer]:
+    """Sec. 5.1.1: 16 (IC, OC) scenes in each of three channel scales."""
+    out = []
+    for g, vals in CHANNEL_GROUPS.items():
+        for c in vals:
+            for k in vals:
+                hw = _hw(c, k)
+                out.append(Layer(f"{g}_C{c}_K{k}", n, c, hw, hw, k, 3, 3, 1, 1))
+    return out
+
+
+def _batch_sweep() -> List[Layer]:
+    """Sec. 5.1.2 (and the scenes of Sec. 5.3, Table 2): B in {64, 128, 256}
+    with IC = OC over the channel values of Sec. 5.1.1."""
+    return [Layer(f"B{n}_C{c}", n, c, _hw(c, c), _hw(c, c), c, 3, 3, 1, 1)
+            for n in (64, 128, 256) for c in IC_EQ_OC]
+
+
+def _filter_sweep(n=128) -> List[Layer]:
+    """Sec. 5.1.3: fltH = fltW in {3, 5, 7, 9, 11} with IC = OC."""
+    return [Layer(f"F{r}_C{c}", n, c, _hw(c, c), _hw(c, c), c, r, r, 1, r // 2)
+            for r in (3, 5, 7, 9, 11) for c in IC_EQ_OC]
+
+
+def _padstride_sweep(n=128) -> List[Layer]:
+    """Sec. 5.1.4: (pad, stride) in {(0, 1), (1, 1), (0, 2), (1, 2)}, 3x3, IC = OC."""
+    return [Layer(f"P{p}S{s}_C{c}", n, c, _hw(c, c), _hw(c, c), c, 3, 3, s, p)
+            for (p, s) in ((0, 1), (1, 1), (0, 2), (1, 2)) for c in IC_EQ_OC]
+
+
 # workload id -> (name, layers); the id enters the seed
 WORKLOADS = {
     "single_16x16_32px": (1, [Layer("single", 1, 16, 32, 32, 16, 3, 3, 1, 1)]),
@@ -117,7 +169,18 @@ WORKLOADS = {
     "vgg16_n64": (3, _vgg16()),
     "resnet50_n32": (4, _resnet50()),
     "alexnet_inception_n128": (5, _alexnet_inception()),
+    "channel_scenes_n128": (6, _channel_scenes()),
+    "batch_sweep": (7, _batch_sweep()),
+    "filter_sweep_n128": (8, _filter_sweep()),
+    "padstride_sweep_n128": (9, _padstride_sweep()),
 }
+
+# the workloads named by the benchmark configurations; the others are the
+# paper's Sec. 5.1 / 5.3 scene sweeps
+CONFIG_WORKLOADS = ("single_16x16_32px", "scene_sweep", "vgg16_n64", "resnet50_n32",
+                    "alexnet_inception_n128")
+SWEEP_WORKLOADS = ("channel_scenes_n128", "batch_sweep", "filter_sweep_n128",
+                   "padstride_sweep_n128")
 
 
 def workload(name: str) -> List[Layer]:
@@ -131,16 +194,21 @@ def seeds(workload_name: str, layer_index: int):
 
 
 # ---------------------------------------------------------------- layouts
+def _permute(a, order):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).permute(*order).contiguous().numpy()
+
+
 def nchw_to_hwcn(x):      # x[N,C,H,W] -> x[H,W,C,N]
-    return np.ascontiguousarray(np.transpose(x, (2, 3, 1, 0)))
+    return _permute(x, (2, 3, 1, 0))
 
 
 def kcrs_to_rsck(w):      # w[K,C,R,S] -> w[R,S,C,K]
-    return np.ascontiguousarray(np.transpose(w, (2, 3, 1, 0)))
+    return _permute(w, (2, 3, 1, 0))
 
 
 def hwcn_to_nchw(y):      # y[Ho,Wo,K,N] -> y[N,K,Ho,Wo]
-    return np.ascontiguousarray(np.transpose(y, (3, 2, 0, 1)))
+    return _permute(y, (3, 2, 0, 1))
 
 
 def to_layout(x_nchw, w_kcrs, layout: str):
@@ -152,22 +220,55 @@ def to_layout(x_nchw, w_kcrs, layout: str):
 
 
 # ---------------------------------------------------------------- generators
+CHUNK = 1 << 22
+_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def _draw(n, seed, fill):
+    """n values in logical order; chunk i from PCG64(seed).jumped(i).
+    fill(generator, out_view) writes one chunk."""
+    out = np.empty(n, np.float32)
+    chunks = (n + CHUNK - 1) // CHUNK
+
+    def one(i):
+        g = np.random.Generator(np.random.PCG64(seed).jumped(i))
+        fill(g, out[i * CHUNK:min(n, (i + 1) * CHUNK)])
+
+    if chunks <= 1:
+        for i in range(chunks):
+            one(i)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(min(_THREADS, chunks)) as ex:
+            list(ex.map(one, range(chunks)))
+    return out
+
+
 def uniform(shape, seed):
-    rng = np.random.Generator(np.random.PCG64(seed))
     n = int(np.prod(shape))
-    return (rng.random(n, dtype=np.float32) * np.float32(2) - np.float32(1)).reshape(shape)
+
+    def fill(g, o):
+        g.random(out=o, dtype=np.float32)
+        o *= np.float32(2)
+        o -= np.float32(1)
+    return _draw(n, seed, fill).reshape(shape)
 
 
 def he_normal(shape, fan_in, seed):
-    rng = np.random.Generator(np.random.PCG64(seed))
     n = int(np.prod(shape))
     scale = np.float32(np.sqrt(2.0 / fan_in))
-    return (rng.standard_normal(n, dtype=np.float32) * scale).reshape(shape)
+
+    def fill(g, o):
+        g.standard_normal(out=o, dtype=np.float32)
+        o *= scale
+    return _draw(n, seed, fill).reshape(shape)
 
 
 def small_int(shape, seed, lo=-2, hi=2):
-    rng = np.random.Generator(np.random.PCG64(seed))
-    return rng.integers(lo, hi + 1, size=shape).astype(np.float32)
+    n = int(np.prod(shape))
+
+    def fill(g, o):
+        o[:] = g.integers(lo, hi + 1, size=o.size)
+    return _draw(n, seed, fill).reshape(shape)
 
 
 def make_tensors(layer: Layer, seed_x: int, seed_w: int, layout: str = "HWCN", dist: str = None):
