@@ -3,6 +3,7 @@
 
     python experiments.py adaptability [--workloads W,...] [--reps R] [--out FILE]
     python experiments.py ablation [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
+    python experiments.py acc64 [--workloads W,...] [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
 
 adaptability -- Sec. 5.1: the channel-scale scenes (5.1.1), the batch sweep
     (5.1.2), the filter-size sweep (5.1.3) and the padding/stride sweep
@@ -16,6 +17,10 @@ ablation -- Sec. 5.3, Table 2: one fixed work-group mapping for every scene
     selector, on the batch-sweep scenes (B in {64, 128, 256}, IC = OC from 16 to
     1024); average efficiency per B, and the tile the selector picked per scene
     (the analogue of Fig. 14's best-grained map).
+acc64 -- the fp64-accumulating entry point (the paper's own numerics: fp32
+    data, fp64 arithmetic, Sec. 4.1.1 / Alg. 2) against the fp32 one, per
+    layer: TFLOPS and % of each path's MFMA peak (fp64 78.6, fp32 157.3),
+    with the selector's plan and any fixed acc64 tile plans given.
 
 Inputs are the seeded synthetic tensors of ``workloads`` (HWCN, resident on
 the GPU before timing).  Each scene is warmed up for ~100 ms, then timed over
@@ -36,12 +41,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = 157.3
+PEAK64_TFLOPS = 78.6
 
 
-def _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache):
+def _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache, acc64=False):
     """Mean microseconds per call of one plan (None = the selector)."""
     args = (L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
-    need = mg3m.conv2d_fwd_f32_workspace_bytes(*args, plan)
+    need = 0 if acc64 else mg3m.conv2d_fwd_f32_workspace_bytes(*args, plan)
     if need > ws_cache["bytes"]:
         ws_cache["t"] = None
         torch.cuda.empty_cache()
@@ -49,7 +55,10 @@ def _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache):
         ws_cache["bytes"] = need
 
     def call():
-        if plan is None:
+        if acc64:
+            mg3m.conv2d_fwd_f32_acc64(xd, wd, yd, L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride,
+                                      L.stride, L.pad, L.pad, "HWCN", plan)
+        elif plan is None:
             mg3m.conv2d_fwd_f32(xd, wd, yd, *args)
         else:
             ws = ws_cache["t"] if need else None
@@ -66,9 +75,11 @@ def _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache):
     return e0.elapsed_time(e1) * 1e3 / reps
 
 
-def run_scenes(workload_names, plans, reps, emit):
+def run_scenes(workload_names, plans, reps, emit, acc64_plans=None):
     """Time every scene of the workloads with the selector and the given
-    fixed plans; emit one record per scene."""
+    fixed plans; emit one record per scene.  acc64_plans: also time the
+    fp64-accumulating entry point with its selector (None in the list) and
+    these fixed plans, keyed "acc64:<plan>"."""
     import torch
 
     import workloads
@@ -101,6 +112,15 @@ def run_scenes(workload_names, plans, reps, emit):
                 key = plan or "selector"
                 rec[key] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 2),
                             "pct_peak": round(100 * flops / us / 1e6 / PEAK_TFLOPS, 2)}
+            if acc64_plans is not None:
+                info = mg3m.conv2d_fwd_f32_acc64_plan_string(L.N, L.C, L.H, L.W, L.K, L.R, L.S,
+                                                             L.stride, L.stride, L.pad, L.pad, "HWCN")
+                rec["acc64_selector_plan"] = info.split(",")[1]
+                for plan in acc64_plans:
+                    us = _time_plan(mg3m, torch, L, xd, wd, yd, plan, reps, ws_cache, acc64=True)
+                    rec["acc64:" + (plan or "selector")] = {
+                        "us": round(us, 2), "tflops": round(flops / us / 1e6, 2),
+                        "pct_peak64": round(100 * flops / us / 1e6 / PEAK64_TFLOPS, 2)}
             records.append(rec)
             emit(rec)
             del xd, wd, yd
@@ -114,10 +134,11 @@ def _mean(v):
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["adaptability", "ablation"])
+    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64"])
     ap.add_argument("--workloads", default=None)
-    ap.add_argument("--fixed", default="tile=128x128,split=1;tile=32x64,split=1",
-                    help="ablation: fixed plans separated by ';'")
+    ap.add_argument("--fixed", default=None,
+                    help="ablation / acc64: fixed plans separated by ';' (ablation default: "
+                         "tile=128x128,split=1;tile=32x64,split=1; acc64 default: none)")
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--out", default=None)
     a = ap.parse_args()
@@ -151,8 +172,24 @@ def main():
         emit({"summary": "adaptability", "metric": "mean % of the fp32 MFMA peak per group",
               "groups": {g: _mean(v) for g, v in groups.items()},
               "max_pct_peak": max(r["selector"]["pct_peak"] for r in recs)})
+    elif a.mode == "acc64":
+        fixed = [p for p in (a.fixed or "").split(";") if p]
+        names = a.workloads.split(",") if a.workloads else ["vgg16_n64", "resnet50_n32"]
+        recs = run_scenes(names, [], a.reps, emit, acc64_plans=[None] + fixed)
+        per_wl = collections.defaultdict(lambda: {"flop": 0.0, "us32": 0.0, "us64": 0.0})
+        for r in recs:
+            d = per_wl[r["workload"]]
+            d["flop"] += r["gflop"] * 1e9
+            d["us32"] += r["selector"]["us"]
+            d["us64"] += r["acc64:selector"]["us"]
+        emit({"summary": "acc64", "metric": "whole-workload TFLOPS, fp32 vs fp64 accumulation",
+              "workloads": {w: {"fp32_tflops": round(d["flop"] / d["us32"] / 1e6, 2),
+                                "acc64_tflops": round(d["flop"] / d["us64"] / 1e6, 2),
+                                "acc64_pct_fp64_peak": round(100 * d["flop"] / d["us64"] / 1e6
+                                                             / PEAK64_TFLOPS, 2)}
+                            for w, d in per_wl.items()}})
     else:
-        fixed = [p for p in a.fixed.split(";") if p]
+        fixed = [p for p in (a.fixed or "tile=128x128,split=1;tile=32x64,split=1").split(";") if p]
         names = a.workloads.split(",") if a.workloads else ["batch_sweep"]
         recs = run_scenes(names, fixed, a.reps, emit)
         per_b = collections.defaultdict(lambda: collections.defaultdict(list))

@@ -109,6 +109,50 @@ int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
                       void *workspace, size_t workspace_bytes,
                       const char *plan, void *stream);
 
+/* Separate vertical and horizontal stride and padding (Table 1's stdH, stdW,
+ * padH, padW).  Output size: Ho = floor((H + 2*pad_h - R)/stride_h) + 1,
+ * Wo = floor((W + 2*pad_w - S)/stride_w) + 1.  Ho, Wo: host out-parameters.
+ * Returns MG3M_OK or MG3M_ERR_SHAPE / MG3M_ERR_NULL / MG3M_ERR_TOO_LARGE. */
+int conv2d_out_dims_hw(int H, int W, int R, int S, int stride_h, int stride_w,
+                       int pad_h, int pad_w, int *Ho, int *Wo);
+
+/* As conv2d_fwd_f32_ex with separate vertical and horizontal stride and
+ * padding (everything else, including the workspace rules and the plan
+ * override, is the same). */
+int conv2d_fwd_f32_hw(const float *x, const float *w, float *y,
+                      int N, int C, int H, int W, int K, int R, int S,
+                      int stride_h, int stride_w, int pad_h, int pad_w, int layout,
+                      void *workspace, size_t workspace_bytes,
+                      const char *plan, void *stream);
+
+/* Workspace bytes of conv2d_fwd_f32_hw's plan (host only). */
+int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, int S,
+                                      int stride_h, int stride_w, int pad_h, int pad_w,
+                                      int layout, const char *plan, size_t *bytes);
+
+/* y = conv(x, w) with the numerics of the paper's kernel: fp32 operands,
+ * every product and partial sum in fp64, and one round-to-nearest-even to
+ * fp32 per output at the store (Sec. 4.1.1, Alg. 2, which converts each
+ * staged tile to double and computes in double).  Each output is therefore
+ * within one fp32 rounding of its fp64 sum.  On fp64 MFMA (half the fp32
+ * peak).  Separate vertical and horizontal stride and padding as in
+ * conv2d_fwd_f32_hw.  Every output tile is computed whole by one work-group
+ * (no split of the reduction), so no workspace is used.  plan: NULL, or an
+ * override with only the key tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
+ * 64x128, 128x64, 64x64, 32x64, 64x32); split, tail or a kt other than 16
+ * -> MG3M_ERR_PLAN.  Pointers, ownership, validation and errors as for
+ * conv2d_fwd_f32. */
+int conv2d_fwd_f32_acc64(const float *x, const float *w, float *y,
+                         int N, int C, int H, int W, int K, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, int layout,
+                         const char *plan, void *stream);
+
+/* The plan of conv2d_fwd_f32_acc64 for this shape, as text (host only; buffer
+ * rules as conv2d_fwd_f32_plan_string). */
+int conv2d_fwd_f32_acc64_plan_string(int N, int C, int H, int W, int K, int R, int S,
+                                     int stride_h, int stride_w, int pad_h, int pad_w,
+                                     int layout, const char *plan, char *buf, size_t len);
+
 /* The plan the selector (or the override) picks for this shape, as text,
  * e.g. "tile=128x128,waves=2x2,kt=16,split=1,grid=1568,...".  Host only; no
  * HIP call.  buf: host buffer of `len` bytes, always NUL-terminated on
@@ -145,7 +189,7 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,
 /* Measurement hook for timing the main convolution kernel alone with HIP
  * events on the stream it runs on.  start and stop are hipEvent_t handles
  * created by the caller (both non-NULL), or both NULL to clear the hook.  The
- * next compute call (conv2d_fwd_f32 / _ex) made on the calling host thread
+ * next compute call (conv2d_fwd_f32, _ex, _hw or _acc64) made on the calling host thread
  * records start on its stream immediately before launching its main kernel
  * and stop immediately after it -- before any split-K reduction -- and then
  * clears the hook; a call rejected by validation leaves it set.  Returns

@@ -18,7 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmg3m.so")
 SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn.hip", "conv_hwcn_vecc.hip", "conv_hwcn_veca.hip", "conv_hwcn_scalar.hip",
-           "conv_nchw.hip", "conv_launch.hip", "plan.cpp", "abi.cpp"]
+           "conv_nchw.hip", "conv_acc64_hwcn_tap.hip", "conv_acc64_hwcn.hip", "conv_acc64_nchw.hip",
+           "conv_launch.hip", "plan.cpp", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -28,8 +29,14 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# The fp64-accumulating kernels keep their accumulators in VGPRs: left to
+# choose, the compiler carries them across the main loop in VGPRs and copies
+# them into AGPRs around every stage's MFMAs.
+PER_SOURCE = {s: ["-mllvm", "-amdgpu-mfma-vgpr-form=1"] for s in SOURCES if s.startswith("conv_acc64_")}
+
+
 def _compile(src: str, obj: str, extra=()):
-    cmd = [HIPCC, *COMMON, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *COMMON, *PER_SOURCE.get(src, []), *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     p = subprocess.run(cmd, capture_output=True, text=True)
     if p.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{p.stdout}\n{p.stderr}")

@@ -31,29 +31,41 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   return pa < pb + nb && pb < pa + na;
 }
 
-int shape_and_plan(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int layout,
-                   const char* plan, bool x16, bool w16, bool y16, mg3m::ConvShape* s,
-                   mg3m::Plan* p) {
+// A convolution's arguments as the entry points receive them, and which
+// kernel family computes it (fp32 or fp64 accumulation).
+struct Geom {
+  int N, C, H, W, K, R, S;
+  int sh, sw, ph, pw;
+  int layout;
+  bool acc64;
+};
+
+Geom geom(int N, int C, int H, int W, int K, int R, int S, int sh, int sw, int ph, int pw, int layout,
+          bool acc64 = false) {
+  return Geom{N, C, H, W, K, R, S, sh, sw, ph, pw, layout, acc64};
+}
+
+int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16,
+                   mg3m::ConvShape* s, mg3m::Plan* p) {
   std::string err;
-  int rc = mg3m::make_shape(N, C, H, W, K, R, S, stride, pad, layout, s, &err);
+  int rc = mg3m::make_shape(g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout, s, &err);
   if (rc) return fail(rc, err);
-  rc = mg3m::make_plan(*s, plan, x16, w16, y16, p, &err);
+  rc = mg3m::make_plan(*s, plan, g.acc64, x16, w16, y16, p, &err);
   if (rc) return fail(rc, err);
   return MG3M_OK;
 }
 
-int run(const float* x, const float* w, float* y, int N, int C, int H, int W, int K, int R, int S,
-        int stride, int pad, int layout, void* workspace, size_t workspace_bytes, bool own_workspace,
-        const char* plan, void* stream) {
+int run(const float* x, const float* w, float* y, const Geom& g, void* workspace,
+        size_t workspace_bytes, bool own_workspace, const char* plan, void* stream) {
   g_last_error.clear();
   if (x == nullptr || w == nullptr || y == nullptr) return fail(MG3M_ERR_NULL, "x, w and y must be non-NULL");
   if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4))
     return fail(MG3M_ERR_ALIGN, "x, w and y must be 4-byte aligned");
   mg3m::ConvShape s;
   mg3m::Plan p;
-  int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, aligned(x, 16),
-                          aligned(w, 16), aligned(y, 16), &s, &p);
+  int rc = shape_and_plan(g, plan, aligned(x, 16), aligned(w, 16), aligned(y, 16), &s, &p);
   if (rc) return rc;
+  const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
   const size_t xb = 4ull * N * C * H * W, wb = 4ull * K * C * R * S;
   const size_t yb = 4ull * (size_t)s.Mg * (size_t)s.Ng;
   if (overlap(y, yb, x, xb) || overlap(y, yb, w, wb))
@@ -124,22 +136,29 @@ int run(const float* x, const float* w, float* y, int N, int C, int H, int W, in
 
 extern "C" {
 
-int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int* Ho, int* Wo) {
+int conv2d_out_dims_hw(int H, int W, int R, int S, int stride_h, int stride_w, int pad_h, int pad_w,
+                       int* Ho, int* Wo) {
   g_last_error.clear();
   if (Ho == nullptr || Wo == nullptr) return fail(MG3M_ERR_NULL, "Ho and Wo must be non-NULL");
   mg3m::ConvShape s;
   std::string err;
-  int rc = mg3m::make_shape(1, 1, H, W, 1, R, S, stride, pad, MG3M_LAYOUT_HWCN, &s, &err);
+  int rc = mg3m::make_shape(1, 1, H, W, 1, R, S, stride_h, stride_w, pad_h, pad_w, MG3M_LAYOUT_HWCN,
+                            &s, &err);
   if (rc) return fail(rc, err);
   *Ho = s.Ho;
   *Wo = s.Wo;
   return MG3M_OK;
 }
 
+int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int* Ho, int* Wo) {
+  return conv2d_out_dims_hw(H, W, R, S, stride, stride, pad, pad, Ho, Wo);
+}
+
 int conv2d_fwd_f32(const float* x, const float* w, float* y, int N, int C, int H, int W, int K,
                    int R, int S, int stride, int pad, int layout, void* stream) {
   try {
-    return run(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, nullptr, 0, true, nullptr, stream);
+    return run(x, w, y, geom(N, C, H, W, K, R, S, stride, stride, pad, pad, layout), nullptr, 0,
+               true, nullptr, stream);
   } catch (const std::exception& e) {
     return fail(MG3M_ERR_HIP, e.what());
   } catch (...) {
@@ -151,8 +170,8 @@ int conv2d_fwd_f32_ex(const float* x, const float* w, float* y, int N, int C, in
                       int R, int S, int stride, int pad, int layout, void* workspace,
                       size_t workspace_bytes, const char* plan, void* stream) {
   try {
-    return run(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, workspace, workspace_bytes, false,
-               plan, stream);
+    return run(x, w, y, geom(N, C, H, W, K, R, S, stride, stride, pad, pad, layout), workspace,
+               workspace_bytes, false, plan, stream);
   } catch (const std::exception& e) {
     return fail(MG3M_ERR_HIP, e.what());
   } catch (...) {
@@ -160,14 +179,26 @@ int conv2d_fwd_f32_ex(const float* x, const float* w, float* y, int N, int C, in
   }
 }
 
-int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
-                                   int pad, int layout, const char* plan, size_t* bytes) {
+int conv2d_fwd_f32_hw(const float* x, const float* w, float* y, int N, int C, int H, int W, int K,
+                      int R, int S, int stride_h, int stride_w, int pad_h, int pad_w, int layout,
+                      void* workspace, size_t workspace_bytes, const char* plan, void* stream) {
+  try {
+    return run(x, w, y, geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout),
+               workspace, workspace_bytes, false, plan, stream);
+  } catch (const std::exception& e) {
+    return fail(MG3M_ERR_HIP, e.what());
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+static int workspace_bytes(const Geom& g, const char* plan, size_t* bytes) {
   try {
     g_last_error.clear();
     if (bytes == nullptr) return fail(MG3M_ERR_NULL, "bytes must be non-NULL");
     mg3m::ConvShape s;
     mg3m::Plan p;
-    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    int rc = shape_and_plan(g, plan, true, true, true, &s, &p);
     if (rc) return rc;
     *bytes = p.ws_bytes;
     return MG3M_OK;
@@ -176,14 +207,25 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
   }
 }
 
-int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                               int layout, const char* plan, char* buf, size_t len) {
+int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride,
+                                   int pad, int layout, const char* plan, size_t* bytes) {
+  return workspace_bytes(geom(N, C, H, W, K, R, S, stride, stride, pad, pad, layout), plan, bytes);
+}
+
+int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, int S, int stride_h,
+                                      int stride_w, int pad_h, int pad_w, int layout, const char* plan,
+                                      size_t* bytes) {
+  return workspace_bytes(geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout), plan,
+                         bytes);
+}
+
+static int plan_string(const Geom& g, const char* plan, char* buf, size_t len) {
   try {
     g_last_error.clear();
     if (buf == nullptr) return fail(MG3M_ERR_NULL, "buf must be non-NULL");
     mg3m::ConvShape s;
     mg3m::Plan p;
-    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    int rc = shape_and_plan(g, plan, true, true, true, &s, &p);
     if (rc) return rc;
     std::string text = mg3m::plan_to_string(s, p);
     if (len < text.size() + 1) return fail(MG3M_ERR_ARG, "buffer too short for the plan string");
@@ -194,6 +236,31 @@ int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S, 
   }
 }
 
+int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                               int layout, const char* plan, char* buf, size_t len) {
+  return plan_string(geom(N, C, H, W, K, R, S, stride, stride, pad, pad, layout), plan, buf, len);
+}
+
+int conv2d_fwd_f32_acc64(const float* x, const float* w, float* y, int N, int C, int H, int W,
+                         int K, int R, int S, int stride_h, int stride_w, int pad_h, int pad_w,
+                         int layout, const char* plan, void* stream) {
+  try {
+    return run(x, w, y, geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout, true),
+               nullptr, 0, false, plan, stream);
+  } catch (const std::exception& e) {
+    return fail(MG3M_ERR_HIP, e.what());
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv2d_fwd_f32_acc64_plan_string(int N, int C, int H, int W, int K, int R, int S, int stride_h,
+                                     int stride_w, int pad_h, int pad_w, int layout, const char* plan,
+                                     char* buf, size_t len) {
+  return plan_string(geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout, true), plan,
+                     buf, len);
+}
+
 int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                              int layout, const char* plan, mg3m_plan_info* info) {
   try {
@@ -201,7 +268,8 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     if (info == nullptr) return fail(MG3M_ERR_NULL, "info must be non-NULL");
     mg3m::ConvShape s;
     mg3m::Plan p;
-    int rc = shape_and_plan(N, C, H, W, K, R, S, stride, pad, layout, plan, true, true, true, &s, &p);
+    int rc = shape_and_plan(geom(N, C, H, W, K, R, S, stride, stride, pad, pad, layout), plan, true,
+                            true, true, &s, &p);
     if (rc) return rc;
     info->mt = p.t.mt; info->nt = p.t.nt; info->kt = p.t.kt;
     info->waves_m = p.t.wm; info->waves_n = p.t.wn;

@@ -50,6 +50,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // are limited to kMaxTensorBytes): a raw buffer load there returns zero.
 constexpr unsigned kOOB = 0xFFFFFFC0u;
 
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float* p, unsigned bytes) {
   // stride 0 (raw buffer), num_records = bytes, 32-bit data format.
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, (int)bytes, 0x00020000);
@@ -62,23 +64,31 @@ __device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, unsigned off) 
 }
 __device__ __forceinline__ void st4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 
-template <int MT, int NT, int KT, int WM, int WN>
+// Tile geometry.  ACC64 selects the fp64-accumulating kernel's LDS padding:
+// its 16x16x4 MFMA fragments read four k-rows per instruction, so rows are
+// padded by 16 floats instead of 32 to keep the four rows on distinct banks.
+template <int MT, int NT, int KT, int WM, int WN, bool ACC64 = false>
 struct Cfg {
   static constexpr int T = WM * WN * 64;        // threads per work-group
   static constexpr int WTM = MT / WM;           // wave tile rows
   static constexpr int WTN = NT / WN;           // wave tile columns
   static constexpr int TM = WTM / 32;           // 32x32 MFMA blocks per wave, rows
   static constexpr int TN = WTN / 32;           // ... columns
-  static constexpr int AS = lds_row_stride(MT);
-  static constexpr int BS = lds_row_stride(NT);
+  static constexpr int TM16 = WTM / 16;         // 16x16 MFMA blocks per wave (fp64), rows
+  static constexpr int TN16 = WTN / 16;         // ... columns
+  static constexpr int AS = ACC64 ? lds_row_stride64(MT) : lds_row_stride(MT);
+  static constexpr int BS = ACC64 ? lds_row_stride64(NT) : lds_row_stride(NT);
   static constexpr int A_STAGE = KT * AS;
   static constexpr int B_STAGE = KT * BS;
   static constexpr int LDS_FLOATS = 2 * A_STAGE + 2 * B_STAGE;
   static constexpr int A_ELEMS = KT * MT / T;    // A elements each thread loads per stage
   static constexpr int B_ELEMS = KT * NT / T;
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
-  static_assert(KT % 2 == 0, "the 32x32x2 MFMA consumes two reduction rows");
-  static_assert(LDS_FLOATS * 4 == lds_bytes_for(TileDesc{MT, NT, KT, WM, WN, 0, 0.0}), "LDS size model");
+  static_assert(ACC64 || (WTM % 32 == 0 && WTN % 32 == 0), "wave tile must be whole 32x32 blocks");
+  static_assert(!ACC64 || (WTM % 16 == 0 && WTN % 16 == 0), "wave tile must be whole 16x16 blocks");
+  static_assert(KT % 4 == 0, "MFMA steps consume 2 (fp32) or 4 (fp64) reduction rows");
+  static_assert(LDS_FLOATS * 4 == (ACC64 ? lds_bytes_for64(TileDesc{MT, NT, KT, WM, WN, 0, 0.0})
+                                         : lds_bytes_for(TileDesc{MT, NT, KT, WM, WN, 0, 0.0})),
+                "LDS size model");
 };
 
 // Reduction index k -> (filter row r, filter column s, input channel c).
@@ -511,6 +521,101 @@ __device__ __forceinline__ void mma_stage(floatx16 (&acc)[C::TM][C::TN], const f
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
 }
 
+// fp64 16x16x4 MFMA operand layout (checked on gfx950): lane (g, q) =
+// (lane / 16, lane % 16) supplies A[row q][k = g] and B[k = g][column q].  The fp32 operands are
+// widened exactly, so every product is exact and only the fp64 additions
+// round.
+template <class C, int KT>
+__device__ __forceinline__ void mma_stage64(f64x4 (&acc)[C::TM16][C::TN16], const float* As,
+                                            const float* Bs, int wm, int wn, int g, int q) {
+  const float* Ac = As + wm * C::WTM + q;
+  const float* Bc = Bs + wn * C::WTN + q;
+#pragma unroll
+  for (int kk = 0; kk < KT / 4; ++kk) {
+    double av[C::TM16], bv[C::TN16];
+#pragma unroll
+    for (int i = 0; i < C::TM16; ++i) av[i] = (double)Ac[(4 * kk + g) * C::AS + i * 16];
+#pragma unroll
+    for (int j = 0; j < C::TN16; ++j) bv[j] = (double)Bc[(4 * kk + g) * C::BS + j * 16];
+#pragma unroll
+    for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN16; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
+  }
+}
+
+// ------------------------------------------------------ stage pipeline
+// Runs nk stages of the reduction through the two LDS buffers, calling
+// compute(As, Bs) on each staged pair.  The loads of stage it+1 are issued
+// before stage it's MFMAs and land in the other buffer after them; one
+// barrier per stage.  Buffer cur^1 was last read in iteration it-1, which
+// every wave finished before the barrier that ended it.  Stages alternate
+// between the two buffers, so the loop is unrolled by two to make the buffer
+// offsets compile-time constants.
+template <class C, class AL, class BL, class F>
+__device__ __forceinline__ void run_stages(const KArgs& a, AL& al, BL& bl, float* As0, float* Bs0,
+                                           int nk, __amdgpu_buffer_rsrc_t xr,
+                                           __amdgpu_buffer_rsrc_t wr, F&& compute) {
+  if (nk <= 0) return;
+  al.load(a, wr);
+  bl.load(a, xr);
+  al.store(As0);
+  bl.store(Bs0);
+  __syncthreads();
+  auto step = [&](auto cur_c) {
+    constexpr int CUR = decltype(cur_c)::value;
+    al.advance(a);
+    bl.advance(a);
+    al.load(a, wr);
+    bl.load(a, xr);
+    // keep the global loads ahead of the MFMAs (the scheduler would
+    // otherwise sink them next to their LDS stores and expose their latency)
+    __builtin_amdgcn_sched_barrier(0);
+    compute(As0 + CUR * C::A_STAGE, Bs0 + CUR * C::B_STAGE);
+    __builtin_amdgcn_sched_barrier(0);
+    al.store(As0 + (CUR ^ 1) * C::A_STAGE);
+    bl.store(Bs0 + (CUR ^ 1) * C::B_STAGE);
+    __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  int it = 0;
+  for (; it + 2 <= nk - 1; it += 2) {
+    step(B0{});
+    step(B1{});
+  }
+  if (it < nk - 1) {
+    step(B0{});
+    ++it;
+  }
+  const int last = it & 1;
+  compute(As0 + last * C::A_STAGE, Bs0 + last * C::B_STAGE);
+}
+
+// ------------------------------------------------------ tile mapping
+// XCD grouping of the whole tiles: work-group i runs on XCD i % 8, so the G
+// whole tiles are renumbered to give each XCD a contiguous run of them (tiles
+// sharing a patch tile or halo rows then share one L2).  The runs differ in
+// length by at most one.  Work-groups at or past G keep their number.
+__device__ __forceinline__ int xcd_group(int L, int G) {
+  if (L >= G) return L;
+  const int q8 = G >> 3, r8 = G & 7, xcd = L & 7, loc = L >> 3;
+  return (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
+}
+
+// Output element (m, n) sits at out_colbase(n) + m * mstride in either layout.
+template <int LAYOUT>
+__device__ __forceinline__ int out_colbase(const KArgs& a, int n) {
+  if constexpr (LAYOUT == kHWCN) {
+    const int pix = n / a.N, b = n - pix * a.N;
+    return pix * a.K * a.N + b;
+  } else {
+    const int hw = a.Ho * a.Wo, b = n / hw, pix = n - b * hw;
+    return b * a.K * hw + pix;
+  }
+}
+
 // ------------------------------------------------------------------ kernel
 template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64)
@@ -523,18 +628,11 @@ void conv_igemm_f32(KArgs a) {
   // Work-group -> (tile, range of k-tiles).  Work-groups [0, dp_tiles) each
   // compute one whole tile; the rest compute one chunk of kps k-tiles of a
   // tail tile, consecutive work-groups taking different tiles of the same
-  // chunk.  The whole tiles are regrouped so that each XCD gets a contiguous
-  // run of them (tiles sharing a patch tile or halo rows then share one L2);
-  // the tail chunks keep their place at the end of the dispatch order.
-  int L = blockIdx.x;
-  if (L < a.dp_tiles) {
-    // XCD grouping of the whole tiles only (tail chunks keep their place at
-    // the end of the dispatch order): work-group i runs on XCD i % 8, so give
-    // each XCD a contiguous run of tiles.  dp_tiles is a multiple of 8
-    // whenever there is a tail; otherwise the runs differ by one.
-    const int G = a.dp_tiles, q8 = G >> 3, r8 = G & 7, xcd = L & 7, loc = L >> 3;
-    L = (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
-  }
+  // chunk.
+  // The whole tiles are regrouped per XCD; the tail chunks keep their place
+  // at the end of the dispatch order (dp_tiles is a multiple of 8 whenever
+  // there is a tail).
+  const int L = xcd_group(blockIdx.x, a.dp_tiles);
   int tile, kt0, nk, chunk = 0;
   const bool partial = L >= a.dp_tiles;
   if (!partial) {
@@ -576,47 +674,9 @@ void conv_igemm_f32(KArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  if (nk > 0) {
-    al.load(a, wr);
-    bl.load(a, xr);
-    al.store(As0);
-    bl.store(Bs0);
-    __syncthreads();
-    // Steady state: the loads of stage it+1 are issued before the MFMAs of
-    // stage it and land in the other LDS buffer after them; one barrier per
-    // stage.  Buffer cur^1 was last read in iteration it-1, which every wave
-    // finished before the barrier that ended it.  Stages alternate between
-    // the two buffers, so the loop is unrolled by two to make the buffer
-    // offsets compile-time constants.
-    auto step = [&](auto cur_c) {
-      constexpr int CUR = decltype(cur_c)::value;
-      al.advance(a);
-      bl.advance(a);
-      al.load(a, wr);
-      bl.load(a, xr);
-      // keep the global loads ahead of the MFMAs (the scheduler would
-      // otherwise sink them next to their LDS stores and expose their latency)
-      __builtin_amdgcn_sched_barrier(0);
-      mma_stage<C, KT>(acc, As0 + CUR * C::A_STAGE, Bs0 + CUR * C::B_STAGE, wm, wn, hh, q);
-      __builtin_amdgcn_sched_barrier(0);
-      al.store(As0 + (CUR ^ 1) * C::A_STAGE);
-      bl.store(Bs0 + (CUR ^ 1) * C::B_STAGE);
-      __syncthreads();
-    };
-    using B0 = std::integral_constant<int, 0>;
-    using B1 = std::integral_constant<int, 1>;
-    int it = 0;
-    for (; it + 2 <= nk - 1; it += 2) {
-      step(B0{});
-      step(B1{});
-    }
-    if (it < nk - 1) {
-      step(B0{});
-      ++it;
-    }
-    const int last = it & 1;
-    mma_stage<C, KT>(acc, As0 + last * C::A_STAGE, Bs0 + last * C::B_STAGE, wm, wn, hh, q);
-  }
+  run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
+    mma_stage<C, KT>(acc, As, Bs, wm, wn, hh, q);
+  });
 
   // Epilogue, straight from the accumulators.  32x32 accumulator layout:
   // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
@@ -636,20 +696,12 @@ void conv_igemm_f32(KArgs a) {
     }
     return;
   }
-  // Output element (m, n) sits at colbase(n) + m*mstride in either layout.
   float* const out = a.y;
 #pragma unroll
   for (int j = 0; j < C::TN; ++j) {
     const int n = n0 + wn * C::WTN + j * 32 + q;
     if (n >= a.Ng) continue;
-    int colbase;
-    if constexpr (LAYOUT == kHWCN) {
-      const int pix = n / a.N, b = n - pix * a.N;
-      colbase = pix * a.K * a.N + b;
-    } else {
-      const int hw = a.Ho * a.Wo, b = n / hw, pix = n - b * hw;
-      colbase = b * a.K * hw + pix;
-    }
+    const int colbase = out_colbase<LAYOUT>(a, n);
 #pragma unroll
     for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -686,6 +738,85 @@ template <int LAYOUT, int AM, int BM>
 KernelFn kernel_for_tile(int tile) {
   if (tile < 0 || tile >= kNumTiles) return nullptr;
   return pick_tile<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles>{});
+}
+
+// ------------------------------------------------- fp64-accumulating kernel
+// Same operand staging as conv_igemm_f32 (fp32 tiles in LDS); the MFMAs take
+// the operands widened to fp64 and accumulate in fp64, and each output is
+// rounded to fp32 once, at the store.  Every tile is computed whole (no
+// reduction split), so the sum never leaves fp64 before that rounding.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_acc64(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN, true>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  const int t = threadIdx.x;
+  const int tile = xcd_group(blockIdx.x, a.dp_tiles);
+  const int tm = tile % a.tiles_m;
+  const int tn = tile / a.tiles_m;
+  const int m0 = tm * MT, n0 = tn * NT;
+
+  float* const As0 = lds;
+  float* const Bs0 = lds + 2 * C::A_STAGE;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+
+  typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
+  typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
+  al.init(a, t, m0, 0);
+  bl.init(a, t, n0, 0);
+
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave % WM, wn = wave / WM;
+  const int g = lane >> 4, q = lane & 15;
+
+  f64x4 acc[C::TM16][C::TN16];
+#pragma unroll
+  for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN16; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+
+  run_stages<C>(a, al, bl, As0, Bs0, a.k_tiles, xr, wr, [&](const float* As, const float* Bs) {
+    mma_stage64<C, KT>(acc, As, Bs, wm, wn, g, q);
+  });
+
+  // 16x16 fp64 accumulator layout: element e of lane (g, q) holds row
+  // g + 4*e, column q.  A lane's four rows are not adjacent, so the stores
+  // are single elements (lanes g = 0..3 together cover four adjacent rows).
+  float* const out = a.y;
+#pragma unroll
+  for (int j = 0; j < C::TN16; ++j) {
+    const int n = n0 + wn * C::WTN + j * 16 + q;
+    if (n >= a.Ng) continue;
+    const int colbase = out_colbase<LAYOUT>(a, n);
+#pragma unroll
+    for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = m0 + wm * C::WTM + i * 16 + g + 4 * e;
+        if (row < a.Mg) out[colbase + row * a.mstride] = (float)acc[i][j][e];
+      }
+  }
+}
+
+template <int LAYOUT, int AM, int BM, int TI>
+constexpr KernelFn kernel64_at() {
+  constexpr TileDesc d = kTiles64[TI];
+  return &conv_igemm_acc64<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn>;
+}
+
+template <int LAYOUT, int AM, int BM, int... TI>
+KernelFn pick_tile64(int tile, std::integer_sequence<int, TI...>) {
+  KernelFn fn = nullptr;
+  ((fn = (tile == TI ? kernel64_at<LAYOUT, AM, BM, TI>() : fn)), ...);
+  return fn;
+}
+
+template <int LAYOUT, int AM, int BM>
+KernelFn kernel64_for_tile(int tile) {
+  if (tile < 0 || tile >= kNumTiles64) return nullptr;
+  return pick_tile64<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles64>{});
 }
 
 }  // namespace mg3m

@@ -62,8 +62,21 @@ static KernelFn kernel_for(int variant, int tile) {
   }
 }
 
+static KernelFn kernel64_for(int variant, int tile) {
+  switch (variant) {
+    case kVarHwcnVecNTap: return conv_kernel64_hwcn_vecn_tap(tile);
+    case kVarHwcnVecN:
+    case kVarHwcnVecC:
+    case kVarHwcnVecA:
+    case kVarHwcnScalar: return conv_kernel64_hwcn(variant, tile);
+    case kVarNchwVecA:
+    case kVarNchwScalar: return conv_kernel64_nchw(variant, tile);
+    default: return nullptr;
+  }
+}
+
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
-  KernelFn fn = kernel_for(p.variant, p.tile);
+  KernelFn fn = p.acc64 ? kernel64_for(p.variant, p.tile) : kernel_for(p.variant, p.tile);
   if (fn == nullptr) {
     *err = "internal: no kernel for this loader variant and tile";
     return MG3M_ERR_PLAN;

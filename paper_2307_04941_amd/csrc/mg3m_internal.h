@@ -85,6 +85,33 @@ constexpr int lds_row_stride(int dim) { return dim % 64 == 0 ? dim + 32 : dim; }
 constexpr int lds_bytes_for(const TileDesc& t) {
   return 4 * (2 * t.kt * lds_row_stride(t.mt) + 2 * t.kt * lds_row_stride(t.nt));
 }
+// The fp64-accumulating kernel's 16x16x4 fragments read four k-rows of 16
+// floats per instruction; a row stride of 16 (mod 32) floats puts the four
+// rows on disjoint banks.
+constexpr int lds_row_stride64(int dim) { return dim % 32 == 0 ? dim + 16 : dim; }
+constexpr int lds_bytes_for64(const TileDesc& t) {
+  return 4 * (2 * t.kt * lds_row_stride64(t.mt) + 2 * t.kt * lds_row_stride64(t.nt));
+}
+
+// Tile menu of the fp64-accumulating kernel (fp32 operands, every product and
+// partial sum in fp64, one rounding to fp32 at the store: the numerics of the
+// paper's kernel, Sec. 4.1.1 and Alg. 2).  It runs data parallel only.  regs
+// as above.  eff is not a measured fraction here: on full layers every tile
+// of this menu sustains 80-87% of the fp64 MFMA peak on MI355X, and these
+// values are the ones with which the cost model's pick per layer matched the
+// fastest tile measured on the VGG-16 and ResNet-50 layers (within 1% in
+// total time; the model's occupancy term already favours the small tiles).
+constexpr int kNumTiles64 = 8;
+inline constexpr TileDesc kTiles64[kNumTiles64] = {
+    {128, 128, 16, 2, 2, 190, 0.80},   // 0
+    {64, 256, 16, 1, 4, 194, 0.80},    // 1
+    {256, 64, 16, 4, 1, 194, 0.80},    // 2
+    {64, 128, 16, 1, 2, 198, 0.75},    // 3
+    {128, 64, 16, 2, 1, 198, 0.75},    // 4
+    {64, 64, 16, 1, 1, 196, 0.70},     // 5
+    {32, 64, 16, 1, 2, 80, 0.60},      // 6
+    {64, 32, 16, 2, 1, 80, 0.60},      // 7
+};
 
 // Largest tensor the kernels address: byte offsets are 32-bit and 0xFFFFFFC0
 // is reserved as the out-of-range offset that reads as zero.
@@ -102,7 +129,8 @@ constexpr long long kMaxTensorBytes = 0xFFFFFFC0LL;
 // running mostly empty.
 struct Plan {
   int layout;
-  int tile;                 // index into kTiles
+  int acc64;                // 1: the fp64-accumulating kernel (tile indexes kTiles64)
+  int tile;                 // index into kTiles (kTiles64 when acc64)
   TileDesc t;
   int k_tiles;              // ceil(Kg / kt)
   int tiles_m, tiles_n;
@@ -146,10 +174,10 @@ struct RArgs {
 
 // Planner (host only, no HIP calls).  Returns 0 or an mg3m_status code and
 // fills *err with a message on failure.
-int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-               int layout, ConvShape* s, std::string* err);
-int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16, bool y16,
-              Plan* p, std::string* err);
+int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride_h, int stride_w,
+               int pad_h, int pad_w, int layout, ConvShape* s, std::string* err);
+int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x16, bool w16,
+              bool y16, Plan* p, std::string* err);
 std::string plan_to_string(const ConvShape& s, const Plan& p);
 
 // Kernel entry points by (variant, tile): conv_hwcn_*.hip, conv_nchw.hip.
@@ -160,6 +188,10 @@ KernelFn conv_kernel_hwcn_vecc(int tile);
 KernelFn conv_kernel_hwcn_veca(int tile);
 KernelFn conv_kernel_hwcn_scalar(int tile);
 KernelFn conv_kernel_nchw(int variant, int tile);
+// fp64-accumulating kernels by (variant, tile): conv_acc64_*.hip.
+KernelFn conv_kernel64_hwcn_vecn_tap(int tile);
+KernelFn conv_kernel64_hwcn(int variant, int tile);
+KernelFn conv_kernel64_nchw(int variant, int tile);
 
 // Kernel launchers (conv_launch.hip).
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);

@@ -26,6 +26,7 @@ namespace {
 constexpr int kCUs = 256;                    // MI355X: 8 XCDs x 32 CUs
 constexpr double kClockHz = 2.4e9;
 constexpr double kFlopPerClkCU = 256.0;      // fp32 MFMA: 4 SIMDs x 64 flop/clk
+constexpr double kFlopPerClkCU64 = 128.0;    // fp64 MFMA: 4 SIMDs x 32 flop/clk
 constexpr int kLdsBytesPerCU = 160 * 1024;
 constexpr int kRegsPerLane = 512;            // unified VGPR + AGPR file per SIMD lane
 constexpr int kMaxWavesPerSimd = 8;
@@ -40,13 +41,16 @@ constexpr double kUtilBase = 0.4, kUtilPerWave = 0.2;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
+const TileDesc& tile_desc(bool acc64, int i) { return acc64 ? kTiles64[i] : kTiles[i]; }
+int lds_bytes(const TileDesc& t, bool acc64) { return acc64 ? lds_bytes_for64(t) : lds_bytes_for(t); }
+
 // Work-groups of this tile resident on one CU, limited by LDS and registers.
-int resident_wgs(const TileDesc& t) {
+int resident_wgs(const TileDesc& t, bool acc64) {
   const int waves = t.wm * t.wn;
   const int regs = (t.regs + 7) / 8 * 8;
   const int waves_per_simd = std::min(kMaxWavesPerSimd, kRegsPerLane / regs);
   const int by_regs = std::max(1, 4 * waves_per_simd / waves);
-  const int by_lds = std::max(1, kLdsBytesPerCU / lds_bytes_for(t));
+  const int by_lds = std::max(1, kLdsBytesPerCU / lds_bytes(t, acc64));
   return std::min(by_regs, by_lds);
 }
 
@@ -131,9 +135,10 @@ enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2 };
 
 // Fill the shape-dependent parts of a plan for one (tile, schedule, split)
 // choice.  Returns false when the tile count does not fit a launch.
-bool shape_plan(const ConvShape& s, int tile, int sched, int split_req, Plan* p) {
-  const TileDesc& t = kTiles[tile];
+bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, int split_req, Plan* p) {
+  const TileDesc& t = tile_desc(acc64, tile);
   p->layout = s.layout;
+  p->acc64 = acc64 ? 1 : 0;
   p->tile = tile;
   p->t = t;
   p->k_tiles = (int)cdiv(s.Kg, t.kt);
@@ -150,7 +155,7 @@ bool shape_plan(const ConvShape& s, int tile, int sched, int split_req, Plan* p)
   } else {
     // whole rounds of resident work-groups run unsplit (none if the tiles do
     // not fill one round: then every tile is split)
-    const long long slots = (long long)kCUs * resident_wgs(t);
+    const long long slots = (long long)kCUs * resident_wgs(t, acc64);
     const long long dp = tiles / slots * slots;
     p->dp_tiles = (int)dp;
     p->tail_tiles = (int)(tiles - dp);
@@ -168,7 +173,7 @@ bool shape_plan(const ConvShape& s, int tile, int sched, int split_req, Plan* p)
     }
   }
   p->grid = (long long)p->dp_tiles + (long long)p->tail_tiles * p->split;
-  p->lds_bytes = lds_bytes_for(t);
+  p->lds_bytes = lds_bytes(t, acc64);
   const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
                         (double)p->k_tiles * t.kt;
   p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
@@ -186,7 +191,8 @@ bool shape_plan(const ConvShape& s, int tile, int sched, int split_req, Plan* p)
 // partials) once; the tail reduction adds its traffic and a second launch.
 double predict_us(const ConvShape& s, const Plan& p) {
   const TileDesc& t = p.t;
-  const int occ = resident_wgs(t);
+  const int occ = resident_wgs(t, p.acc64);
+  const double rate = p.acc64 ? kFlopPerClkCU64 : kFlopPerClkCU;
   const double tile_flops = 2.0 * t.mt * t.nt * (double)t.kt;
   auto phase = [&](long long wgs, int k_tiles) {
     if (wgs <= 0) return 0.0;
@@ -194,7 +200,7 @@ double predict_us(const ConvShape& s, const Plan& p) {
     const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
     const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
     const double eff = t.eff * variant_factor(p.variant) * util;
-    return (double)per_cu * tile_flops * k_tiles / (kFlopPerClkCU * kClockHz * eff) * 1e6 +
+    return (double)per_cu * tile_flops * k_tiles / (rate * kClockHz * eff) * 1e6 +
            (double)cdiv(per_cu, occ) * kRoundUs;
   };
   const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase((long long)p.tail_tiles * p.split, p.kps);
@@ -212,30 +218,34 @@ double predict_us(const ConvShape& s, const Plan& p) {
 
 }  // namespace
 
-int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int layout,
-               ConvShape* s, std::string* err) {
+int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride_h, int stride_w,
+               int pad_h, int pad_w, int layout, ConvShape* s, std::string* err) {
   if (layout != kHWCN && layout != kNCHW) {
     *err = "unknown layout";
     return MG3M_ERR_LAYOUT;
   }
-  if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) {
-    *err = "dimensions and stride must be >= 1, pad >= 0";
+  if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride_h < 1 ||
+      stride_w < 1 || pad_h < 0 || pad_w < 0) {
+    *err = "dimensions and strides must be >= 1, pads >= 0";
     return MG3M_ERR_SHAPE;
   }
-  if (pad > (1 << 24) || H > (1 << 24) || W > (1 << 24) || R > (1 << 24) || S > (1 << 24)) {
-    *err = "a spatial size or pad exceeds 2^24";
+  if (pad_h > (1 << 24) || pad_w > (1 << 24) || H > (1 << 24) || W > (1 << 24) ||
+      R > (1 << 24) || S > (1 << 24) || stride_h > (1 << 24) || stride_w > (1 << 24)) {
+    *err = "a spatial size, stride or pad exceeds 2^24";
     return MG3M_ERR_TOO_LARGE;
   }
-  const long long eh = (long long)H + 2LL * pad - R, ew = (long long)W + 2LL * pad - S;
+  const long long eh = (long long)H + 2LL * pad_h - R, ew = (long long)W + 2LL * pad_w - S;
   if (eh < 0 || ew < 0) {
     *err = "filter larger than the padded input: empty output";
     return MG3M_ERR_SHAPE;
   }
   s->N = N; s->C = C; s->H = H; s->W = W; s->K = K; s->R = R; s->S = S;
-  s->sh = s->sw = stride;
-  s->ph = s->pw = pad;
-  s->Ho = (int)(eh / stride + 1);
-  s->Wo = (int)(ew / stride + 1);
+  s->sh = stride_h;
+  s->sw = stride_w;
+  s->ph = pad_h;
+  s->pw = pad_w;
+  s->Ho = (int)(eh / stride_h + 1);
+  s->Wo = (int)(ew / stride_w + 1);
   s->layout = layout;
   s->Mg = K;
   s->Ng = (long long)N * s->Ho * s->Wo;
@@ -275,13 +285,19 @@ void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
   // the split-K workspace is 256-byte aligned and has the output's layout.
   const bool out16 = p->split > 1 ? true : y16;
   p->e_mode = (s.layout == kHWCN && s.N == 1 && s.K % 4 == 0 && out16) ? kEVecM : kEElem;
+  // the fp64 accumulator holds no four adjacent rows in one lane
+  if (p->acc64) p->e_mode = kEElem;
 }
 
-int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16, bool y16,
-              Plan* p, std::string* err) {
+int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x16, bool w16,
+              bool y16, Plan* p, std::string* err) {
   Override o;
   int rc = parse_override(override_text, &o, err);
   if (rc) return rc;
+  if (acc64 && (o.split > 1 || o.tail || (o.kt && o.kt != 16))) {
+    *err = "plan override: the fp64-accumulating kernel computes every tile whole with kt=16";
+    return MG3M_ERR_PLAN;
+  }
 
   int best = -1;
   Plan best_plan{};
@@ -289,7 +305,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
   const int splits[] = {2, 3, 4, 6, 8, 16};
   auto consider = [&](int ti, int sched, int sp) {
     Plan c{};
-    if (!shape_plan(s, ti, sched, sp, &c)) return;
+    if (!shape_plan(s, acc64, ti, sched, sp, &c)) return;
     choose_modes(s, x16, w16, y16, &c);
     c.est_us = predict_us(s, c);
     // ties: less workspace traffic, then the larger tile
@@ -302,11 +318,14 @@ int make_plan(const ConvShape& s, const char* override_text, bool x16, bool w16,
       best_plan = c;
     }
   };
-  for (int ti = 0; ti < kNumTiles; ++ti) {
-    if (o.mt && !(kTiles[ti].mt == o.mt && kTiles[ti].nt == o.nt)) continue;
+  for (int ti = 0; ti < (acc64 ? kNumTiles64 : kNumTiles); ++ti) {
+    const TileDesc& td = tile_desc(acc64, ti);
+    if (o.mt && !(td.mt == o.mt && td.nt == o.nt)) continue;
     // a forced tile without a depth means the default depth of 16
-    if ((o.kt || o.mt) && kTiles[ti].kt != (o.kt ? o.kt : 16)) continue;
-    if (o.split) {
+    if ((o.kt || o.mt) && td.kt != (o.kt ? o.kt : 16)) continue;
+    if (acc64) {
+      consider(ti, kDataParallel, 1);
+    } else if (o.split) {
       consider(ti, o.split > 1 ? kSplitAll : kDataParallel, o.split);
     } else if (o.tail) {
       consider(ti, kSplitTail, o.tail);
@@ -334,10 +353,10 @@ std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
-                "tile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,grid=%lld,"
+                "%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,grid=%lld,"
                 "tiles=%dx%d,k_tiles=%d,a=%s,b=%s,e=%s,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
                 "Mg=%lld,Ng=%lld,Kg=%lld",
-                p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.grid,
+                p.acc64 ? "acc=f64," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.grid,
                 p.tiles_m, p.tiles_n, p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode],
                 p.lds_bytes, p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
   return buf;

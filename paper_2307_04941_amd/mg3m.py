@@ -63,7 +63,13 @@ def load_library(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     i, p, sz, cp = ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_char_p
     shape = [i] * 10                     # N, C, H, W, K, R, S, stride, pad, layout
+    shape_hw = [i] * 12                  # N, C, H, W, K, R, S, sh, sw, ph, pw, layout
     lib.conv2d_out_dims.argtypes = [i] * 6 + [ctypes.POINTER(i)] * 2
+    lib.conv2d_out_dims_hw.argtypes = [i] * 8 + [ctypes.POINTER(i)] * 2
+    lib.conv2d_fwd_f32_hw.argtypes = [p, p, p] + shape_hw + [p, sz, cp, p]
+    lib.conv2d_fwd_f32_hw_workspace_bytes.argtypes = shape_hw + [cp, ctypes.POINTER(sz)]
+    lib.conv2d_fwd_f32_acc64.argtypes = [p, p, p] + shape_hw + [cp, p]
+    lib.conv2d_fwd_f32_acc64_plan_string.argtypes = shape_hw + [cp, ctypes.c_char_p, sz]
     lib.conv2d_fwd_f32.argtypes = [p, p, p] + shape + [p]
     lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
     lib.conv2d_fwd_f32_workspace_bytes.argtypes = shape + [cp, ctypes.POINTER(sz)]
@@ -75,7 +81,9 @@ def load_library(path: str = LIB_PATH):
     lib.mg3m_status_string.restype = ctypes.c_char_p
     lib.mg3m_last_error.argtypes = []
     lib.mg3m_last_error.restype = ctypes.c_char_p
-    for name in ("conv2d_out_dims", "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
+    for name in ("conv2d_out_dims", "conv2d_out_dims_hw", "conv2d_fwd_f32_hw",
+                 "conv2d_fwd_f32_hw_workspace_bytes", "conv2d_fwd_f32_acc64",
+                 "conv2d_fwd_f32_acc64_plan_string", "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
                  "conv2d_fwd_f32_workspace_bytes", "conv2d_fwd_f32_plan_string",
                  "conv2d_fwd_f32_plan_info", "mg3m_padding_overhead", "mg3m_time_next_kernel"):
         getattr(lib, name).restype = i
@@ -136,6 +144,46 @@ def conv2d_out_dims(H, W, R, S, stride, pad):
     ho, wo = ctypes.c_int(), ctypes.c_int()
     _check(load_library().conv2d_out_dims(H, W, R, S, stride, pad, ctypes.byref(ho), ctypes.byref(wo)))
     return ho.value, wo.value
+
+
+def conv2d_out_dims_hw(H, W, R, S, stride_h, stride_w, pad_h, pad_w):
+    ho, wo = ctypes.c_int(), ctypes.c_int()
+    _check(load_library().conv2d_out_dims_hw(H, W, R, S, stride_h, stride_w, pad_h, pad_w,
+                                             ctypes.byref(ho), ctypes.byref(wo)))
+    return ho.value, wo.value
+
+
+def conv2d_fwd_f32_hw(x, w, y, N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout,
+                      workspace=None, workspace_bytes=0, plan=None, stream=None):
+    _check(load_library().conv2d_fwd_f32_hw(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
+                                            stride_h, stride_w, pad_h, pad_w, _layout(layout),
+                                            _ptr(workspace), workspace_bytes, _enc(plan),
+                                            _stream(stream)))
+
+
+def conv2d_fwd_f32_hw_workspace_bytes(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w,
+                                      layout, plan=None) -> int:
+    b = ctypes.c_size_t()
+    _check(load_library().conv2d_fwd_f32_hw_workspace_bytes(
+        N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, _layout(layout), _enc(plan),
+        ctypes.byref(b)))
+    return b.value
+
+
+def conv2d_fwd_f32_acc64(x, w, y, N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout,
+                         plan=None, stream=None):
+    _check(load_library().conv2d_fwd_f32_acc64(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
+                                               stride_h, stride_w, pad_h, pad_w, _layout(layout),
+                                               _enc(plan), _stream(stream)))
+
+
+def conv2d_fwd_f32_acc64_plan_string(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout,
+                                     plan=None) -> str:
+    buf = ctypes.create_string_buffer(1024)
+    _check(load_library().conv2d_fwd_f32_acc64_plan_string(
+        N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, _layout(layout), _enc(plan), buf,
+        len(buf)))
+    return buf.value.decode()
 
 
 def conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):
@@ -202,24 +250,44 @@ def dims_of(x, w, layout):
     return N, C, H, W, K, R, S
 
 
-def conv2d_fwd(x, w, stride: int = 1, pad: int = 0, layout="HWCN", plan: Optional[str] = None,
-               out=None, workspace=None, stream=None):
+def _pair(v):
+    if isinstance(v, (tuple, list)):
+        return int(v[0]), int(v[1])
+    return int(v), int(v)
+
+
+def conv2d_fwd(x, w, stride=1, pad=0, layout="HWCN", plan: Optional[str] = None,
+               out=None, workspace=None, stream=None, acc64: bool = False):
     """y = conv(x, w) for torch tensors on the GPU; allocates y unless `out`
-    is given.  With `plan` or `workspace` the _ex entry point is used."""
+    is given.  stride and pad: an int, or (vertical, horizontal).  With
+    `plan`, `workspace` or unequal per-axis values the _ex / _hw entry
+    points are used (workspace allocated here when needed).  acc64=True
+    uses conv2d_fwd_f32_acc64 (fp64 accumulation, no workspace)."""
     import torch
     N, C, H, W, K, R, S = dims_of(x, w, layout)
-    Ho, Wo = conv2d_out_dims(H, W, R, S, stride, pad)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv2d_out_dims_hw(H, W, R, S, sh, sw, ph, pw)
     shape = (Ho, Wo, K, N) if _layout(layout) == HWCN else (N, K, Ho, Wo)
     y = out if out is not None else torch.empty(shape, dtype=torch.float32, device=x.device)
     if tuple(y.shape) != shape:
         raise ValueError(f"out has shape {tuple(y.shape)}, expected {shape}")
-    if plan is None and workspace is None:
-        conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream)
+    if acc64:
+        if workspace is not None:
+            raise ValueError("the fp64-accumulating path takes no workspace")
+        conv2d_fwd_f32_acc64(x, w, y, N, C, H, W, K, R, S, sh, sw, ph, pw, layout, plan, stream)
+        return y
+    square = sh == sw and ph == pw
+    if square and plan is None and workspace is None:
+        conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, sh, ph, layout, stream)
+        return y
+    wsb = conv2d_fwd_f32_hw_workspace_bytes(N, C, H, W, K, R, S, sh, sw, ph, pw, layout, plan)
+    if workspace is None and wsb > 0:
+        workspace = torch.empty((wsb + 3) // 4, dtype=torch.float32, device=x.device)
+    wsz = workspace.numel() * 4 if workspace is not None else 0
+    if square:
+        conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, sh, ph, layout, workspace, wsz, plan, stream)
     else:
-        wsb = conv2d_fwd_f32_workspace_bytes(N, C, H, W, K, R, S, stride, pad, layout, plan)
-        if workspace is None and wsb > 0:
-            workspace = torch.empty((wsb + 3) // 4, dtype=torch.float32, device=x.device)
-        wsz = workspace.numel() * 4 if workspace is not None else 0
-        conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, stride, pad, layout,
-                          workspace, wsz, plan, stream)
+        conv2d_fwd_f32_hw(x, w, y, N, C, H, W, K, R, S, sh, sw, ph, pw, layout, workspace, wsz,
+                          plan, stream)
     return y

@@ -199,3 +199,91 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert p.returncode == 2
     assert "one GPU" in p.stderr
+
+
+def test_out_dims_hw_match_oracle():
+    rng = np.random.Generator(np.random.PCG64(3))
+    for _ in range(300):
+        H, W = (int(v) for v in rng.integers(1, 40, 2))
+        R, S = (int(v) for v in rng.integers(1, 8, 2))
+        sh, sw = (int(v) for v in rng.integers(1, 5, 2))
+        ph, pw = (int(v) for v in rng.integers(0, 5, 2))
+        if H + 2 * ph < R or W + 2 * pw < S:
+            with pytest.raises(mg3m.Mg3mError):
+                mg3m.conv2d_out_dims_hw(H, W, R, S, sh, sw, ph, pw)
+            continue
+        assert mg3m.conv2d_out_dims_hw(H, W, R, S, sh, sw, ph, pw) == \
+            oracle.out_dims(H, W, R, S, (sh, sw), (ph, pw))
+
+
+@pytest.mark.parametrize("args,status", [
+    ((2, 8, 10, 10, 16, 3, 3, 0, 1, 1, 1), 2), ((2, 8, 10, 10, 16, 3, 3, 1, 0, 1, 1), 2),
+    ((2, 8, 10, 10, 16, 3, 3, 1, 1, -1, 1), 2), ((2, 8, 10, 10, 16, 3, 3, 1, 1, 1, -1), 2),
+    ((2, 8, 2, 10, 16, 5, 3, 1, 1, 0, 1), 2),
+])
+def test_hw_shape_errors(args, status):
+    lib = mg3m.load_library()
+    assert lib.conv2d_fwd_f32_hw(X, Wp, Y, *args, 0, None, 0, None, None) == status
+
+
+# ------------------------------------------------ fp64-accumulating entry point
+TILES64 = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x64", "64x32"]
+
+
+def _acc64_plan(shape, layout, plan=None):
+    N, C, H, W, K, R, S, (sh, sw), (ph, pw) = shape
+    text = mg3m.conv2d_fwd_f32_acc64_plan_string(N, C, H, W, K, R, S, sh, sw, ph, pw, layout, plan)
+    assert text.startswith("acc=f64,")
+    f = dict(kv.split("=", 1) for kv in text.split(","))
+    Ho, Wo = mg3m.conv2d_out_dims_hw(H, W, R, S, sh, sw, ph, pw)
+    Mg, Ng, Kg = K, N * Ho * Wo, C * R * S
+    assert (int(f["Mg"]), int(f["Ng"]), int(f["Kg"])) == (Mg, Ng, Kg)
+    mt, nt = (int(v) for v in f["tile"].split("x"))
+    tm, tn = (int(v) for v in f["tiles"].split("x"))
+    assert (tm - 1) * mt < Mg <= tm * mt and (tn - 1) * nt < Ng <= tn * nt
+    # every tile whole, one work-group each, no workspace
+    assert f["kt"] == "16" and f["split"] == "1" and f["tail_tiles"] == "0" and f["ws"] == "0"
+    assert f["e"] == "elem"
+    assert int(f["dp_tiles"]) == int(f["grid"]) == tm * tn
+    assert int(f["k_tiles"]) == -(-Kg // 16)
+    assert 0 < int(f["lds"]) <= 160 * 1024
+    return f
+
+
+def test_acc64_plans_for_catalogue_layers_and_overrides():
+    for wl, (_, layers) in workloads.WORKLOADS.items():
+        for L in layers:
+            for layout in ("HWCN", "NCHW"):
+                _acc64_plan((L.N, L.C, L.H, L.W, L.K, L.R, L.S, (L.stride,) * 2, (L.pad,) * 2), layout)
+    rng = np.random.Generator(np.random.PCG64(4))
+    for _ in range(100):
+        N = int(rng.integers(1, 33))
+        C, K = (int(v) for v in rng.integers(1, 300, 2))
+        H, W = (int(v) for v in rng.integers(1, 40, 2))
+        R, S = (int(v) for v in rng.choice([1, 2, 3, 5], 2))
+        sh, sw = (int(v) for v in rng.integers(1, 4, 2))
+        ph, pw = (int(v) for v in rng.integers(0, 3, 2))
+        if H + 2 * ph < R or W + 2 * pw < S:
+            continue
+        shape = (N, C, H, W, K, R, S, (sh, sw), (ph, pw))
+        t = str(rng.choice(TILES64))
+        for layout in ("HWCN", "NCHW"):
+            _acc64_plan(shape, layout)
+            assert _acc64_plan(shape, layout, f"tile={t}")["tile"] == t
+
+
+def test_acc64_errors():
+    lib = mg3m.load_library()
+    good = (4, 64, 14, 14, 96, 3, 3, 1, 1, 1, 1, 0)
+    for bad in (b"split=2", b"tail=4", b"kt=32", b"tile=256x128", b"tile=7x7", b"bogus=1"):
+        assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, *good, bad, None) == 7, bad
+    assert lib.conv2d_fwd_f32_acc64(None, Wp, Y, *good, None, None) == 1
+    assert lib.conv2d_fwd_f32_acc64(X, Wp, Y + 2, *good, None, None) == 9
+    assert lib.conv2d_fwd_f32_acc64(X, Wp, X + 64, *good, None, None) == 5
+    assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, 4, 64, 14, 14, 96, 3, 3, 1, 1, 1, 1, 2, None, None) == 3
+    assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, 4, 64, 2, 14, 96, 5, 3, 1, 1, 0, 1, 0, None, None) == 2
+    assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, 1 << 16, 1 << 10, 64, 64, 16, 3, 3, 1, 1, 1, 1, 0,
+                                    None, None) == 4
+    assert mg3m.mg3m_last_error() != ""
+    # a split-only override is accepted by the fp32 entry point
+    assert mg3m.conv2d_fwd_f32_plan_string(4, 64, 14, 14, 96, 3, 3, 1, 1, "HWCN", "split=2")

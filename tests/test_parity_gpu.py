@@ -109,6 +109,39 @@ def test_tail_split_bit_exact():
         assert np.array_equal(y.astype(np.float64), acc), f"{plan}: not bit-exact"
 
 
+def _rect_grid():
+    rng = np.random.Generator(np.random.PCG64(20230705))
+    cases = []
+    while len(cases) < 16:
+        N = int(rng.choice([1, 2, 4, 8]))
+        C = int(rng.choice([3, 4, 16, 32]))
+        K = int(rng.choice([8, 17, 64]))
+        H, W = (int(v) for v in rng.integers(3, 20, 2))
+        R, S = (int(v) for v in rng.choice([1, 2, 3, 5], 2))
+        sh, sw = (int(v) for v in rng.integers(1, 4, 2))
+        ph, pw = (int(v) for v in rng.integers(0, 3, 2))
+        if (sh, ph) == (sw, pw) or H + 2 * ph < R or W + 2 * pw < S:
+            continue
+        cases.append((N, C, H, W, K, R, S, (sh, sw), (ph, pw)))
+    return cases
+
+
+RECT = _rect_grid()
+
+
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+@pytest.mark.parametrize("case", range(len(RECT)))
+def test_rectangular_stride_pad(case, layout):
+    """conv2d_fwd_f32_hw: separate vertical / horizontal stride and padding."""
+    shape = RECT[case]
+    say(f"rectangular {case} {layout} shape={shape}")
+    x, w, st, pd = make(shape, 2000 + case, layout)
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    for plan in (None, "split=3"):
+        y = run_gpu(x, w, st, pd, layout, plan=plan)
+        assert_parity(y, acc, mag, f"{shape} {layout} {plan}")
+
+
 @pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
 def test_misaligned_pointers(layout):
     """4-byte but not 16-byte aligned buffers take the element-wise paths."""

@@ -273,12 +273,17 @@ def small_int(shape, seed, lo=-2, hi=2):
 
 def make_tensors(layer: Layer, seed_x: int, seed_w: int, layout: str = "HWCN", dist: str = None):
     """Logical tensors x[N,C,H,W], w[K,C,R,S] for one layer, returned in `layout`.
-    dist: None -> x uniform and w per layer.wdist; "int" -> small integers."""
+    dist: None -> x uniform and w per layer.wdist; "int" -> small integers
+    (every partial sum an integer below 2^24); "wideint" -> integers in
+    [-2048, 2048] (products up to 2^22, sums past 2^24 but far below 2^53)."""
     xs = (layer.N, layer.C, layer.H, layer.W)
     ws = (layer.K, layer.C, layer.R, layer.S)
     if dist == "int":
         x = small_int(xs, seed_x)
         w = small_int(ws, seed_w)
+    elif dist == "wideint":
+        x = small_int(xs, seed_x, -2048, 2048)
+        w = small_int(ws, seed_w, -2048, 2048)
     else:
         x = uniform(xs, seed_x)
         if layer.wdist == "he":
