@@ -28,14 +28,22 @@ HBM_GBS = 8000.0             # MI355X HBM3E
 METRIC = "fp32 conv TFLOPS and % of MI355X fp32 MFMA peak per layer, 1 GPU"
 
 
-def kernel_source_digest() -> str:
-    """Digest of every library source: profile figures taken on other sources
-    are not reused."""
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2307_04941_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+def kernel_digest(name: str, launches) -> str:
+    """Digest of one kernel's machine code (from the build's
+    kernel_digests.json) and of the launches a step makes of it (layer, tile,
+    schedule, grid): HBM-traffic counters taken on this kernel in this
+    workload are reused exactly while both are unchanged.  None if the build
+    recorded no digest for it."""
+    path = os.path.join(ROOT, "paper_2307_04941_amd", "kernel_digests.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        code = json.load(f).get(name)
+    if code is None:
+        return None
+    h = hashlib.sha256(code.encode())
+    for r in launches:
+        h.update(f"|{r['layer']}:{r['tile']}:{r['dp_tiles']}:{r['tail_tiles']}:{r['split']}:{r['grid']}".encode())
     return h.hexdigest()[:16]
 
 
@@ -206,6 +214,7 @@ def main():
             "pct_roofline": round(100 * fl / us / 1e6 / attainable, 1),
             "bound": "mfma" if ai * HBM_GBS / 1e3 >= PEAK_TFLOPS else "hbm",
             "tile": f"{plan['mt']}x{plan['nt']}x{plan['kt']}", "split": plan["split"],
+            "dp_tiles": plan["dp_tiles"], "tail_tiles": plan["tail_tiles"],
             "grid": plan["grid"], "kernel": kernel_name(plan),
             "flops": fl, "alg_bytes": by,
         })
@@ -220,12 +229,13 @@ def main():
         g["layers"].append(r["layer"])
     dname, dg = max(groups.items(), key=lambda kv: kv[1]["us"])
     achieved = dg["flops"] / dg["us"] / 1e6
+    digest = kernel_digest(dname, [r for r in per_layer if r["kernel"] == dname])
     traffic = None
     prof = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
-    if os.path.exists(prof) and not args.plan:
+    if os.path.exists(prof) and not args.plan and digest is not None:
         with open(prof) as f:
             t = json.load(f)
-        if t.get("kernel_digest") == kernel_source_digest() and t.get("kernel") == dname:
+        if t.get("kernel_digest") == digest and t.get("kernel") == dname:
             traffic = t.get("hbm_bytes_per_launch")
     roofline = {
         "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -261,7 +271,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "layers": per_layer,
-        "kernel_digest": kernel_source_digest(),
+        "kernel_digest": digest,
     }
     print(json.dumps(out), flush=True)
 

@@ -132,15 +132,18 @@ int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, 
 
 /* y = conv(x, w) with the numerics of the paper's kernel: fp32 operands,
  * every product and partial sum in fp64, and one round-to-nearest-even to
- * fp32 per output at the store (Sec. 4.1.1, Alg. 2, which converts each
- * staged tile to double and computes in double).  Each output is therefore
- * within one fp32 rounding of its fp64 sum.  On fp64 MFMA (half the fp32
- * peak).  Separate vertical and horizontal stride and padding as in
- * conv2d_fwd_f32_hw.  Every output tile is computed whole by one work-group
- * (no split of the reduction), so no workspace is used.  plan: NULL, or an
- * override with only the key tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
- * 64x128, 128x64, 64x64, 32x64, 64x32); split, tail or a kt other than 16
- * -> MG3M_ERR_PLAN.  Pointers, ownership, validation and errors as for
+ * fp32 per output (Sec. 4.1.1, Alg. 2, which converts each staged tile to
+ * double and computes in double).  Each output is therefore within one fp32
+ * rounding of its fp64 sum.  On fp64 MFMA (half the fp32 peak).  Separate
+ * vertical and horizontal stride and padding as in conv2d_fwd_f32_hw.  When
+ * the plan splits the reduction of some tiles, their chunks' fp64 partial
+ * sums go to a workspace taken from HIP's stream-ordered allocator
+ * (hipMallocAsync / hipFreeAsync on `stream`) and a second kernel adds them
+ * in chunk order in fp64 before the one rounding, so results are
+ * deterministic run to run.  plan: NULL, or an override with the keys of
+ * conv2d_fwd_f32_ex: tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
+ * 64x128, 128x64, 64x64, 32x64, 64x32), split=<n>, tail=<n>; kt other than
+ * 16 -> MG3M_ERR_PLAN.  Pointers, ownership, validation and errors as for
  * conv2d_fwd_f32. */
 int conv2d_fwd_f32_acc64(const float *x, const float *w, float *y,
                          int N, int C, int H, int W, int K, int R, int S,

@@ -7,6 +7,8 @@ Compiles in-tree with hipcc; the shared library lands next to this file.
 from __future__ import annotations
 
 import concurrent.futures
+import hashlib
+import json
 import os
 import subprocess
 import sys
@@ -43,12 +45,84 @@ def _compile(src: str, obj: str, extra=()):
     return obj
 
 
+LLVM_BIN = "/opt/rocm/llvm/bin"
+DIGESTS = os.path.join(PKG, "kernel_digests.json")
+
+
+def _device_code_object(obj: str, tmp: str) -> str:
+    """The gfx950 code object inside a compiled host object (our own build)."""
+    base = os.path.join(tmp, os.path.basename(obj))
+    fat, co = base + ".fatbin", base + ".gfx950.co"
+    subprocess.run([f"{LLVM_BIN}/llvm-objcopy", "--dump-section", f".hip_fatbin={fat}", obj, base + ".junk"],
+                   check=True, capture_output=True)
+    subprocess.run([f"{LLVM_BIN}/clang-offload-bundler", "--unbundle", "--type=o",
+                    f"--targets=hipv4-amdgcn-amd-amdhsa--{ARCH}", f"--input={fat}", f"--output={co}"],
+                   check=True, capture_output=True)
+    return co
+
+
+def _kernel_digests(co: str) -> dict:
+    """Per kernel (mangled name): sha256 of its instructions (addresses and
+    encodings dropped) and of its resource metadata (registers, LDS, ...)."""
+    dis = subprocess.run([f"{LLVM_BIN}/llvm-objdump", "-d", "--no-show-raw-insn", "--no-leading-addr", co],
+                         check=True, capture_output=True, text=True).stdout
+    code, name = {}, None
+    for line in dis.splitlines():
+        if line.endswith(">:") and line.startswith("<"):
+            name = line[1:-2]
+            code[name] = []
+        elif name and line.strip():
+            code[name].append(line.split("//")[0].split("<")[0].strip())
+        elif not line.strip():
+            name = None
+    notes = subprocess.run([f"{LLVM_BIN}/llvm-readelf", "--notes", co], check=True, capture_output=True,
+                           text=True).stdout
+    meta, block = {}, []
+    for line in notes.splitlines():
+        if line.startswith("  - ") and block:
+            meta.update(_meta_block(block))
+            block = []
+        if line.startswith("  - ") or (block and line.startswith("    ")):
+            block.append(line.strip())
+    if block:
+        meta.update(_meta_block(block))
+    out = {}
+    for k, lines in code.items():
+        h = hashlib.sha256("\n".join(lines).encode() + b"\0" + "\n".join(meta.get(k, [])).encode())
+        out[k] = h.hexdigest()[:16]
+    return out
+
+
+def _meta_block(block):
+    name = next((l.split(":", 1)[1].strip() for l in block if l.startswith(".name:")), None)
+    return {name: block} if name else {}
+
+
+def write_kernel_digests(objs, tmp) -> dict:
+    """kernel_digests.json: demangled kernel name (as rocprofv3 prints it) ->
+    digest of its machine code, so that a profile taken on a kernel is reused
+    exactly as long as that kernel's code is unchanged."""
+    digests = {}
+    for obj in objs:
+        if obj.endswith(".hip.o"):
+            digests.update(_kernel_digests(_device_code_object(obj, tmp)))
+    names = sorted(digests)
+    dem = subprocess.run(["c++filt"], input="\n".join(names), capture_output=True, text=True,
+                         check=True).stdout.splitlines()
+    table = {d: digests[n] for n, d in zip(names, dem)}
+    with open(DIGESTS + ".tmp", "w") as f:
+        json.dump(table, f, indent=0, sort_keys=True)
+    os.replace(DIGESTS + ".tmp", DIGESTS)
+    return table
+
+
 def build(verbose: bool = False, extra=()) -> str:
     """Compile every source and link libmg3m.so; returns its path."""
     with tempfile.TemporaryDirectory(prefix="mg3m_build_") as tmp:
         objs = [os.path.join(tmp, s + ".o") for s in SOURCES]
         with concurrent.futures.ThreadPoolExecutor(len(SOURCES)) as ex:
             list(ex.map(lambda so: _compile(so[0], so[1], extra), zip(SOURCES, objs)))
+        write_kernel_digests(objs, tmp)
         out_tmp = LIB + ".tmp"
         cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out_tmp, *objs]
         p = subprocess.run(cmd, capture_output=True, text=True)

@@ -119,6 +119,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     r.Mg = (int)s.Mg; r.Ng = (int)s.Ng;
     const bool contiguous4 = s.layout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
     r.vec4 = contiguous4 && aligned(y, 16);
+    r.f64 = p.acc64;
     rc = mg3m::launch_tail_reduce(r, stream, &err);
   }
   if (own_workspace && ws != nullptr) {
@@ -246,7 +247,7 @@ int conv2d_fwd_f32_acc64(const float* x, const float* w, float* y, int N, int C,
                          int layout, const char* plan, void* stream) {
   try {
     return run(x, w, y, geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout, true),
-               nullptr, 0, false, plan, stream);
+               nullptr, 0, true, plan, stream);
   } catch (const std::exception& e) {
     return fail(MG3M_ERR_HIP, e.what());
   } catch (...) {

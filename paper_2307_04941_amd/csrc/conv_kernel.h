@@ -64,9 +64,23 @@ __device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, unsigned off) 
 }
 __device__ __forceinline__ void st4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
 
-// Tile geometry.  ACC64 selects the fp64-accumulating kernel's LDS padding:
-// its 16x16x4 MFMA fragments read four k-rows per instruction, so rows are
-// padded by 16 floats instead of 32 to keep the four rows on distinct banks.
+// Placement of one staged operand tile (rows of DIM floats) in LDS: the row
+// stride, and the column swizzle that keeps the rows one fragment read
+// touches on disjoint banks (see lds_row_stride).  The swizzle permutes
+// 16-float groups inside each 64-float block, so 16-byte stores stay whole,
+// and it depends on the row only through row % 2 (fp32) or row % 4 (fp64).
+template <int DIM, bool ACC64>
+struct LdsLayout {
+  static constexpr int kStride = ACC64 ? lds_row_stride64(DIM) : lds_row_stride(DIM);
+  static constexpr bool kSwz = DIM % 64 == 0;
+  __device__ static constexpr int col(int row, int c) {
+    if constexpr (!kSwz) return c;
+    else if constexpr (ACC64) return c ^ ((row & 3) << 4);
+    else return c ^ ((row & 1) << 5);
+  }
+};
+
+// Tile geometry.  ACC64 selects the fp64-accumulating kernel's LDS layout.
 template <int MT, int NT, int KT, int WM, int WN, bool ACC64 = false>
 struct Cfg {
   static constexpr int T = WM * WN * 64;        // threads per work-group
@@ -76,8 +90,10 @@ struct Cfg {
   static constexpr int TN = WTN / 32;           // ... columns
   static constexpr int TM16 = WTM / 16;         // 16x16 MFMA blocks per wave (fp64), rows
   static constexpr int TN16 = WTN / 16;         // ... columns
-  static constexpr int AS = ACC64 ? lds_row_stride64(MT) : lds_row_stride(MT);
-  static constexpr int BS = ACC64 ? lds_row_stride64(NT) : lds_row_stride(NT);
+  using LA = LdsLayout<MT, ACC64>;
+  using LB = LdsLayout<NT, ACC64>;
+  static constexpr int AS = LA::kStride;
+  static constexpr int BS = LB::kStride;
   static constexpr int A_STAGE = KT * AS;
   static constexpr int B_STAGE = KT * BS;
   static constexpr int LDS_FLOATS = 2 * A_STAGE + 2 * B_STAGE;
@@ -145,8 +161,10 @@ struct AVecM {
     }
   }
   __device__ void store(float* As) const {
+    static_assert(RSTEP % 4 == 0, "a thread's rows share their swizzle");
+    const int col = C::LA::col(kr0, m4 * 4);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + m4 * 4, v[i]);
+    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + col, v[i]);
   }
 };
 
@@ -190,8 +208,10 @@ struct AVecMTap {
     }
   }
   __device__ void store(float* As) const {
+    static_assert(RSTEP % 4 == 0, "a thread's rows share their swizzle");
+    const int col = C::LA::col(kr0, m4 * 4);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + m4 * 4, v[i]);
+    for (int i = 0; i < NV; ++i) st4(As + (kr0 + i * RSTEP) * C::AS + col, v[i]);
   }
 };
 
@@ -227,7 +247,7 @@ struct AVecK {
     for (int i = 0; i < NV; ++i) {
       const int mm = mr0 + i * MSTEP;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) As[(4 * k4 + e) * C::AS + mm] = v[i][e];
+      for (int e = 0; e < 4; ++e) As[(4 * k4 + e) * C::AS + C::LA::col(4 * k4 + e, mm)] = v[i][e];
     }
   }
 };
@@ -262,7 +282,7 @@ struct AScalar {
     for (int i = 0; i < NE; ++i) {
       int m, kr;
       coords(t_ + i * C::T, m, kr);
-      As[kr * C::AS + m] = v[i];
+      As[kr * C::AS + C::LA::col(kr, m)] = v[i];
     }
   }
 };
@@ -325,8 +345,10 @@ struct BVecNTap {
     }
   }
   __device__ void store(float* Bs) const {
+    static_assert(RSTEP % 4 == 0, "a thread's rows share their swizzle");
+    const int col = C::LB::col(kr0, n4 * 4);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + n4 * 4, v[i]);
+    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + col, v[i]);
   }
 };
 
@@ -377,8 +399,10 @@ struct BVecN {
     }
   }
   __device__ void store(float* Bs) const {
+    static_assert(RSTEP % 4 == 0, "a thread's rows share their swizzle");
+    const int col = C::LB::col(kr0, n4 * 4);
 #pragma unroll
-    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + n4 * 4, v[i]);
+    for (int i = 0; i < NV; ++i) st4(Bs + (kr0 + i * RSTEP) * C::BS + col, v[i]);
   }
 };
 
@@ -428,7 +452,7 @@ struct BVecC {
     for (int i = 0; i < NV; ++i) {
       const int n = nc0 + i * NSTEP;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) Bs[(4 * k4 + e) * C::BS + n] = v[i][e];
+      for (int e = 0; e < 4; ++e) Bs[(4 * k4 + e) * C::BS + C::LB::col(4 * k4 + e, n)] = v[i][e];
     }
   }
 };
@@ -469,7 +493,7 @@ struct BScalar {
 #pragma unroll
     for (int i = 0; i < NE; ++i) {
       const int e = t_ + i * C::T;
-      Bs[(e / NT) * C::BS + e % NT] = v[i];
+      Bs[(e / NT) * C::BS + C::LB::col(e / NT, e % NT)] = v[i];
     }
   }
 };
@@ -502,15 +526,20 @@ struct BSel<LAYOUT, kBScalar, C, NT, KT> { using type = BScalar<LAYOUT, C, NT, K
 template <class C, int KT>
 __device__ __forceinline__ void mma_stage(floatx16 (&acc)[C::TM][C::TN], const float* As,
                                           const float* Bs, int wm, int wn, int hh, int q) {
-  const float* Ac = As + wm * C::WTM + q;
-  const float* Bc = Bs + wn * C::WTN + q;
+  // Row 2*kk + hh, logical column c + q with c a multiple of 32: the
+  // swizzle depends on the row only through hh and leaves q (< 32) alone.
+  int ca[C::TM], cb[C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i) ca[i] = hh * C::AS + C::LA::col(hh, wm * C::WTM + i * 32) + q;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) cb[j] = hh * C::BS + C::LB::col(hh, wn * C::WTN + j * 32) + q;
   float av[KT / 2][C::TM], bv[KT / 2][C::TN];
 #pragma unroll
   for (int kk = 0; kk < KT / 2; ++kk) {
 #pragma unroll
-    for (int i = 0; i < C::TM; ++i) av[kk][i] = Ac[(2 * kk + hh) * C::AS + i * 32];
+    for (int i = 0; i < C::TM; ++i) av[kk][i] = As[ca[i] + 2 * kk * C::AS];
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j) bv[kk][j] = Bc[(2 * kk + hh) * C::BS + j * 32];
+    for (int j = 0; j < C::TN; ++j) bv[kk][j] = Bs[cb[j] + 2 * kk * C::BS];
   }
 #pragma unroll
   for (int kk = 0; kk < KT / 2; ++kk)
@@ -528,15 +557,20 @@ __device__ __forceinline__ void mma_stage(floatx16 (&acc)[C::TM][C::TN], const f
 template <class C, int KT>
 __device__ __forceinline__ void mma_stage64(f64x4 (&acc)[C::TM16][C::TN16], const float* As,
                                             const float* Bs, int wm, int wn, int g, int q) {
-  const float* Ac = As + wm * C::WTM + q;
-  const float* Bc = Bs + wn * C::WTN + q;
+  // Row 4*kk + g, logical column c + q with c a multiple of 16: the
+  // swizzle depends on the row only through g and leaves q (< 16) alone.
+  int ca[C::TM16], cb[C::TN16];
+#pragma unroll
+  for (int i = 0; i < C::TM16; ++i) ca[i] = g * C::AS + C::LA::col(g, wm * C::WTM + i * 16) + q;
+#pragma unroll
+  for (int j = 0; j < C::TN16; ++j) cb[j] = g * C::BS + C::LB::col(g, wn * C::WTN + j * 16) + q;
 #pragma unroll
   for (int kk = 0; kk < KT / 4; ++kk) {
     double av[C::TM16], bv[C::TN16];
 #pragma unroll
-    for (int i = 0; i < C::TM16; ++i) av[i] = (double)Ac[(4 * kk + g) * C::AS + i * 16];
+    for (int i = 0; i < C::TM16; ++i) av[i] = (double)As[ca[i] + 4 * kk * C::AS];
 #pragma unroll
-    for (int j = 0; j < C::TN16; ++j) bv[j] = (double)Bc[(4 * kk + g) * C::BS + j * 16];
+    for (int j = 0; j < C::TN16; ++j) bv[j] = (double)Bs[cb[j] + 4 * kk * C::BS];
 #pragma unroll
     for (int i = 0; i < C::TM16; ++i)
 #pragma unroll
@@ -741,10 +775,12 @@ KernelFn kernel_for_tile(int tile) {
 }
 
 // ------------------------------------------------- fp64-accumulating kernel
-// Same operand staging as conv_igemm_f32 (fp32 tiles in LDS); the MFMAs take
-// the operands widened to fp64 and accumulate in fp64, and each output is
-// rounded to fp32 once, at the store.  Every tile is computed whole (no
-// reduction split), so the sum never leaves fp64 before that rounding.
+// Same operand staging and tile schedule as conv_igemm_f32 (fp32 tiles in
+// LDS; whole tiles, then chunks of the split tail tiles); the MFMAs take the
+// operands widened to fp64 and accumulate in fp64.  A whole tile rounds each
+// output to fp32 once, at the store.  A chunk stores its fp64 partial sums,
+// which the tail reduction adds in fp64 and then rounds once, so the sum
+// never leaves fp64 before that one rounding.
 template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64)
 void conv_igemm_acc64(KArgs a) {
@@ -752,10 +788,24 @@ void conv_igemm_acc64(KArgs a) {
   __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
 
   const int t = threadIdx.x;
-  const int tile = xcd_group(blockIdx.x, a.dp_tiles);
+  const int L = xcd_group(blockIdx.x, a.dp_tiles);
+  int tile, kt0, nk, chunk = 0;
+  const bool partial = L >= a.dp_tiles;
+  if (!partial) {
+    tile = L;
+    kt0 = 0;
+    nk = a.k_tiles;
+  } else {
+    const int j = L - a.dp_tiles;
+    chunk = j / a.tail_tiles;
+    tile = a.dp_tiles + (j - chunk * a.tail_tiles);
+    kt0 = chunk * a.kps;
+    nk = min(a.kps, a.k_tiles - kt0);
+  }
   const int tm = tile % a.tiles_m;
   const int tn = tile / a.tiles_m;
   const int m0 = tm * MT, n0 = tn * NT;
+  const int kbeg = kt0 * KT;
 
   float* const As0 = lds;
   float* const Bs0 = lds + 2 * C::A_STAGE;
@@ -764,8 +814,8 @@ void conv_igemm_acc64(KArgs a) {
 
   typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
   typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
-  al.init(a, t, m0, 0);
-  bl.init(a, t, n0, 0);
+  al.init(a, t, m0, kbeg);
+  bl.init(a, t, n0, kbeg);
 
   const int wave = t >> 6, lane = t & 63;
   const int wm = wave % WM, wn = wave / WM;
@@ -777,13 +827,27 @@ void conv_igemm_acc64(KArgs a) {
 #pragma unroll
     for (int j = 0; j < C::TN16; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  run_stages<C>(a, al, bl, As0, Bs0, a.k_tiles, xr, wr, [&](const float* As, const float* Bs) {
+  run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
     mma_stage64<C, KT>(acc, As, Bs, wm, wn, g, q);
   });
 
   // 16x16 fp64 accumulator layout: element e of lane (g, q) holds row
   // g + 4*e, column q.  A lane's four rows are not adjacent, so the stores
   // are single elements (lanes g = 0..3 together cover four adjacent rows).
+  if (partial) {
+    // tile-local fp64 partial sums, row-major mt x nt, chunk-major over the tail
+    double* const part = reinterpret_cast<double*>(a.ws) +
+                         ((long long)chunk * a.tail_tiles + (tile - a.dp_tiles)) * (MT * NT);
+#pragma unroll
+    for (int j = 0; j < C::TN16; ++j) {
+      const int col = wn * C::WTN + j * 16 + q;
+#pragma unroll
+      for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) part[(wm * C::WTM + i * 16 + g + 4 * e) * NT + col] = acc[i][j][e];
+    }
+    return;
+  }
   float* const out = a.y;
 #pragma unroll
   for (int j = 0; j < C::TN16; ++j) {

@@ -10,12 +10,16 @@
 namespace mg3m {
 
 typedef float f32x4r __attribute__((ext_vector_type(4)));
+typedef double f64x2r __attribute__((ext_vector_type(2)));
 
 // Tail reduction: for every element of every tail tile, y = sum of the
 // tile's chunk partials in chunk order 0, 1, ..., split-1, so the result does
-// not depend on scheduling.  One thread per four consecutive columns of one
-// tile row; rows and columns past the output are skipped.
-__global__ __launch_bounds__(256) void tail_reduce_f32(RArgs r) {
+// not depend on scheduling.  F64: the partials are fp64 (from the
+// fp64-accumulating kernel), summed in fp64 and rounded to fp32 once.  One
+// thread per four consecutive columns of one tile row; rows and columns past
+// the output are skipped.
+template <bool F64>
+__global__ __launch_bounds__(256) void tail_reduce(RArgs r) {
   const long long tile_elems = (long long)r.mt * r.nt;
   const long long per_tile4 = tile_elems / 4;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
@@ -23,10 +27,22 @@ __global__ __launch_bounds__(256) void tail_reduce_f32(RArgs r) {
   const int t = (int)(i / per_tile4);
   const int e = (int)(i - (long long)t * per_tile4) * 4;
   const int row = e / r.nt, col = e - row * r.nt;
-  const float* p = r.ws + (long long)t * tile_elems + e;
+  const long long off = (long long)t * tile_elems + e;
   const long long chunk_stride = (long long)r.tail_tiles * tile_elems;
-  f32x4r sum = *reinterpret_cast<const f32x4r*>(p);
-  for (int c = 1; c < r.split; ++c) sum += *reinterpret_cast<const f32x4r*>(p + c * chunk_stride);
+  f32x4r sum;
+  if constexpr (F64) {
+    const double* p = static_cast<const double*>(r.ws) + off;
+    f64x2r lo = *reinterpret_cast<const f64x2r*>(p), hi = *reinterpret_cast<const f64x2r*>(p + 2);
+    for (int c = 1; c < r.split; ++c) {
+      lo += *reinterpret_cast<const f64x2r*>(p + c * chunk_stride);
+      hi += *reinterpret_cast<const f64x2r*>(p + c * chunk_stride + 2);
+    }
+    sum = f32x4r{(float)lo[0], (float)lo[1], (float)hi[0], (float)hi[1]};
+  } else {
+    const float* p = static_cast<const float*>(r.ws) + off;
+    sum = *reinterpret_cast<const f32x4r*>(p);
+    for (int c = 1; c < r.split; ++c) sum += *reinterpret_cast<const f32x4r*>(p + c * chunk_stride);
+  }
   const int tile = r.dp_tiles + t;
   const int tm = tile % r.tiles_m, tn = tile / r.tiles_m;
   const int m = tm * r.mt + row;
@@ -102,7 +118,10 @@ int launch_tail_reduce(const RArgs& r, void* stream, std::string* err) {
     *err = "internal: tail reduction shape out of range";
     return MG3M_ERR_PLAN;
   }
-  hipLaunchKernelGGL(tail_reduce_f32, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, r);
+  if (r.f64)
+    hipLaunchKernelGGL(tail_reduce<true>, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, r);
+  else
+    hipLaunchKernelGGL(tail_reduce<false>, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, r);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("tail reduction launch: ") + hipGetErrorString(e);

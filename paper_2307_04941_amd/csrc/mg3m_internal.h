@@ -62,55 +62,57 @@ struct TileDesc {
 // The tile menu.  Every entry is instantiated for every loader variant.
 constexpr int kNumTiles = 13;
 inline constexpr TileDesc kTiles[kNumTiles] = {
-    {128, 128, 16, 2, 2, 136, 0.824},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 136, 0.803},    // 1: four waves sharing one filter tile (TB(1,8)-like)
-    {256, 64, 16, 4, 1, 144, 0.843},    // 2: four waves sharing one patch tile
-    {64, 128, 16, 1, 2, 144, 0.648},    // 3
-    {128, 64, 16, 2, 1, 144, 0.647},    // 4
-    {64, 64, 16, 1, 1, 146, 0.657},     // 5: one wave per work-group (TB(1,1)-like)
-    {32, 128, 16, 1, 2, 104, 0.698},    // 6
-    {32, 64, 16, 1, 1, 104, 0.645},     // 7
-    {128, 32, 16, 2, 1, 104, 0.741},    // 8
-    {64, 32, 16, 1, 1, 104, 0.660},     // 9
-    {256, 128, 16, 4, 2, 130, 0.790},   // 10: eight waves
-    {128, 256, 16, 2, 4, 130, 0.763},   // 11: eight waves
-    {128, 128, 32, 2, 2, 192, 0.799},   // 12: deeper reduction step
+    {128, 128, 16, 2, 2, 108, 0.861},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
+    {64, 256, 16, 1, 4, 112, 0.852},    // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {256, 64, 16, 4, 1, 112, 0.891},    // 2: four waves sharing one patch tile
+    {64, 128, 16, 1, 2, 120, 0.809},    // 3
+    {128, 64, 16, 2, 1, 116, 0.823},    // 4
+    {64, 64, 16, 1, 1, 120, 0.740},     // 5: one wave per work-group (TB(1,1)-like)
+    {32, 128, 16, 1, 2, 88, 0.799},    // 6
+    {32, 64, 16, 1, 1, 88, 0.724},     // 7
+    {128, 32, 16, 2, 1, 84, 0.808},    // 8
+    {64, 32, 16, 1, 1, 88, 0.708},     // 9
+    {256, 128, 16, 4, 2, 104, 0.886},   // 10: eight waves
+    {128, 256, 16, 2, 4, 104, 0.832},   // 11: eight waves
+    {128, 128, 32, 2, 2, 124, 0.785},   // 12: deeper reduction step
 };
 
-// LDS row strides (floats) of the staged operand tiles.  The two half-waves of
-// an MFMA operand read hit rows k and k+1; a stride of 32 (mod 64) floats keeps
-// them on disjoint banks.
-constexpr int lds_row_stride(int dim) { return dim % 64 == 0 ? dim + 32 : dim; }
+// LDS row strides (floats) of the staged operand tiles.  An MFMA fragment
+// read touches 2 (fp32 32x32x2) or 4 (fp64 16x16x4) consecutive k-rows at the
+// same columns.  Rows whose length is a multiple of 64 floats are stored
+// unpadded and XOR-swizzled in the kernels (bit 5 of the column flipped on odd
+// rows for fp32, bits 4-5 by the row mod 4 for fp64), which puts those rows
+// on disjoint banks.  32-float rows need nothing for fp32 (rows already 32
+// banks apart) and 16 floats of padding for fp64.
+constexpr int lds_row_stride(int dim) { return dim; }
+constexpr int lds_row_stride64(int dim) { return (dim % 64 != 0 && dim % 32 == 0) ? dim + 16 : dim; }
 // LDS bytes per work-group: two stages of the A and B tiles.
 constexpr int lds_bytes_for(const TileDesc& t) {
   return 4 * (2 * t.kt * lds_row_stride(t.mt) + 2 * t.kt * lds_row_stride(t.nt));
 }
-// The fp64-accumulating kernel's 16x16x4 fragments read four k-rows of 16
-// floats per instruction; a row stride of 16 (mod 32) floats puts the four
-// rows on disjoint banks.
-constexpr int lds_row_stride64(int dim) { return dim % 32 == 0 ? dim + 16 : dim; }
 constexpr int lds_bytes_for64(const TileDesc& t) {
   return 4 * (2 * t.kt * lds_row_stride64(t.mt) + 2 * t.kt * lds_row_stride64(t.nt));
 }
 
 // Tile menu of the fp64-accumulating kernel (fp32 operands, every product and
 // partial sum in fp64, one rounding to fp32 at the store: the numerics of the
-// paper's kernel, Sec. 4.1.1 and Alg. 2).  It runs data parallel only.  regs
-// as above.  eff is not a measured fraction here: on full layers every tile
-// of this menu sustains 80-87% of the fp64 MFMA peak on MI355X, and these
-// values are the ones with which the cost model's pick per layer matched the
-// fastest tile measured on the VGG-16 and ResNet-50 layers (within 1% in
-// total time; the model's occupancy term already favours the small tiles).
+// paper's kernel, Sec. 4.1.1 and Alg. 2).  Split tiles keep fp64 partials.  regs
+// as above.  eff is not a measured fraction here: it is fitted so that the
+// cost model's pick per layer (tile and schedule) matches the fastest plan
+// measured on MI355X over the VGG-16 and ResNet-50 layers (within 0.3% in
+// total time).  On full layers the large tiles sustain 80-87% of the fp64
+// MFMA peak, the one-wave tiles (64x64, 32x64, 64x32) 75-80%; the model's
+// occupancy term already credits the latter with more resident waves.
 constexpr int kNumTiles64 = 8;
 inline constexpr TileDesc kTiles64[kNumTiles64] = {
-    {128, 128, 16, 2, 2, 190, 0.80},   // 0
-    {64, 256, 16, 1, 4, 194, 0.80},    // 1
-    {256, 64, 16, 4, 1, 194, 0.80},    // 2
-    {64, 128, 16, 1, 2, 198, 0.75},    // 3
-    {128, 64, 16, 2, 1, 198, 0.75},    // 4
-    {64, 64, 16, 1, 1, 196, 0.70},     // 5
-    {32, 64, 16, 1, 2, 80, 0.60},      // 6
-    {64, 32, 16, 2, 1, 80, 0.60},      // 7
+    {128, 128, 16, 2, 2, 200, 0.925},  // 0
+    {64, 256, 16, 1, 4, 206, 0.900},   // 1
+    {256, 64, 16, 4, 1, 208, 0.800},   // 2
+    {64, 128, 16, 1, 2, 214, 0.800},   // 3
+    {128, 64, 16, 2, 1, 210, 0.800},   // 4
+    {64, 64, 16, 1, 1, 212, 0.500},    // 5
+    {32, 64, 16, 1, 2, 78, 0.500},     // 6
+    {64, 32, 16, 2, 1, 78, 0.500},     // 7
 };
 
 // Largest tensor the kernels address: byte offsets are 32-bit and 0xFFFFFFC0
@@ -140,7 +142,7 @@ struct Plan {
   long long grid;           // dp_tiles + tail_tiles * split
   int a_mode, b_mode, e_mode;
   int variant;
-  size_t ws_bytes;          // tail_tiles * split * mt * nt floats
+  size_t ws_bytes;          // tail_tiles * split * mt * nt partials (4 or 8 bytes each)
   int lds_bytes;
   double pad_eff;
   double est_us;
@@ -151,7 +153,7 @@ struct KArgs {
   const float* x;
   const float* w;
   float* y;
-  float* ws;                // tile-local partials of the tail tiles
+  float* ws;                // tile-local partials of the tail tiles (fp64 in the fp64-accumulating kernel)
   unsigned x_bytes, w_bytes;
   int N, C, H, W, K, R, S;
   int sh, sw, ph, pw, Ho, Wo;
@@ -164,12 +166,13 @@ struct KArgs {
 
 // Arguments of the tail reduction.
 struct RArgs {
-  const float* ws;
+  const void* ws;           // fp32 partials, or fp64 ones when f64
   float* y;
   int mt, nt;               // tile shape
   int tiles_m, dp_tiles, tail_tiles, split;
   int layout, N, K, HoWo, Mg, Ng;
   int vec4;                 // four consecutive columns are contiguous in y
+  int f64;                  // the partials are fp64
 };
 
 // Planner (host only, no HIP calls).  Returns 0 or an mg3m_status code and

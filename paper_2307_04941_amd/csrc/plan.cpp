@@ -34,10 +34,10 @@ constexpr int kMaxWavesPerSimd = 8;
 // streaming rate, the cost of one kernel launch on the stream, the fixed cost
 // of each round of resident work-groups (prologue loads, epilogue stores), and
 // how MFMA utilisation falls when fewer than ~2 waves per SIMD are resident.
-constexpr double kStreamBytesPerS = 5.0e12;
-constexpr double kLaunchUs = 4.0;
+constexpr double kStreamBytesPerS = 4.0e12;
+constexpr double kLaunchUs = 3.0;
 constexpr double kRoundUs = 3.0;
-constexpr double kUtilBase = 0.4, kUtilPerWave = 0.2;
+constexpr double kUtilBase = 0.5, kUtilPerWave = 0.1;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
@@ -177,7 +177,7 @@ bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, int split_r
   const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
                         (double)p->k_tiles * t.kt;
   p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
-  p->ws_bytes = (size_t)p->tail_tiles * p->split * t.mt * t.nt * sizeof(float);
+  p->ws_bytes = (size_t)p->tail_tiles * p->split * t.mt * t.nt * (acc64 ? sizeof(double) : sizeof(float));
   p->est_us = 0.0;
   return true;
 }
@@ -294,8 +294,8 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   Override o;
   int rc = parse_override(override_text, &o, err);
   if (rc) return rc;
-  if (acc64 && (o.split > 1 || o.tail || (o.kt && o.kt != 16))) {
-    *err = "plan override: the fp64-accumulating kernel computes every tile whole with kt=16";
+  if (acc64 && o.kt && o.kt != 16) {
+    *err = "plan override: the fp64-accumulating kernel steps the reduction by kt=16";
     return MG3M_ERR_PLAN;
   }
 
@@ -323,9 +323,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     if (o.mt && !(td.mt == o.mt && td.nt == o.nt)) continue;
     // a forced tile without a depth means the default depth of 16
     if ((o.kt || o.mt) && td.kt != (o.kt ? o.kt : 16)) continue;
-    if (acc64) {
-      consider(ti, kDataParallel, 1);
-    } else if (o.split) {
+    if (o.split) {
       consider(ti, o.split > 1 ? kSplitAll : kDataParallel, o.split);
     } else if (o.tail) {
       consider(ti, kSplitTail, o.tail);

@@ -241,11 +241,14 @@ def _acc64_plan(shape, layout, plan=None):
     mt, nt = (int(v) for v in f["tile"].split("x"))
     tm, tn = (int(v) for v in f["tiles"].split("x"))
     assert (tm - 1) * mt < Mg <= tm * mt and (tn - 1) * nt < Ng <= tn * nt
-    # every tile whole, one work-group each, no workspace
-    assert f["kt"] == "16" and f["split"] == "1" and f["tail_tiles"] == "0" and f["ws"] == "0"
+    # whole tiles and split tail tiles partition the tiles; fp64 partials
+    kt, split, dp, tail = int(f["k_tiles"]), int(f["split"]), int(f["dp_tiles"]), int(f["tail_tiles"])
+    assert f["kt"] == "16" and kt == -(-Kg // 16)
+    assert dp + tail == tm * tn
+    assert int(f["grid"]) == dp + tail * split
+    assert (split >= 2) if tail else (split == 1)
+    assert int(f["ws"]) == 8 * tail * split * mt * nt
     assert f["e"] == "elem"
-    assert int(f["dp_tiles"]) == int(f["grid"]) == tm * tn
-    assert int(f["k_tiles"]) == -(-Kg // 16)
     assert 0 < int(f["lds"]) <= 160 * 1024
     return f
 
@@ -267,15 +270,19 @@ def test_acc64_plans_for_catalogue_layers_and_overrides():
             continue
         shape = (N, C, H, W, K, R, S, (sh, sw), (ph, pw))
         t = str(rng.choice(TILES64))
+        sp = int(rng.integers(1, 20))
         for layout in ("HWCN", "NCHW"):
             _acc64_plan(shape, layout)
             assert _acc64_plan(shape, layout, f"tile={t}")["tile"] == t
+            f = _acc64_plan(shape, layout, f"tile={t},split={sp}")
+            assert int(f["split"]) <= sp and f["tile"] == t
+            _acc64_plan(shape, layout, f"tile={t},tail={max(2, sp)}")
 
 
 def test_acc64_errors():
     lib = mg3m.load_library()
     good = (4, 64, 14, 14, 96, 3, 3, 1, 1, 1, 1, 0)
-    for bad in (b"split=2", b"tail=4", b"kt=32", b"tile=256x128", b"tile=7x7", b"bogus=1"):
+    for bad in (b"kt=32", b"tile=256x128", b"tile=7x7", b"bogus=1", b"split=0", b"tail=1"):
         assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, *good, bad, None) == 7, bad
     assert lib.conv2d_fwd_f32_acc64(None, Wp, Y, *good, None, None) == 1
     assert lib.conv2d_fwd_f32_acc64(X, Wp, Y + 2, *good, None, None) == 9
@@ -285,5 +292,6 @@ def test_acc64_errors():
     assert lib.conv2d_fwd_f32_acc64(X, Wp, Y, 1 << 16, 1 << 10, 64, 64, 16, 3, 3, 1, 1, 1, 1, 0,
                                     None, None) == 4
     assert mg3m.mg3m_last_error() != ""
-    # a split-only override is accepted by the fp32 entry point
-    assert mg3m.conv2d_fwd_f32_plan_string(4, 64, 14, 14, 96, 3, 3, 1, 1, "HWCN", "split=2")
+    # split and tail overrides are accepted (fp64 partials)
+    assert "split=2" in mg3m.conv2d_fwd_f32_acc64_plan_string(4, 64, 14, 14, 96, 3, 3, 1, 1, 1, 1,
+                                                               "HWCN", "tile=64x64,split=2")

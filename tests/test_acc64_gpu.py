@@ -80,7 +80,7 @@ def test_every_loader_pair(case):
     shape, layout, am, bm = VARIANTS[case]
     f = _plan_fields(shape, layout)
     assert (f["a"], f["b"]) == (am, bm), f
-    assert f["acc"] == "f64" and f["split"] == "1" and f["tail_tiles"] == "0" and f["ws"] == "0"
+    assert f["acc"] == "f64"
     say(f"acc64 loaders a={am} b={bm} {layout} shape={shape} tile={f['tile']}")
     x, w, st, pd = make(shape, 310 + case, layout, dist="wideint")
     acc, _ = oracle.conv2d(x, w, st, pd, layout)
@@ -102,6 +102,34 @@ def test_every_tile_random_data(tile, layout):
     acc, mag = oracle.conv2d(x, w, st, pd, layout)
     y = run_gpu(x, w, st, pd, layout, plan=f"tile={tile}", acc64=True)
     assert_parity_acc64(y, acc, mag, _kg(shape), f"tile {tile} {layout}")
+
+
+# Shape with more tiles than one round of resident work-groups for every
+# tested plan, so tail=n leaves whole tiles and split tiles.
+SPLIT_SHAPE = (24, 16, 61, 61, 96, 3, 3, 1, 1)
+SPLIT_PLANS = ["tile=128x128,split=3", "tile=32x64,split=5", "tile=64x256,tail=4", "tile=256x64,tail=2",
+               "tile=64x32,tail=6"]
+
+
+@pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
+@pytest.mark.parametrize("plan", SPLIT_PLANS)
+def test_split_reduction_keeps_fp64(plan, layout):
+    """Split tiles add fp64 partials in fp64 and round once: still bit-exact
+    on wide integers, still within one rounding on random data."""
+    f = _plan_fields(SPLIT_SHAPE, layout, plan)
+    say(f"acc64 split {plan} {layout}: dp_tiles {f['dp_tiles']} tail_tiles {f['tail_tiles']} "
+        f"split {f['split']} ws {f['ws']}")
+    assert int(f["tail_tiles"]) > 0 and int(f["split"]) >= 2
+    if "tail=" in plan:
+        assert int(f["dp_tiles"]) > 0
+    x, w, st, pd = make(SPLIT_SHAPE, 390, layout, dist="wideint")
+    acc, _ = oracle.conv2d(x, w, st, pd, layout)
+    y = run_gpu(x, w, st, pd, layout, plan=plan, acc64=True)
+    assert np.array_equal(y.view(np.uint32), _exact_f32(acc).view(np.uint32))
+    x, w, st, pd = make(SPLIT_SHAPE, 391, layout)
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    y = run_gpu(x, w, st, pd, layout, plan=plan, acc64=True)
+    assert_parity_acc64(y, acc, mag, _kg(SPLIT_SHAPE), f"{plan} {layout}")
 
 
 def _rect_cases():

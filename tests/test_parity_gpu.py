@@ -84,7 +84,7 @@ def test_every_tile_nchw(tile):
 # Enough output tiles for more than one round of resident work-groups, so that
 # tail=n splits only the leftover tiles (e.g. 256x64 tiles: 3081 tiles against
 # 768 resident work-groups -> 3072 whole, 9 split).
-TAIL_SHAPE = (16, 16, 111, 111, 32, 3, 3, 1, 1)
+TAIL_SHAPE = (24, 16, 111, 111, 32, 3, 3, 1, 1)
 
 
 @pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
