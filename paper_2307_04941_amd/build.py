@@ -86,6 +86,10 @@ def _kernel_digests(co: str) -> dict:
             block.append(line.strip())
     if block:
         meta.update(_meta_block(block))
+    for k, block in meta.items():
+        for line in block:
+            if line.startswith(".private_segment_fixed_size:") and int(line.split(":")[1]) != 0:
+                raise RuntimeError(f"kernel {k} uses scratch memory ({line}); keep it in registers")
     out = {}
     for k, lines in code.items():
         h = hashlib.sha256("\n".join(lines).encode() + b"\0" + "\n".join(meta.get(k, [])).encode())

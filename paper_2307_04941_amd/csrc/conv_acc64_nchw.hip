@@ -1,13 +1,14 @@
 // Instantiations of the fp64-accumulating kernel for the NCHW layout (vector
-// or scalar filter loads, scalar patch gathers), one per tile of the fp64 menu.
+// or scalar filter loads; patches as 16-byte runs along W where possible),
+// one per tile of the fp64 menu.
 #include "conv_kernel.h"
 
 namespace mg3m {
 
 KernelFn conv_kernel64_nchw(int variant, int tile) {
   switch (variant) {
-    case kVarNchwVecA: return kernel64_for_tile<kNCHW, kAVecK, kBScalar>(tile);
-    case kVarNchwScalar: return kernel64_for_tile<kNCHW, kAScalar, kBScalar>(tile);
+    case kVarNchwVecA: return kernel64_for_tile<kNCHW, kAVecK, kBVecW>(tile);
+    case kVarNchwScalar: return kernel64_for_tile<kNCHW, kAScalar, kBVecW>(tile);
     default: return nullptr;
   }
 }

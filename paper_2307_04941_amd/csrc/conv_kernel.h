@@ -352,6 +352,105 @@ struct BVecNTap {
   }
 };
 
+// NCHW input x[N][C][H][W] (Eq. 1's order), reduction order k = (c*R + r)*S + s.
+// Each thread owns four consecutive output columns n..n+3 (consecutive output
+// pixels of one image) and NV consecutive rows of the KT x NT tile.  With
+// stride_w == 1 the four columns of one output row read four consecutive
+// inputs along W, so when they lie inside the image one 16-byte load covers
+// them; otherwise (image borders, a group that wraps to the next output row,
+// any stride_w > 1) the four elements are loaded one by one from per-column
+// bases computed once per work-group.  The row index (c, r, s) advances by
+// carries, with no division in the main loop.
+template <class C, int NT, int KT>
+struct BVecW {
+  static constexpr int NC4 = NT / 4;
+  static constexpr int RG = C::T / NC4;      // threads sharing one column group
+  static constexpr int NV = KT / RG;         // consecutive rows per thread
+  static_assert(C::T % NC4 == 0 && KT % RG == 0 && NV * 4 == C::B_ELEMS, "B vec-W split");
+  int n4, kr0;
+  int cb[4], ih0[4], iw0[4];   // per column: x index at (c, r, s) = 0, and the tap origin
+  bool vrow;                   // the four columns are one run of one output row (stride_w 1)
+  int c, r, s;                 // reduction index of the thread's first row
+  int dc, dr, ds;              // KT in the mixed radix (C, R, S)
+  f32x4 v[NV], e4[NV];         // row loaded as one vector, or element by element
+  bool fast_[NV];              // row i took the vector load
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    n4 = t % NC4;
+    kr0 = (t / NC4) * NV;
+    const int n = n0 + n4 * 4, hw = a.Ho * a.Wo;
+    int wo_first = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int ne = n + e;
+      const int b = ne / hw, pix = ne - b * hw;
+      const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+      if (e == 0) wo_first = wo;
+      const bool live = ne < a.Ng;
+      ih0[e] = live ? ho * a.sh - a.ph : -(1 << 30);   // columns past the end read nothing
+      iw0[e] = wo * a.sw - a.pw;
+      cb[e] = live ? (b * a.C * a.H + ih0[e]) * a.W + iw0[e] : 0;
+    }
+    vrow = (a.sw == 1) & (n + 3 < a.Ng) & (wo_first + 3 < a.Wo);
+    const int rs = a.R * a.S, k0 = kbeg + kr0;
+    c = k0 / rs;
+    r = (k0 - c * rs) / a.S;
+    s = k0 - c * rs - r * a.S;
+    dc = KT / rs;
+    dr = (KT - dc * rs) / a.S;
+    ds = KT - dc * rs - dr * a.S;
+    // e4 is carried from stage to stage (stale in rows that take the vector
+    // load, where it is not used), so it never shares registers with v
+#pragma unroll
+    for (int i = 0; i < NV; ++i) e4[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ void advance(const KArgs& a) {
+    s += ds;
+    r += dr;
+    c += dc;
+    if (s >= a.S) { s -= a.S; ++r; }
+    if (r >= a.R) { r -= a.R; ++c; }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+    const int hw = a.H * a.W;
+    int ci = c, ri = r, si = s;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      if (i > 0) {
+        if (++si == a.S) {
+          si = 0;
+          if (++ri == a.R) { ri = 0; ++ci; }
+        }
+      }
+      const int rel = ci * hw + ri * a.W + si;
+      const bool k_ok = ci < a.C;
+      const int iw = iw0[0] + si;
+      const bool fast = vrow & k_ok & ((unsigned)(ih0[0] + ri) < (unsigned)a.H) & (iw >= 0) & (iw + 3 < a.W);
+      fast_[i] = fast;
+      v[i] = bload4(xr, fast ? (unsigned)(cb[0] + rel) * 4u : kOOB);
+      // separate registers: writing v[i] again would make the compiler wait
+      // for the vector load here, inside the load phase
+      if (!fast) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = k_ok & ((unsigned)(ih0[e] + ri) < (unsigned)a.H) &
+                          ((unsigned)(iw0[e] + si) < (unsigned)a.W);
+          e4[i][e] = bload1(xr, ok ? (unsigned)(cb[e] + rel) * 4u : kOOB);
+        }
+      }
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = fast_[i] ? v[i][e] : e4[i][e];
+      st4(Bs + (kr0 + i) * C::BS + C::LB::col(kr0 + i, n4 * 4), o);
+    }
+  }
+};
+
 // HWCN, N % 4 == 0: each thread owns one 4-wide batch vector of one output
 // pixel (a fixed column group) and NV rows of the KT x NT tile.
 template <class C, int NT, int KT>
@@ -517,6 +616,8 @@ template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecNTap, C, NT, KT> { using type = BVecNTap<C, NT, KT>; };
 template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecC, C, NT, KT> { using type = BVecC<C, NT, KT>; };
+template <class C, int NT, int KT>
+struct BSel<kNCHW, kBVecW, C, NT, KT> { using type = BVecW<C, NT, KT>; };
 template <int LAYOUT, class C, int NT, int KT>
 struct BSel<LAYOUT, kBScalar, C, NT, KT> { using type = BScalar<LAYOUT, C, NT, KT>; };
 

@@ -19,17 +19,19 @@ enum Layout : int { kHWCN = 0, kNCHW = 1 };
 //                               per staged slab (HWCN, N % 4 == 0, C % kt == 0)
 //                      kBVecN   16-byte vectors along the batch (HWCN, N % 4 == 0)
 //                      kBVecC   16-byte vectors along channels  (HWCN, N == 1, C % 4 == 0)
-//                      kBScalar single elements                 (any)
+//                      kBScalar single elements                 (HWCN, any)
+//                      kBVecW   16-byte vectors along W where four columns of one
+//                               output row allow it, else per-column elements (NCHW)
 enum AMode : int { kAVecM = 0, kAVecK = 1, kAScalar = 2 };
-enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3 };
+enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3, kBVecW = 4 };
 // The loader pairs that are instantiated.
 enum Variant : int {
   kVarHwcnVecN = 0,     // HWCN, A vec-M, B vec-N
   kVarHwcnVecC = 1,     // HWCN, A vec-M, B vec-C
   kVarHwcnVecA = 2,     // HWCN, A vec-M, B scalar
   kVarHwcnScalar = 3,   // HWCN, A scalar, B scalar
-  kVarNchwVecA = 4,     // NCHW, A vec-K, B scalar
-  kVarNchwScalar = 5,   // NCHW, A scalar, B scalar
+  kVarNchwVecA = 4,     // NCHW, A vec-K, B vec-W
+  kVarNchwScalar = 5,   // NCHW, A scalar, B vec-W
   kVarHwcnVecNTap = 6,  // HWCN, A vec-M, B vec-N with one tap per slab (the tuned path)
   kNumVariants = 7
 };

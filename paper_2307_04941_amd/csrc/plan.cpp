@@ -277,7 +277,7 @@ void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
       p->variant = kVarHwcnScalar;
     }
   } else {
-    p->b_mode = kBScalar;
+    p->b_mode = kBVecW;
     if (s.Kg % 4 == 0 && w16) p->a_mode = kAVecK, p->variant = kVarNchwVecA;
     else p->a_mode = kAScalar, p->variant = kVarNchwScalar;
   }
@@ -347,7 +347,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
 
 std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* an[] = {"vec_m", "vec_k", "scalar"};
-  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap"};
+  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap", "vec_w"};
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,

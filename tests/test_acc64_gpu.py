@@ -39,8 +39,8 @@ VARIANTS = [
     ((1, 12, 15, 15, 24, 3, 3, 1, 1), "HWCN", "vec_m", "vec_c"),
     ((3, 8, 10, 10, 16, 3, 3, 1, 1), "HWCN", "vec_m", "scalar"),
     ((3, 5, 9, 9, 7, 3, 3, 1, 1), "HWCN", "scalar", "scalar"),
-    ((2, 4, 9, 9, 16, 3, 3, 1, 1), "NCHW", "vec_k", "scalar"),
-    ((3, 5, 9, 9, 7, 3, 3, 1, 1), "NCHW", "scalar", "scalar"),
+    ((2, 4, 9, 9, 16, 3, 3, 1, 1), "NCHW", "vec_k", "vec_w"),
+    ((3, 5, 9, 9, 7, 3, 3, 1, 1), "NCHW", "scalar", "vec_w"),
 ]
 
 

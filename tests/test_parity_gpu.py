@@ -87,6 +87,35 @@ def test_every_tile_nchw(tile):
 TAIL_SHAPE = (24, 16, 111, 111, 32, 3, 3, 1, 1)
 
 
+# NCHW patch loader (16-byte runs along W, else per column): output widths
+# that do and do not divide by 4 (groups of four columns wrap to the next
+# output row or image), strides 1-3 along W, padding on either side, ragged
+# Ng, single-pixel outputs.  Integer data, so every output must be exact.
+NCHW_EDGES = [
+    (2, 3, 7, 9, 5, 3, 3, 1, 1),             # Wo 9: runs cross rows
+    (3, 4, 6, 4, 8, 3, 3, 1, (0, 1)),        # Wo 4, padding on both sides
+    (1, 8, 5, 18, 16, 1, 3, (1, 1), (0, 2)), # wide rows, pad 2 along W only
+    (5, 2, 9, 13, 7, 3, 5, 1, 2),            # Wo 13, N*Ho*Wo odd
+    (2, 16, 8, 11, 32, 3, 3, (1, 2), 1),     # stride 2 along W: element path
+    (4, 5, 10, 10, 9, 2, 2, (2, 3), (1, 0)), # stride 3 along W
+    (3, 6, 3, 3, 12, 3, 3, 1, 0),            # Wo 1
+    (2, 7, 4, 5, 6, 3, 2, 1, (1, 0)),        # Wo 4, every group one row
+    (1, 32, 14, 14, 64, 3, 3, 1, 1),         # Wo 14 (VGG conv5 blocks)
+    (2, 16, 28, 28, 24, 1, 1, 1, 0),         # 1x1, one contiguous plane per channel
+]
+
+
+@pytest.mark.parametrize("case", range(len(NCHW_EDGES)))
+def test_nchw_row_vector_loader(case):
+    shape = NCHW_EDGES[case]
+    say(f"NCHW loader edge {case} shape={shape}")
+    x, w, st, pd = make(shape, 700 + case, "NCHW", dist="int")
+    acc, _ = oracle.conv2d(x, w, st, pd, "NCHW")
+    for plan in (None, "tile=32x64,split=1", "tile=128x128,split=2"):
+        y = run_gpu(x, w, st, pd, "NCHW", plan=plan)
+        assert np.array_equal(y, acc.astype(np.float32)), f"{shape} {plan}"
+
+
 @pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
 @pytest.mark.parametrize("plan", ["tile=256x64,tail=2", "tile=256x64,tail=3", "tile=256x64,tail=5",
                                   "tile=64x256,tail=4", "tile=128x128,kt=32,tail=2"])
