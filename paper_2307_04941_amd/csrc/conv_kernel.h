@@ -356,10 +356,12 @@ struct BVecNTap {
 // Each thread owns four consecutive output columns n..n+3 (consecutive output
 // pixels of one image) and NV consecutive rows of the KT x NT tile.  With
 // stride_w == 1 the four columns of one output row read four consecutive
-// inputs along W, so when they lie inside the image one 16-byte load covers
-// them; otherwise (image borders, a group that wraps to the next output row,
-// any stride_w > 1) the four elements are loaded one by one from per-column
-// bases computed once per work-group.  The row index (c, r, s) advances by
+// inputs along W: one 16-byte load covers them, and elements that fall off
+// the left or right edge of the image row (padding) are zeroed afterwards --
+// the load itself only has to stay inside the tensor.  Otherwise (a group
+// that wraps to the next output row, any stride_w > 1, the tensor's first or
+// last words) the four elements are loaded one by one from per-column bases
+// computed once per work-group.  The row index (c, r, s) advances by
 // carries, with no division in the main loop.
 template <class C, int NT, int KT>
 struct BVecW {
@@ -374,6 +376,7 @@ struct BVecW {
   int dc, dr, ds;              // KT in the mixed radix (C, R, S)
   f32x4 v[NV], e4[NV];         // row loaded as one vector, or element by element
   bool fast_[NV];              // row i took the vector load
+  unsigned keep;               // bits 4i..4i+3: elements of row i's vector inside the image row
 
   __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
     n4 = t % NC4;
@@ -413,7 +416,9 @@ struct BVecW {
   }
   __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
     const int hw = a.H * a.W;
+    const int x_elems = (int)(a.x_bytes / 4u);
     int ci = c, ri = r, si = s;
+    keep = 0;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       if (i > 0) {
@@ -424,10 +429,14 @@ struct BVecW {
       }
       const int rel = ci * hw + ri * a.W + si;
       const bool k_ok = ci < a.C;
-      const int iw = iw0[0] + si;
-      const bool fast = vrow & k_ok & ((unsigned)(ih0[0] + ri) < (unsigned)a.H) & (iw >= 0) & (iw + 3 < a.W);
+      const int iw = iw0[0] + si, off = cb[0] + rel;
+      const bool fast = vrow & k_ok & ((unsigned)(ih0[0] + ri) < (unsigned)a.H) & (off >= 0) &
+                        (off + 3 < x_elems);
+      keep |= (((unsigned)iw < (unsigned)a.W) | (((unsigned)(iw + 1) < (unsigned)a.W) << 1) |
+               (((unsigned)(iw + 2) < (unsigned)a.W) << 2) | (((unsigned)(iw + 3) < (unsigned)a.W) << 3))
+              << (4 * i);
       fast_[i] = fast;
-      v[i] = bload4(xr, fast ? (unsigned)(cb[0] + rel) * 4u : kOOB);
+      v[i] = bload4(xr, fast ? (unsigned)off * 4u : kOOB);
       // separate registers: writing v[i] again would make the compiler wait
       // for the vector load here, inside the load phase
       if (!fast) {
@@ -445,7 +454,7 @@ struct BVecW {
     for (int i = 0; i < NV; ++i) {
       f32x4 o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = fast_[i] ? v[i][e] : e4[i][e];
+      for (int e = 0; e < 4; ++e) o[e] = fast_[i] ? (((keep >> (4 * i + e)) & 1u) ? v[i][e] : 0.f) : e4[i][e];
       st4(Bs + (kr0 + i) * C::BS + C::LB::col(kr0 + i, n4 * 4), o);
     }
   }
