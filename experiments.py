@@ -4,6 +4,7 @@
     python experiments.py adaptability [--workloads W,...] [--reps R] [--out FILE]
     python experiments.py ablation [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
     python experiments.py acc64 [--workloads W,...] [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
+    python experiments.py net [--nets vgg16,alexnet,resnet50] [--batch B] [--layout L] [--reps R] [--out FILE]
 
 adaptability -- Sec. 5.1: the channel-scale scenes (5.1.1), the batch sweep
     (5.1.2), the filter-size sweep (5.1.3) and the padding/stride sweep
@@ -21,6 +22,12 @@ acc64 -- the fp64-accumulating entry point (the paper's own numerics: fp32
     data, fp64 arithmetic, Sec. 4.1.1 / Alg. 2) against the fp32 one, per
     layer: TFLOPS and % of each path's MFMA peak (fp64 78.6, fp32 157.3),
     with the selector's plan and any fixed acc64 tile plans given.
+net -- whole convolution stacks of the real networks (Sec. 5.2) through the
+    native executor: VGG-16 and AlexNet feature extractors and the ResNet-50
+    trunk, with ReLU and residual additions fused into the convolutions and
+    max pooling between blocks.  Per network: forward time run eagerly and
+    replayed from a HIP graph, convolution TFLOPS over the whole forward, and
+    the activation arena against keeping every activation.
 
 Inputs are the seeded synthetic tensors of ``workloads`` (HWCN, resident on
 the GPU before timing).  Each scene is warmed up for ~100 ms, then timed over
@@ -128,13 +135,69 @@ def run_scenes(workload_names, plans, reps, emit, acc64_plans=None):
     return records
 
 
+def run_nets(names, batch, layout, reps, emit):
+    import torch
+
+    import workloads
+    import workloads.nets as nets
+    from paper_2307_04941_amd import mg3m
+
+    mg3m.load_library()
+    torch.cuda.set_device(0)
+    recs = []
+    for name in names:
+        N = batch.get(name, 64)
+        layers = nets.filters(nets.NETS[name](), layout, seed=1)
+        shape = (N, 3, 224, 224)
+        flops, shapes = nets.conv_flops(layers, shape)
+        net = mg3m.Net(layers, shape, layout)
+        kept = sum(4 * n * c * h * w for n, c, h, w in shapes[1:-1])
+        x = workloads.uniform((N, 3, 224, 224), 7)
+        if layout == "HWCN":
+            x = x.transpose(2, 3, 1, 0).copy()
+        xd = torch.from_numpy(x).cuda()
+        y = torch.empty(net.shape(net.n_layers), dtype=torch.float32, device="cuda")
+        s = torch.cuda.Stream()
+        res = {}
+        with torch.cuda.stream(s):
+            for mode in ("eager", "graph"):
+                t_end = time.perf_counter() + 0.2
+                while time.perf_counter() < t_end:
+                    net.forward(xd, out=y, graph=mode == "graph", stream=s)
+                    s.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(s)
+                for _ in range(reps):
+                    net.forward(xd, out=y, graph=mode == "graph", stream=s)
+                e1.record(s)
+                s.synchronize()
+                ms = e0.elapsed_time(e1) / reps
+                res[mode] = {"ms": round(ms, 3), "conv_tflops": round(flops / ms / 1e9, 2),
+                             "pct_peak": round(100 * flops / ms / 1e9 / PEAK_TFLOPS, 2)}
+        arena, ws = net.memory()
+        rec = {"net": name, "layout": layout, "N": N, "layers": len(layers),
+               "convs": sum(1 for d in layers if d["op"] == "conv"), "conv_gflop": round(flops / 1e9, 2),
+               "arena_mib": round(arena / 2**20, 1), "kept_mib": round(kept / 2**20, 1),
+               "workspace_mib": round(ws / 2**20, 1), **res}
+        recs.append(rec)
+        emit(rec)
+        net.close()
+        del xd, y
+        torch.cuda.empty_cache()
+    return recs
+
+
 def _mean(v):
     return round(sum(v) / len(v), 2) if v else None
 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64"])
+    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64", "net"])
+    ap.add_argument("--nets", default="vgg16,alexnet,resnet50")
+    ap.add_argument("--batch", default="vgg16=64,alexnet=128,resnet50=64",
+                    help="net: batch per network, name=N,...")
+    ap.add_argument("--layout", default="HWCN")
     ap.add_argument("--workloads", default=None)
     ap.add_argument("--fixed", default=None,
                     help="ablation / acc64: fixed plans separated by ';' (ablation default: "
@@ -152,7 +215,10 @@ def main():
             out.write(line + "\n")
             out.flush()
 
-    if a.mode == "adaptability":
+    if a.mode == "net":
+        batch = {k: int(v) for k, v in (kv.split("=") for kv in a.batch.split(","))}
+        run_nets(a.nets.split(","), batch, a.layout, a.reps, emit)
+    elif a.mode == "adaptability":
         names = (a.workloads.split(",") if a.workloads else
                  ["channel_scenes_n128", "batch_sweep", "filter_sweep_n128", "padstride_sweep_n128"])
         recs = run_scenes(names, [], a.reps, emit)

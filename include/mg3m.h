@@ -156,6 +156,95 @@ int conv2d_fwd_f32_acc64_plan_string(int N, int C, int H, int W, int K, int R, i
                                      int stride_h, int stride_w, int pad_h, int pad_w,
                                      int layout, const char *plan, char *buf, size_t len);
 
+/* y = act(conv(x, w) + add): the convolution of conv2d_fwd_f32_hw with the
+ * network's elementwise steps fused into its output stage (whole tiles store
+ * the finished value; split tiles finish it in the reduction), so the
+ * activation never makes an extra trip through HBM.  add: NULL, or a device
+ * tensor with y's shape and layout (a residual connection); it may be y
+ * itself (in place) but may not partly overlap it.  relu: 0 = none, 1 =
+ * max(v, 0) with NaN kept.  Workspace, plan override and errors as for
+ * conv2d_fwd_f32_hw (workspace size from conv2d_fwd_f32_hw_workspace_bytes). */
+int conv2d_fwd_f32_fused(const float *x, const float *w, float *y, const float *add, int relu,
+                         int N, int C, int H, int W, int K, int R, int S,
+                         int stride_h, int stride_w, int pad_h, int pad_w, int layout,
+                         void *workspace, size_t workspace_bytes,
+                         const char *plan, void *stream);
+
+/* Max pooling over R x S windows with stride and padding per axis, padded
+ * taps ignored (the pooling layers of VGG, AlexNet and ResNet), in either
+ * layout: x[H][W][C][N] -> y[Ho][Wo][C][N], or x[N][C][H][W] ->
+ * y[N][C][Ho][Wo].  Ho, Wo by the convolution's floor formula.  Padding is
+ * at most half the window on each axis, so every window holds an input.  A
+ * NaN in a window gives NaN.  Device pointers, stream-ordered; errors as for
+ * conv2d_fwd_f32 (MG3M_ERR_SHAPE also for padding over half the window). */
+int maxpool2d_f32(const float *x, float *y, int N, int C, int H, int W, int R, int S,
+                  int stride_h, int stride_w, int pad_h, int pad_w, int layout, void *stream);
+
+/* Output size of maxpool2d_f32 (host only). */
+int maxpool2d_out_dims(int H, int W, int R, int S, int stride_h, int stride_w,
+                       int pad_h, int pad_w, int *Ho, int *Wo);
+
+/* ---------------------------------------------------------------------------
+ * Network executor: a chain of convolution and pooling layers run back to
+ * back on the device (the convolution stacks of the real networks of
+ * Sec. 5.2), activations kept in one device arena, all launches on one
+ * stream, optionally replayed from a captured HIP graph.
+ *
+ * Activations are numbered: 0 is the network input, i >= 1 the output of
+ * layer i-1; the last layer writes the caller's y.  A layer reads any earlier
+ * activation, so branches and residual connections are expressed by `input`
+ * and `add`. */
+enum mg3m_op {
+    MG3M_OP_CONV = 0,        /* y = act(conv(in, w) + add) */
+    MG3M_OP_MAXPOOL = 1      /* y = maxpool(in) */
+};
+
+typedef struct mg3m_layer {
+    int op;                  /* MG3M_OP_* */
+    int input;               /* activation read (0 .. layer index) */
+    int add;                 /* CONV: activation added before the ReLU (same shape as the output), -1 = none */
+    int relu;                /* CONV: 1 = ReLU, 0 = none */
+    int K;                   /* CONV: output channels */
+    int R, S;                /* filter (CONV) or window (MAXPOOL) height and width */
+    int stride, pad;         /* both axes */
+    const float *w;          /* CONV: device filter in the network's layout (HWCN [R][S][C][K], NCHW [K][C][R][S]),
+                                owned by the caller and kept alive while the network is used */
+} mg3m_layer;
+
+typedef struct mg3m_net mg3m_net;
+
+/* Validate the chain for an input of N images of C x H x W, infer every
+ * activation's shape, plan every convolution, and allocate (hipMalloc, on the
+ * current device) one arena for the activations and one split-K workspace.
+ * keep_all = 0: activations share arena space once no later layer reads
+ * them (liveness); 1: every activation keeps its own space, for inspection.
+ * On success *net is set; on failure nothing is allocated and the status
+ * (MG3M_ERR_ARG for a bad layer list, _SHAPE, _LAYOUT, _TOO_LARGE, _HIP) is
+ * returned with the failing layer in mg3m_last_error(). */
+int mg3m_net_create(const mg3m_layer *layers, int n_layers, int N, int C, int H, int W,
+                    int layout, int keep_all, mg3m_net **net);
+
+/* Shape of activation id (0 .. n_layers) and, for 1 .. n_layers-1, its device
+ * pointer in the arena (NULL for the input and the output, which the caller
+ * owns).  Host only.  ptr may be NULL. */
+int mg3m_net_activation(const mg3m_net *net, int id, int *C, int *H, int *W, const float **ptr);
+
+/* Bytes of the activation arena and of the split-K workspace (host only). */
+int mg3m_net_memory(const mg3m_net *net, size_t *arena_bytes, size_t *workspace_bytes);
+
+/* Run the whole chain: x (activation 0) -> y (the last activation), both
+ * device tensors in the network's layout, on `stream` (NULL = default).
+ * Calls on one network must not overlap (they share the arena). */
+int mg3m_net_forward(mg3m_net *net, const float *x, float *y, void *stream);
+
+/* As mg3m_net_forward, replayed from a HIP graph captured on the first call
+ * (and again whenever x, y or stream differ from the captured ones).  stream
+ * must not be the default stream (it cannot be captured): MG3M_ERR_ARG. */
+int mg3m_net_forward_graph(mg3m_net *net, const float *x, float *y, void *stream);
+
+/* Free the arena, the workspace and any captured graph (NULL is accepted). */
+int mg3m_net_destroy(mg3m_net *net);
+
 /* The plan the selector (or the override) picks for this shape, as text,
  * e.g. "tile=128x128,waves=2x2,kt=16,split=1,grid=1568,...".  Host only; no
  * HIP call.  buf: host buffer of `len` bytes, always NUL-terminated on

@@ -4,9 +4,11 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  The product (``paper_2307_04941_amd``)
 never imports it, and it imports nothing from the product.
 
-The arithmetic lives in ``direct_conv.c`` (plain C, seven nested loops of
-Eq. 1 of the MG3MConv paper, Sec. 2.1, accumulated in fp64).  This module only
-builds that file with gcc and marshals numpy arrays into it.
+The convolution's arithmetic lives in ``direct_conv.c`` (plain C, seven
+nested loops of Eq. 1 of the MG3MConv paper, Sec. 2.1, accumulated in fp64);
+this module builds that file with gcc and marshals numpy arrays into it.
+``maxpool2d`` -- the pooling between the convolution blocks of the networks
+the paper runs (Sec. 5.2) -- is written here in numpy, from its definition.
 """
 from __future__ import annotations
 
@@ -148,3 +150,40 @@ def check(y: np.ndarray, acc: np.ndarray, mag: np.ndarray, rtol: float = 1e-5):
     if np.isnan(ratio).any():
         worst = float("inf")
     return n_fail == 0, worst, n_fail, first
+
+
+def maxpool2d(x: np.ndarray, R, S=None, stride=None, pad=0, layout="NCHW"):
+    """Max pooling from its definition: y[b,c,oh,ow] = max over the window taps
+    (r, s) in [0,R) x [0,S) whose input position ih = oh*sh + r - ph,
+    iw = ow*sw + s - pw lies inside the image (padded taps are skipped, never
+    read as a value).  Output size by the same floor formula as the
+    convolution.  A NaN in a window gives NaN.  stride defaults to the window.
+    Returns a float32 array in ``layout`` (NCHW x[N,C,H,W] or HWCN x[H,W,C,N]).
+    Parity unpinned by the paper, which prints no pooling example; pinned in
+    tests by hand-computed values, brute force and scipy.ndimage."""
+    lay = LAYOUTS[layout] if isinstance(layout, str) else int(layout)
+    S = R if S is None else S
+    sh, sw = _pair((R, S) if stride is None else stride)
+    ph, pw = _pair(pad)
+    x = np.asarray(x, dtype=np.float32)
+    xn = x if lay == NCHW else np.transpose(x, (3, 2, 0, 1))        # -> [N, C, H, W]
+    N, C, H, W = xn.shape
+    Ho, Wo = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    if Ho < 1 or Wo < 1:
+        raise ValueError("empty pooling output")
+    y = np.full((N, C, Ho, Wo), -np.inf, np.float32)
+    oh, ow = np.arange(Ho), np.arange(Wo)
+    for r in range(R):
+        ih = oh * sh + r - ph
+        rows = (ih >= 0) & (ih < H)
+        for s in range(S):
+            iw = ow * sw + s - pw
+            cols = (iw >= 0) & (iw < W)
+            if not rows.any() or not cols.any():
+                continue
+            tap = xn[:, :, ih[rows]][:, :, :, iw[cols]]
+            cur = y[:, :, rows][:, :, :, cols]
+            # NaN-propagating maximum
+            new = np.where(np.isnan(tap) | (tap > cur), tap, cur)
+            y[np.ix_(np.arange(N), np.arange(C), np.flatnonzero(rows), np.flatnonzero(cols))] = new
+    return y if lay == NCHW else np.ascontiguousarray(np.transpose(y, (2, 3, 1, 0)))

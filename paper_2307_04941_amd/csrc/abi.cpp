@@ -31,14 +31,7 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   return pa < pb + nb && pb < pa + na;
 }
 
-// A convolution's arguments as the entry points receive them, and which
-// kernel family computes it (fp32 or fp64 accumulation).
-struct Geom {
-  int N, C, H, W, K, R, S;
-  int sh, sw, ph, pw;
-  int layout;
-  bool acc64;
-};
+using Geom = mg3m::ConvGeom;
 
 Geom geom(int N, int C, int H, int W, int K, int R, int S, int sh, int sw, int ph, int pw, int layout,
           bool acc64 = false) {
@@ -56,11 +49,13 @@ int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16
 }
 
 int run(const float* x, const float* w, float* y, const Geom& g, void* workspace,
-        size_t workspace_bytes, bool own_workspace, const char* plan, void* stream) {
+        size_t workspace_bytes, bool own_workspace, const char* plan, void* stream,
+        const float* add = nullptr, int relu = 0) {
   g_last_error.clear();
   if (x == nullptr || w == nullptr || y == nullptr) return fail(MG3M_ERR_NULL, "x, w and y must be non-NULL");
-  if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4))
-    return fail(MG3M_ERR_ALIGN, "x, w and y must be 4-byte aligned");
+  if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(add, 4))
+    return fail(MG3M_ERR_ALIGN, "x, w, y and add must be 4-byte aligned");
+  if (relu != 0 && relu != 1) return fail(MG3M_ERR_ARG, "relu must be 0 or 1");
   mg3m::ConvShape s;
   mg3m::Plan p;
   int rc = shape_and_plan(g, plan, aligned(x, 16), aligned(w, 16), aligned(y, 16), &s, &p);
@@ -70,6 +65,9 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   const size_t yb = 4ull * (size_t)s.Mg * (size_t)s.Ng;
   if (overlap(y, yb, x, xb) || overlap(y, yb, w, wb))
     return fail(MG3M_ERR_ALIAS, "y overlaps x or w");
+  // add may be y itself (each output reads its own add element first), or disjoint from it
+  if (add != nullptr && add != y && overlap(add, yb, y, yb))
+    return fail(MG3M_ERR_ALIAS, "add partly overlaps y");
 
   float* ws = nullptr;
   if (p.tail_tiles > 0) {
@@ -98,6 +96,8 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   a.dp_tiles = p.dp_tiles; a.tail_tiles = p.tail_tiles > 0 ? p.tail_tiles : 1; a.kps = p.kps;
   a.e_mode = p.e_mode;
   a.mstride = s.layout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
+  a.add = add;
+  a.relu = relu;
 
   std::string err;
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
@@ -120,6 +120,8 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     const bool contiguous4 = s.layout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
     r.vec4 = contiguous4 && aligned(y, 16);
     r.f64 = p.acc64;
+    r.add = add;
+    r.relu = relu;
     rc = mg3m::launch_tail_reduce(r, stream, &err);
   }
   if (own_workspace && ws != nullptr) {
@@ -135,7 +137,100 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
 
 }  // namespace
 
+namespace mg3m {
+
+int set_error(int status, const std::string& msg) { return fail(status, msg); }
+void clear_error() { g_last_error.clear(); }
+
+int conv_run(const float* x, const float* w, float* y, const ConvGeom& g, void* workspace,
+             size_t workspace_bytes, bool own_workspace, const char* plan, const float* add, int relu,
+             void* stream) {
+  try {
+    return run(x, w, y, g, workspace, workspace_bytes, own_workspace, plan, stream, add, relu);
+  } catch (const std::exception& e) {
+    return fail(MG3M_ERR_HIP, e.what());
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+int conv_plan(const ConvGeom& g, const char* plan, ConvShape* s, Plan* p) {
+  return shape_and_plan(g, plan, true, true, true, s, p);
+}
+
+int maxpool_dims(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* Ho, int* Wo,
+                 std::string* err) {
+  if (H < 1 || W < 1 || R < 1 || S < 1 || sh < 1 || sw < 1 || ph < 0 || pw < 0) {
+    *err = "pooling: sizes and strides must be >= 1, pads >= 0";
+    return MG3M_ERR_SHAPE;
+  }
+  if (2 * ph > R || 2 * pw > S) {
+    *err = "pooling: padding must be at most half the window";
+    return MG3M_ERR_SHAPE;
+  }
+  ConvShape s;
+  int rc = make_shape(1, 1, H, W, 1, R, S, sh, sw, ph, pw, kHWCN, &s, err);
+  if (rc) return rc;
+  *Ho = s.Ho;
+  *Wo = s.Wo;
+  return MG3M_OK;
+}
+
+int maxpool_run(const float* x, float* y, int N, int C, int H, int W, int R, int S, int sh, int sw,
+                int ph, int pw, int layout, void* stream) {
+  try {
+    g_last_error.clear();
+    if (x == nullptr || y == nullptr) return fail(MG3M_ERR_NULL, "x and y must be non-NULL");
+    if (!aligned(x, 4) || !aligned(y, 4)) return fail(MG3M_ERR_ALIGN, "x and y must be 4-byte aligned");
+    if (layout != kHWCN && layout != kNCHW) return fail(MG3M_ERR_LAYOUT, "unknown layout");
+    if (N < 1 || C < 1) return fail(MG3M_ERR_SHAPE, "N and C must be >= 1");
+    std::string err;
+    int Ho = 0, Wo = 0;
+    int rc = maxpool_dims(H, W, R, S, sh, sw, ph, pw, &Ho, &Wo, &err);
+    if (rc) return fail(rc, err);
+    const long long xe = (long long)N * C * H * W, ye = (long long)N * C * Ho * Wo;
+    if (xe > kMaxTensorBytes / 4 || ye > kMaxTensorBytes / 4)
+      return fail(MG3M_ERR_TOO_LARGE, "a tensor is larger than 4 GiB - 64 bytes");
+    if (overlap(y, 4 * (size_t)ye, x, 4 * (size_t)xe)) return fail(MG3M_ERR_ALIAS, "y overlaps x");
+    PArgs p{};
+    p.x = x; p.y = y;
+    p.N = N; p.C = C; p.H = H; p.W = W; p.R = R; p.S = S;
+    p.sh = sh; p.sw = sw; p.ph = ph; p.pw = pw; p.Ho = Ho; p.Wo = Wo;
+    p.layout = layout;
+    p.aligned16 = aligned(x, 16) && aligned(y, 16);
+    rc = launch_maxpool(p, stream, &err);
+    if (rc) return fail(rc, err);
+    return MG3M_OK;
+  } catch (...) {
+    return fail(MG3M_ERR_HIP, "unknown exception");
+  }
+}
+
+}  // namespace mg3m
+
 extern "C" {
+
+int conv2d_fwd_f32_fused(const float* x, const float* w, float* y, const float* add, int relu, int N,
+                         int C, int H, int W, int K, int R, int S, int stride_h, int stride_w,
+                         int pad_h, int pad_w, int layout, void* workspace, size_t workspace_bytes,
+                         const char* plan, void* stream) {
+  return mg3m::conv_run(x, w, y, geom(N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, layout),
+                        workspace, workspace_bytes, false, plan, add, relu, stream);
+}
+
+int maxpool2d_f32(const float* x, float* y, int N, int C, int H, int W, int R, int S, int stride_h,
+                  int stride_w, int pad_h, int pad_w, int layout, void* stream) {
+  return mg3m::maxpool_run(x, y, N, C, H, W, R, S, stride_h, stride_w, pad_h, pad_w, layout, stream);
+}
+
+int maxpool2d_out_dims(int H, int W, int R, int S, int stride_h, int stride_w, int pad_h, int pad_w,
+                       int* Ho, int* Wo) {
+  g_last_error.clear();
+  if (Ho == nullptr || Wo == nullptr) return fail(MG3M_ERR_NULL, "Ho and Wo must be non-NULL");
+  std::string err;
+  int rc = mg3m::maxpool_dims(H, W, R, S, stride_h, stride_w, pad_h, pad_w, Ho, Wo, &err);
+  return rc ? fail(rc, err) : MG3M_OK;
+}
 
 int conv2d_out_dims_hw(int H, int W, int R, int S, int stride_h, int stride_w, int pad_h, int pad_w,
                        int* Ho, int* Wo) {

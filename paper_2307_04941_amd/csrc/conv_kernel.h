@@ -760,6 +760,12 @@ __device__ __forceinline__ int out_colbase(const KArgs& a, int n) {
   }
 }
 
+// Fused output stage: y = act(conv + add), for the network executor.
+__device__ __forceinline__ float finish1(const KArgs& a, float v, int idx) {
+  if (a.add != nullptr) v += a.add[idx];
+  return (a.relu != 0 && v < 0.f) ? 0.f : v;
+}
+
 // ------------------------------------------------------------------ kernel
 template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
 __global__ __launch_bounds__(WM * WN * 64)
@@ -841,6 +847,7 @@ void conv_igemm_f32(KArgs a) {
     return;
   }
   float* const out = a.y;
+  const bool fused = (a.add != nullptr) | (a.relu != 0);
 #pragma unroll
   for (int j = 0; j < C::TN; ++j) {
     const int n = n0 + wn * C::WTN + j * 32 + q;
@@ -853,13 +860,21 @@ void conv_igemm_f32(KArgs a) {
         const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
         if (a.e_mode == kEVecM) {
           // four consecutive output channels, contiguous when mstride == 1
-          if (row0 < a.Mg)
-            st4(out + colbase + row0,
-                f32x4{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]});
+          if (row0 < a.Mg) {
+            f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+            if (fused) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
+            }
+            st4(out + colbase + row0, v);
+          }
         } else {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (row0 + e < a.Mg) out[colbase + (row0 + e) * a.mstride] = acc[i][j][4 * g + e];
+            if (row0 + e < a.Mg) {
+              const int idx = colbase + (row0 + e) * a.mstride;
+              out[idx] = fused ? finish1(a, acc[i][j][4 * g + e], idx) : acc[i][j][4 * g + e];
+            }
         }
       }
   }

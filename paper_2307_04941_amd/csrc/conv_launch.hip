@@ -56,12 +56,24 @@ __global__ __launch_bounds__(256) void tail_reduce(RArgs r) {
     const int b = n / r.HoWo, pix = n - b * r.HoWo;   // y[N][K][Ho][Wo]
     return ((long long)b * r.K + m) * r.HoWo + pix;
   };
+  auto finish = [&](float v, long long idx) {
+    if (r.add != nullptr) v += r.add[idx];
+    return (r.relu != 0 && v < 0.f) ? 0.f : v;
+  };
   if (r.vec4 && n0 + 3 < r.Ng) {
-    *reinterpret_cast<f32x4r*>(r.y + index(n0)) = sum;
+    const long long i0 = index(n0);
+    if ((r.add != nullptr) | (r.relu != 0)) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sum[q] = finish(sum[q], i0 + q);
+    }
+    *reinterpret_cast<f32x4r*>(r.y + i0) = sum;
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (n0 + q < r.Ng) r.y[index(n0 + q)] = sum[q];
+      if (n0 + q < r.Ng) {
+        const long long idx = index(n0 + q);
+        r.y[idx] = finish(sum[q], idx);
+      }
   }
 }
 

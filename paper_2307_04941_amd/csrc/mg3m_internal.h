@@ -164,6 +164,8 @@ struct KArgs {
   int dp_tiles, tail_tiles, kps;
   int e_mode;
   int mstride;              // output elements between output channels m and m+1
+  const float* add;         // added to each output before the activation (y's layout), or null
+  int relu;                 // 1: y = max(y, 0) (NaN kept)
 };
 
 // Arguments of the tail reduction.
@@ -175,6 +177,27 @@ struct RArgs {
   int layout, N, K, HoWo, Mg, Ng;
   int vec4;                 // four consecutive columns are contiguous in y
   int f64;                  // the partials are fp64
+  const float* add;         // as in KArgs
+  int relu;
+};
+
+// Arguments of max pooling.
+struct PArgs {
+  const float* x;
+  float* y;
+  int N, C, H, W, R, S;
+  int sh, sw, ph, pw, Ho, Wo;
+  int layout;
+  int aligned16;            // x and y are 16-byte aligned
+};
+
+// A convolution's arguments as the entry points receive them, and which
+// kernel family computes it (fp32 or fp64 accumulation).
+struct ConvGeom {
+  int N, C, H, W, K, R, S;
+  int sh, sw, ph, pw;
+  int layout;
+  bool acc64;
 };
 
 // Planner (host only, no HIP calls).  Returns 0 or an mg3m_status code and
@@ -198,8 +221,27 @@ KernelFn conv_kernel64_hwcn_vecn_tap(int tile);
 KernelFn conv_kernel64_hwcn(int variant, int tile);
 KernelFn conv_kernel64_nchw(int variant, int tile);
 
-// Kernel launchers (conv_launch.hip).
+// Kernel launchers (conv_launch.hip, pool.hip).
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
 int launch_tail_reduce(const RArgs& r, void* stream, std::string* err);
+int launch_maxpool(const PArgs& p, void* stream, std::string* err);
+
+// Shared by the C entry points and the network executor (abi.cpp): validate,
+// plan and launch one convolution (y = act(conv + add)).  own_workspace: take
+// a split plan's partials from hipMallocAsync on `stream` instead of
+// `workspace`.  Returns an mg3m_status and records the message for
+// mg3m_last_error().
+int conv_run(const float* x, const float* w, float* y, const ConvGeom& g, void* workspace,
+             size_t workspace_bytes, bool own_workspace, const char* plan, const float* add, int relu,
+             void* stream);
+int conv_plan(const ConvGeom& g, const char* plan, ConvShape* s, Plan* p);   // host only
+// Validate and launch one max pooling; pads at most half the window.
+int maxpool_run(const float* x, float* y, int N, int C, int H, int W, int R, int S, int sh, int sw,
+                int ph, int pw, int layout, void* stream);
+int maxpool_dims(int H, int W, int R, int S, int sh, int sw, int ph, int pw, int* Ho, int* Wo,
+                 std::string* err);
+// Record a status and message for mg3m_last_error() (calling thread); returns status.
+int set_error(int status, const std::string& msg);
+void clear_error();
 
 }  // namespace mg3m

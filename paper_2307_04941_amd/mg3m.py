@@ -50,6 +50,17 @@ class PlanInfo(ctypes.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
+class Layer(ctypes.Structure):
+    """mg3m_layer: one layer of a network for the executor."""
+    _fields_ = [
+        ("op", ctypes.c_int), ("input", ctypes.c_int), ("add", ctypes.c_int), ("relu", ctypes.c_int),
+        ("K", ctypes.c_int), ("R", ctypes.c_int), ("S", ctypes.c_int),
+        ("stride", ctypes.c_int), ("pad", ctypes.c_int), ("w", ctypes.c_void_p),
+    ]
+
+
+OP_CONV, OP_MAXPOOL = 0, 1
+
 _lib = None
 
 
@@ -69,6 +80,16 @@ def load_library(path: str = LIB_PATH):
     lib.conv2d_fwd_f32_hw.argtypes = [p, p, p] + shape_hw + [p, sz, cp, p]
     lib.conv2d_fwd_f32_hw_workspace_bytes.argtypes = shape_hw + [cp, ctypes.POINTER(sz)]
     lib.conv2d_fwd_f32_acc64.argtypes = [p, p, p] + shape_hw + [cp, p]
+    lib.conv2d_fwd_f32_fused.argtypes = [p, p, p, p, i] + shape_hw + [p, sz, cp, p]
+    lib.maxpool2d_f32.argtypes = [p, p] + [i] * 11 + [p]
+    lib.maxpool2d_out_dims.argtypes = [i] * 8 + [ctypes.POINTER(i)] * 2
+    lib.mg3m_net_create.argtypes = [ctypes.POINTER(Layer), i, i, i, i, i, i, i, ctypes.POINTER(p)]
+    lib.mg3m_net_activation.argtypes = [p, i, ctypes.POINTER(i), ctypes.POINTER(i), ctypes.POINTER(i),
+                                        ctypes.POINTER(p)]
+    lib.mg3m_net_memory.argtypes = [p, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.mg3m_net_forward.argtypes = [p, p, p, p]
+    lib.mg3m_net_forward_graph.argtypes = [p, p, p, p]
+    lib.mg3m_net_destroy.argtypes = [p]
     lib.conv2d_fwd_f32_acc64_plan_string.argtypes = shape_hw + [cp, ctypes.c_char_p, sz]
     lib.conv2d_fwd_f32.argtypes = [p, p, p] + shape + [p]
     lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
@@ -83,7 +104,10 @@ def load_library(path: str = LIB_PATH):
     lib.mg3m_last_error.restype = ctypes.c_char_p
     for name in ("conv2d_out_dims", "conv2d_out_dims_hw", "conv2d_fwd_f32_hw",
                  "conv2d_fwd_f32_hw_workspace_bytes", "conv2d_fwd_f32_acc64",
-                 "conv2d_fwd_f32_acc64_plan_string", "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
+                 "conv2d_fwd_f32_acc64_plan_string", "conv2d_fwd_f32_fused", "maxpool2d_f32",
+                 "maxpool2d_out_dims", "mg3m_net_create", "mg3m_net_activation", "mg3m_net_memory",
+                 "mg3m_net_forward", "mg3m_net_forward_graph", "mg3m_net_destroy",
+                 "conv2d_fwd_f32", "conv2d_fwd_f32_ex",
                  "conv2d_fwd_f32_workspace_bytes", "conv2d_fwd_f32_plan_string",
                  "conv2d_fwd_f32_plan_info", "mg3m_padding_overhead", "mg3m_time_next_kernel"):
         getattr(lib, name).restype = i
@@ -184,6 +208,128 @@ def conv2d_fwd_f32_acc64_plan_string(N, C, H, W, K, R, S, stride_h, stride_w, pa
         N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w, _layout(layout), _enc(plan), buf,
         len(buf)))
     return buf.value.decode()
+
+
+def conv2d_fwd_f32_fused(x, w, y, add, relu, N, C, H, W, K, R, S, stride_h, stride_w, pad_h, pad_w,
+                         layout, workspace=None, workspace_bytes=0, plan=None, stream=None):
+    _check(load_library().conv2d_fwd_f32_fused(
+        _ptr(x), _ptr(w), _ptr(y), _ptr(add), int(relu), N, C, H, W, K, R, S, stride_h, stride_w,
+        pad_h, pad_w, _layout(layout), _ptr(workspace), workspace_bytes, _enc(plan), _stream(stream)))
+
+
+def maxpool2d_out_dims(H, W, R, S, stride_h, stride_w, pad_h, pad_w):
+    ho, wo = ctypes.c_int(), ctypes.c_int()
+    _check(load_library().maxpool2d_out_dims(H, W, R, S, stride_h, stride_w, pad_h, pad_w,
+                                             ctypes.byref(ho), ctypes.byref(wo)))
+    return ho.value, wo.value
+
+
+def maxpool2d_f32(x, y, N, C, H, W, R, S, stride_h, stride_w, pad_h, pad_w, layout, stream=None):
+    _check(load_library().maxpool2d_f32(_ptr(x), _ptr(y), N, C, H, W, R, S, stride_h, stride_w,
+                                        pad_h, pad_w, _layout(layout), _stream(stream)))
+
+
+def maxpool2d(x, R, S=None, stride=None, pad=0, layout="HWCN", out=None, stream=None):
+    """Max pooling of a torch tensor on the GPU (allocates y unless `out`)."""
+    import torch
+    S = R if S is None else S
+    sh, sw = _pair(R if stride is None else stride)
+    ph, pw = _pair(pad)
+    if _layout(layout) == HWCN:
+        H, W, C, N = x.shape
+    else:
+        N, C, H, W = x.shape
+    Ho, Wo = maxpool2d_out_dims(H, W, R, S, sh, sw, ph, pw)
+    shape = (Ho, Wo, C, N) if _layout(layout) == HWCN else (N, C, Ho, Wo)
+    y = out if out is not None else torch.empty(shape, dtype=torch.float32, device=x.device)
+    maxpool2d_f32(x, y, N, C, H, W, R, S, sh, sw, ph, pw, layout, stream)
+    return y
+
+
+class Net:
+    """A chain of layers run by the native executor (mg3m_net_*).
+
+    layers: list of dicts with keys op ("conv" or "maxpool"), input (activation
+    id, default: the previous layer's output), and for "conv": K, R, S, stride,
+    pad, relu, add (activation id or -1) and w (a device filter tensor in the
+    network's layout, kept referenced here); for "maxpool": R, S, stride, pad.
+    input_shape: (N, C, H, W).  keep_all: keep every activation (inspection)."""
+
+    def __init__(self, layers, input_shape, layout="HWCN", keep_all=False):
+        lib = load_library()
+        self._filters = []
+        arr = (Layer * len(layers))()
+        for i, d in enumerate(layers):
+            conv = d["op"] == "conv"
+            w = d.get("w") if conv else None
+            if conv:
+                self._filters.append(w)
+            arr[i] = Layer(OP_CONV if conv else OP_MAXPOOL, int(d.get("input", i)), int(d.get("add", -1)),
+                           int(d.get("relu", 0)), int(d.get("K", 0)), int(d["R"]), int(d.get("S", d["R"])),
+                           int(d.get("stride", 1)), int(d.get("pad", 0)), _ptr(w) if w is not None else None)
+        self.n_layers = len(layers)
+        self.layout = layout
+        self.input_shape = tuple(input_shape)
+        self._h = ctypes.c_void_p()
+        N, C, H, W = input_shape
+        _check(lib.mg3m_net_create(arr, len(layers), N, C, H, W, _layout(layout), int(keep_all),
+                                   ctypes.byref(self._h)))
+
+    def dims(self, i):
+        """(C, H, W) of activation i (0 = input, n_layers = output)."""
+        c, h, w = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+        _check(load_library().mg3m_net_activation(self._h, i, ctypes.byref(c), ctypes.byref(h),
+                                                  ctypes.byref(w), None))
+        return c.value, h.value, w.value
+
+    def shape(self, i):
+        c, h, w = self.dims(i)
+        n = self.input_shape[0]
+        return (h, w, c, n) if _layout(self.layout) == HWCN else (n, c, h, w)
+
+    def activation(self, i):
+        """A torch view of stored activation i (1 .. n_layers-1), valid after a
+        forward pass (every one of them only with keep_all)."""
+        import torch
+        c, h, w, p = ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_void_p()
+        _check(load_library().mg3m_net_activation(self._h, i, ctypes.byref(c), ctypes.byref(h),
+                                                  ctypes.byref(w), ctypes.byref(p)))
+        if not p.value:
+            raise ValueError("activation 0 and the last one are the caller's tensors")
+        n = self.input_shape[0] * c.value * h.value * w.value
+        return _device_view(p.value, n, torch).view(self.shape(i))
+
+    def memory(self):
+        a, b = ctypes.c_size_t(), ctypes.c_size_t()
+        _check(load_library().mg3m_net_memory(self._h, ctypes.byref(a), ctypes.byref(b)))
+        return a.value, b.value
+
+    def forward(self, x, out=None, graph=False, stream=None):
+        import torch
+        y = out if out is not None else torch.empty(self.shape(self.n_layers), dtype=torch.float32,
+                                                     device=x.device)
+        fn = load_library().mg3m_net_forward_graph if graph else load_library().mg3m_net_forward
+        _check(fn(self._h, _ptr(x), _ptr(y), _stream(stream)))
+        return y
+
+    def close(self):
+        if self._h:
+            load_library().mg3m_net_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _device_view(addr, n, torch):
+    """A float32 torch tensor over n floats of device memory at addr (no copy,
+    not owned)."""
+    class _Holder:
+        __cuda_array_interface__ = {"shape": (n,), "typestr": "<f4", "data": (addr, False), "version": 2}
+    return torch.as_tensor(_Holder(), device="cuda")
 
 
 def conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):

@@ -295,3 +295,83 @@ def test_acc64_errors():
     # split and tail overrides are accepted (fp64 partials)
     assert "split=2" in mg3m.conv2d_fwd_f32_acc64_plan_string(4, 64, 14, 14, 96, 3, 3, 1, 1, 1, 1,
                                                                "HWCN", "tile=64x64,split=2")
+
+
+# ------------------------------------------------------------ network executor
+def _layers(specs):
+    arr = (mg3m.Layer * len(specs))()
+    for i, d in enumerate(specs):
+        arr[i] = mg3m.Layer(d.get("op", 0), d.get("input", i), d.get("add", -1), d.get("relu", 0),
+                            d.get("K", 8), d.get("R", 3), d.get("S", 3), d.get("stride", 1), d.get("pad", 1),
+                            d.get("w", Wp))
+    return arr
+
+
+@pytest.mark.parametrize("specs,status", [
+    ([], 10),                                                         # no layers
+    ([{"input": 1}], 10),                                             # reads a later activation
+    ([{"input": -1}], 10),
+    ([{"op": 7}], 10),                                                # unknown op
+    ([{"w": None}], 1),                                               # conv without a filter
+    ([{"relu": 2}], 10),
+    ([{"K": 8}, {"K": 16, "add": 1}], 2),                             # residual of another shape
+    ([{"K": 8}, {"K": 8, "add": 2}], 10),                             # residual from the future
+    ([{"op": 1, "R": 2, "pad": 2}], 2),                               # pool padding over half the window
+    ([{"op": 1, "R": 2, "pad": 0, "relu": 1}], 10),                   # pool with an activation
+    ([{"R": 9, "pad": 0}], 2),                                        # filter larger than the input
+])
+def test_net_create_rejects_bad_chains(specs, status):
+    import ctypes
+    lib = mg3m.load_library()
+    h = ctypes.c_void_p()
+    arr = _layers(specs) if specs else (mg3m.Layer * 1)()
+    rc = lib.mg3m_net_create(arr, len(specs), 2, 4, 6, 6, 0, 0, ctypes.byref(h))
+    assert rc == status, mg3m.mg3m_last_error()
+    assert not h.value
+    assert mg3m.mg3m_last_error() != ""
+
+
+def test_net_create_argument_errors():
+    import ctypes
+    lib = mg3m.load_library()
+    h = ctypes.c_void_p()
+    arr = _layers([{}])
+    assert lib.mg3m_net_create(arr, 1, 2, 4, 6, 6, 3, 0, ctypes.byref(h)) == 3       # layout
+    assert lib.mg3m_net_create(arr, 1, 0, 4, 6, 6, 0, 0, ctypes.byref(h)) == 2       # N
+    assert lib.mg3m_net_create(arr, 1, 2, 4, 6, 6, 0, 2, ctypes.byref(h)) == 10      # keep_all
+    assert lib.mg3m_net_create(None, 1, 2, 4, 6, 6, 0, 0, ctypes.byref(h)) == 1
+    assert lib.mg3m_net_destroy(None) == 0
+
+
+def test_network_definitions_shapes_and_flops():
+    import workloads.nets as nets
+    fl, shapes = nets.conv_flops(nets.vgg16_features(), (64, 3, 224, 224))
+    vgg = workloads.workload("vgg16_n64")
+    assert fl == pytest.approx(sum(2.0 * L.N * L.K * L.C * L.R * L.S *
+                                   oracle.out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)[0] ** 2 for L in vgg))
+    assert shapes[-1] == (64, 512, 7, 7)
+    fl, shapes = nets.conv_flops(nets.resnet50_trunk(), (1, 3, 224, 224))
+    assert shapes[-1] == (1, 2048, 7, 7)
+    assert 8.0e9 < fl < 8.4e9            # ~4.1 GMAC per image in the convolutions
+    fl, shapes = nets.conv_flops(nets.alexnet_features(), (1, 3, 224, 224))
+    assert shapes[-1] == (1, 256, 6, 6)
+
+
+def test_maxpool_dims_and_errors():
+    assert mg3m.maxpool2d_out_dims(224, 224, 2, 2, 2, 2, 0, 0) == (112, 112)
+    assert mg3m.maxpool2d_out_dims(112, 112, 3, 3, 2, 2, 1, 1) == (56, 56)
+    assert mg3m.maxpool2d_out_dims(55, 55, 3, 3, 2, 2, 0, 0) == (27, 27)
+    lib = mg3m.load_library()
+    assert lib.maxpool2d_f32(X, Y, 2, 4, 8, 8, 2, 2, 2, 2, 2, 0, 0, None) == 2        # pad > R/2
+    assert lib.maxpool2d_f32(X, Y, 2, 4, 8, 8, 2, 2, 0, 2, 0, 0, 0, None) == 2        # stride 0
+    assert lib.maxpool2d_f32(X, X + 8, 2, 4, 8, 8, 2, 2, 2, 2, 0, 0, 0, None) == 5    # y overlaps x
+    assert lib.maxpool2d_f32(None, Y, 2, 4, 8, 8, 2, 2, 2, 2, 0, 0, 0, None) == 1
+    assert lib.maxpool2d_f32(X, Y, 2, 4, 8, 8, 2, 2, 2, 2, 0, 0, 5, None) == 3
+
+
+def test_fused_conv_argument_errors():
+    lib = mg3m.load_library()
+    shape = (2, 8, 10, 10, 16, 3, 3, 1, 1, 1, 1, 0)
+    assert lib.conv2d_fwd_f32_fused(X, Wp, Y, None, 2, *shape, None, 0, None, None) == 10   # relu
+    assert lib.conv2d_fwd_f32_fused(X, Wp, Y, Y + 8, 1, *shape, None, 0, None, None) == 5   # add overlaps y
+    assert lib.conv2d_fwd_f32_fused(X, Wp, Y, Y + 2, 1, *shape, None, 0, None, None) == 9   # misaligned add
