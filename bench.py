@@ -49,9 +49,10 @@ def kernel_digest(name: str, launches) -> str:
 
 def kernel_name(plan) -> str:
     """The main kernel's symbol as rocprofv3 prints it (its template arguments:
-    layout, filter loader, patch loader, tile rows, columns, depth, waves)."""
+    layout, filter loader, patch loader, tile rows, columns, depth, waves, and
+    false for the plain output stage the benchmark uses)."""
     return (f"void mg3m::conv_igemm_f32<{plan['layout']}, {plan['a_mode']}, {plan['b_mode']}, "
-            f"{plan['mt']}, {plan['nt']}, {plan['kt']}, {plan['waves_m']}, {plan['waves_n']}>"
+            f"{plan['mt']}, {plan['nt']}, {plan['kt']}, {plan['waves_m']}, {plan['waves_n']}, false>"
             f"(mg3m::KArgs)")
 
 

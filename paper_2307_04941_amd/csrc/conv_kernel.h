@@ -767,7 +767,11 @@ __device__ __forceinline__ float finish1(const KArgs& a, float v, int idx) {
 }
 
 // ------------------------------------------------------------------ kernel
-template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
+// FUSE: the output stage applies y = act(conv + add) (KArgs::add, relu).  A
+// separate instantiation: the fused stage works on the accumulators in VGPRs,
+// and the compiler copies all of them out of the AGPRs at once, which in a
+// shared kernel would cost the plain convolution a wave per SIMD.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
 __global__ __launch_bounds__(WM * WN * 64)
 void conv_igemm_f32(KArgs a) {
   using C = Cfg<MT, NT, KT, WM, WN>;
@@ -847,7 +851,6 @@ void conv_igemm_f32(KArgs a) {
     return;
   }
   float* const out = a.y;
-  const bool fused = (a.add != nullptr) | (a.relu != 0);
 #pragma unroll
   for (int j = 0; j < C::TN; ++j) {
     const int n = n0 + wn * C::WTN + j * 32 + q;
@@ -862,7 +865,7 @@ void conv_igemm_f32(KArgs a) {
           // four consecutive output channels, contiguous when mstride == 1
           if (row0 < a.Mg) {
             f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-            if (fused) {
+            if constexpr (FUSE) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
             }
@@ -873,30 +876,31 @@ void conv_igemm_f32(KArgs a) {
           for (int e = 0; e < 4; ++e)
             if (row0 + e < a.Mg) {
               const int idx = colbase + (row0 + e) * a.mstride;
-              out[idx] = fused ? finish1(a, acc[i][j][4 * g + e], idx) : acc[i][j][4 * g + e];
+              if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][4 * g + e], idx);
+              else out[idx] = acc[i][j][4 * g + e];
             }
         }
       }
   }
 }
 
-template <int LAYOUT, int AM, int BM, int TI>
+template <int LAYOUT, int AM, int BM, bool FUSE, int TI>
 constexpr KernelFn kernel_at() {
   constexpr TileDesc d = kTiles[TI];
-  return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn>;
+  return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
 }
 
-template <int LAYOUT, int AM, int BM, int... TI>
+template <int LAYOUT, int AM, int BM, bool FUSE, int... TI>
 KernelFn pick_tile(int tile, std::integer_sequence<int, TI...>) {
   KernelFn fn = nullptr;
-  ((fn = (tile == TI ? kernel_at<LAYOUT, AM, BM, TI>() : fn)), ...);
+  ((fn = (tile == TI ? kernel_at<LAYOUT, AM, BM, FUSE, TI>() : fn)), ...);
   return fn;
 }
 
-template <int LAYOUT, int AM, int BM>
+template <int LAYOUT, int AM, int BM, bool FUSE = false>
 KernelFn kernel_for_tile(int tile) {
   if (tile < 0 || tile >= kNumTiles) return nullptr;
-  return pick_tile<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles>{});
+  return pick_tile<LAYOUT, AM, BM, FUSE>(tile, std::make_integer_sequence<int, kNumTiles>{});
 }
 
 // ------------------------------------------------- fp64-accumulating kernel

@@ -90,6 +90,19 @@ static KernelFn kernel_for(int variant, int tile) {
   }
 }
 
+static KernelFn kernel_fused_for(int variant, int tile) {
+  switch (variant) {
+    case kVarHwcnVecNTap: return conv_kernel_hwcn_vecn_tap_fused(tile);
+    case kVarHwcnVecN: return conv_kernel_hwcn_vecn_fused(tile);
+    case kVarHwcnVecC:
+    case kVarHwcnVecA:
+    case kVarHwcnScalar: return conv_kernel_hwcn_other_fused(variant, tile);
+    case kVarNchwVecA:
+    case kVarNchwScalar: return conv_kernel_nchw_fused(variant, tile);
+    default: return nullptr;
+  }
+}
+
 static KernelFn kernel64_for(int variant, int tile) {
   switch (variant) {
     case kVarHwcnVecNTap: return conv_kernel64_hwcn_vecn_tap(tile);
@@ -104,7 +117,13 @@ static KernelFn kernel64_for(int variant, int tile) {
 }
 
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
-  KernelFn fn = p.acc64 ? kernel64_for(p.variant, p.tile) : kernel_for(p.variant, p.tile);
+  const bool fused = (a.add != nullptr) | (a.relu != 0);
+  if (p.acc64 && fused) {
+    *err = "internal: the fp64-accumulating kernel has no fused output stage";
+    return MG3M_ERR_PLAN;
+  }
+  KernelFn fn = p.acc64 ? kernel64_for(p.variant, p.tile)
+                        : (fused ? kernel_fused_for(p.variant, p.tile) : kernel_for(p.variant, p.tile));
   if (fn == nullptr) {
     *err = "internal: no kernel for this loader variant and tile";
     return MG3M_ERR_PLAN;

@@ -216,6 +216,11 @@ KernelFn conv_kernel_hwcn_vecc(int tile);
 KernelFn conv_kernel_hwcn_veca(int tile);
 KernelFn conv_kernel_hwcn_scalar(int tile);
 KernelFn conv_kernel_nchw(int variant, int tile);
+// The same with the fused output stage: conv_*_fused.hip.
+KernelFn conv_kernel_hwcn_vecn_tap_fused(int tile);
+KernelFn conv_kernel_hwcn_vecn_fused(int tile);
+KernelFn conv_kernel_hwcn_other_fused(int variant, int tile);
+KernelFn conv_kernel_nchw_fused(int variant, int tile);
 // fp64-accumulating kernels by (variant, tile): conv_acc64_*.hip.
 KernelFn conv_kernel64_hwcn_vecn_tap(int tile);
 KernelFn conv_kernel64_hwcn(int variant, int tile);

@@ -78,8 +78,8 @@ def main(argv=None):
     with open(a.bench_log) as f:
         bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
     kernel = bench["roofline"]["kernel"]
-    tmpl = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").replace(",", "_")
-    tag = f"conv_igemm_{tmpl}"
+    args = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").split(",")
+    tag = "conv_igemm_" + "_".join(v for v in args if v.lstrip("-").isdigit())
     os.makedirs(a.out, exist_ok=True)
 
     # ---- kernel statistics
