@@ -8,7 +8,11 @@
 #include <cstdio>
 #include <cstring>
 #include <exception>
+#include <functional>
+#include <mutex>
 #include <string>
+#include <unordered_map>
+#include <utility>
 
 #include "mg3m.h"
 #include "mg3m_internal.h"
@@ -38,13 +42,57 @@ Geom geom(int N, int C, int H, int W, int K, int R, int S, int sh, int sw, int p
   return Geom{N, C, H, W, K, R, S, sh, sw, ph, pw, layout, acc64};
 }
 
+// Plans already made, by everything a plan depends on: the selector scores
+// about 170 candidates (several microseconds of host time), which for the
+// small layers of a network is as long as the kernel.  Bounded; cleared when
+// full.  Guarded by a mutex: calls may come from several host threads.
+struct PlanKey {
+  int v[14];
+  std::string override_text;
+  bool operator==(const PlanKey& o) const {
+    return std::memcmp(v, o.v, sizeof v) == 0 && override_text == o.override_text;
+  }
+};
+struct PlanKeyHash {
+  size_t operator()(const PlanKey& k) const {
+    size_t h = std::hash<std::string>()(k.override_text);
+    for (int x : k.v) h = h * 1000003u ^ std::hash<int>()(x);
+    return h;
+  }
+};
+struct PlanCache {
+  std::mutex mu;
+  std::unordered_map<PlanKey, std::pair<mg3m::ConvShape, mg3m::Plan>, PlanKeyHash> map;
+};
+PlanCache& plan_cache() {
+  static PlanCache* c = new PlanCache();   // never destroyed: usable from exit-time destructors
+  return *c;
+}
+constexpr size_t kPlanCacheMax = 4096;
+
 int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16,
                    mg3m::ConvShape* s, mg3m::Plan* p) {
+  PlanKey key{{g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout,
+               (g.acc64 ? 1 : 0), (x16 ? 4 : 0) | (w16 ? 2 : 0) | (y16 ? 1 : 0)},
+              plan ? std::string(plan) : std::string("\x01")};
+  PlanCache& cache = plan_cache();
+  {
+    std::lock_guard<std::mutex> lock(cache.mu);
+    auto it = cache.map.find(key);
+    if (it != cache.map.end()) {
+      *s = it->second.first;
+      *p = it->second.second;
+      return MG3M_OK;
+    }
+  }
   std::string err;
   int rc = mg3m::make_shape(g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout, s, &err);
   if (rc) return fail(rc, err);
   rc = mg3m::make_plan(*s, plan, g.acc64, x16, w16, y16, p, &err);
   if (rc) return fail(rc, err);
+  std::lock_guard<std::mutex> lock(cache.mu);
+  if (cache.map.size() >= kPlanCacheMax) cache.map.clear();
+  cache.map.emplace(std::move(key), std::make_pair(*s, *p));
   return MG3M_OK;
 }
 
