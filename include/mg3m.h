@@ -80,12 +80,17 @@ int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, in
  * chunks' partial sums go to a workspace that this call takes from HIP's
  * stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`) and a
  * second kernel sums them in chunk order, so results are deterministic run
- * to run. */
+ * to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
+ * a filter of more than one tap and stride_w 1 take the reduction tap-major: a
+ * first kernel copies the filter to [R][S][C][K] in that workspace. */
 int conv2d_fwd_f32(const float *x, const float *w, float *y,
                    int N, int C, int H, int W, int K, int R, int S,
                    int stride, int pad, int layout, void *stream);
 
-/* Bytes of workspace the plan for this shape needs (0 when no tile is split).
+/* Bytes of workspace the plan for this shape needs: the chunk partials when
+ * tiles are split, plus, for NCHW plans taken tap-major (C a multiple of the
+ * plan's kt, K a multiple of 4, R*S > 1, stride_w 1), a [R][S][C][K] copy of
+ * the filter that the call makes first; 0 when neither applies.
  * plan: NULL for the selector's choice, or an override string (below).
  * bytes: host out-parameter. */
 int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int S,

@@ -118,7 +118,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     return fail(MG3M_ERR_ALIAS, "add partly overlaps y");
 
   float* ws = nullptr;
-  if (p.tail_tiles > 0) {
+  if (p.ws_bytes > 0) {
     if (own_workspace) {
       hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), p.ws_bytes,
                                     static_cast<hipStream_t>(stream));
@@ -134,8 +134,11 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     }
   }
 
+  // workspace: [R][S][C][K] filter copy (tap-major NCHW plans), then the partials
+  float* const wt = p.wt_bytes > 0 ? ws : nullptr;
+  float* const part = ws != nullptr ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.wt_bytes) : nullptr;
   mg3m::KArgs a{};
-  a.x = x; a.w = w; a.y = y; a.ws = ws;
+  a.x = x; a.w = wt != nullptr ? wt : w; a.y = y; a.ws = part;
   a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb;
   a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
@@ -148,6 +151,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   a.relu = relu;
 
   std::string err;
+  if (wt != nullptr) rc = mg3m::launch_filter_to_rsck(w, wt, s.K, s.C, s.R, s.S, stream, &err);
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
   g_ev_start = g_ev_stop = nullptr;
   if (ev0 != nullptr) {
@@ -161,7 +165,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   }
   if (rc == MG3M_OK && p.tail_tiles > 0) {
     mg3m::RArgs r{};
-    r.ws = ws; r.y = y; r.mt = p.t.mt; r.nt = p.t.nt;
+    r.ws = part; r.y = y; r.mt = p.t.mt; r.nt = p.t.nt;
     r.tiles_m = p.tiles_m; r.dp_tiles = p.dp_tiles; r.tail_tiles = p.tail_tiles; r.split = p.split;
     r.layout = s.layout; r.N = s.N; r.K = s.K; r.HoWo = s.Ho * s.Wo;
     r.Mg = (int)s.Mg; r.Ng = (int)s.Ng;

@@ -9,6 +9,7 @@ KernelFn conv_kernel64_nchw(int variant, int tile) {
   switch (variant) {
     case kVarNchwVecA: return kernel64_for_tile<kNCHW, kAVecK, kBVecW>(tile);
     case kVarNchwScalar: return kernel64_for_tile<kNCHW, kAScalar, kBVecW>(tile);
+    case kVarNchwTap: return kernel64_for_tile<kNCHW, kAVecM, kBVecWTap>(tile);
     default: return nullptr;
   }
 }

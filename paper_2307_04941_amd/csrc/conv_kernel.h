@@ -460,6 +460,90 @@ struct BVecW {
   }
 };
 
+// NCHW with the reduction taken tap-major, k = (r*S + s)*C + c, and C % KT ==
+// 0: a KT-row slab is one filter tap (r, s) over KT consecutive channels, the
+// same for the whole work-group, and stages run the taps inside each channel
+// slab (as BVecNTap does for HWCN).  The filter is read from its [R][S][C][K]
+// copy by AVecMTap.  Columns as in BVecW; a thread's NV consecutive rows are
+// consecutive channels, H*W apart in x, so the image-bounds test, the border
+// mask and the choice between one 16-byte load per row and element loads are
+// made once per stage.
+template <class C, int NT, int KT>
+struct BVecWTap {
+  static constexpr int NC4 = NT / 4;
+  static constexpr int RG = C::T / NC4;
+  static constexpr int NV = KT / RG;
+  static_assert(C::T % NC4 == 0 && KT % RG == 0 && NV * 4 == C::B_ELEMS, "B vec-W split");
+  int n4, kr0;
+  int cb[4], ih0[4], iw0[4];
+  bool vrow;
+  int r, s, c0;                // uniform: tap and first channel of the slab
+  f32x4 v[NV], e4[NV];
+  bool fast;
+  unsigned keep;
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    n4 = t % NC4;
+    kr0 = (t / NC4) * NV;
+    const int n = n0 + n4 * 4, hw = a.Ho * a.Wo;
+    int wo_first = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int ne = n + e;
+      const int b = ne / hw, pix = ne - b * hw;
+      const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+      if (e == 0) wo_first = wo;
+      const bool live = ne < a.Ng;
+      ih0[e] = live ? ho * a.sh - a.ph : -(1 << 30);
+      iw0[e] = wo * a.sw - a.pw;
+      // x index of (b, channel kr0, ih0, iw0)
+      cb[e] = live ? ((b * a.C + kr0) * a.H + ih0[e]) * a.W + iw0[e] : 0;
+    }
+    vrow = (a.sw == 1) & (n + 3 < a.Ng) & (wo_first + 3 < a.Wo);
+    const int t0 = kbeg / KT, rs = a.R * a.S;
+    const int slab = t0 / rs, tap = t0 - slab * rs;
+    c0 = slab * KT;
+    r = tap / a.S;
+    s = tap - r * a.S;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) e4[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ void advance(const KArgs& a) {
+    if (++s == a.S) {
+      s = 0;
+      if (++r == a.R) { r = 0; c0 += KT; }
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr) {
+    const int hw = a.H * a.W;
+    const int rel = c0 * hw + r * a.W + s;
+    const int iw = iw0[0] + s, off = cb[0] + rel;
+    fast = vrow & ((unsigned)(ih0[0] + r) < (unsigned)a.H) & (off >= 0) &
+           (off + (NV - 1) * hw + 3 < (int)(a.x_bytes / 4u));
+    keep = ((unsigned)iw < (unsigned)a.W) | (((unsigned)(iw + 1) < (unsigned)a.W) << 1) |
+           (((unsigned)(iw + 2) < (unsigned)a.W) << 2) | (((unsigned)(iw + 3) < (unsigned)a.W) << 3);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = bload4(xr, fast ? (unsigned)(off + i * hw) * 4u : kOOB);
+    if (!fast) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = ((unsigned)(ih0[e] + r) < (unsigned)a.H) & ((unsigned)(iw0[e] + s) < (unsigned)a.W);
+#pragma unroll
+        for (int i = 0; i < NV; ++i) e4[i][e] = bload1(xr, ok ? (unsigned)(cb[e] + rel + i * hw) * 4u : kOOB);
+      }
+    }
+  }
+  __device__ void store(float* Bs) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = fast ? (((keep >> e) & 1u) ? v[i][e] : 0.f) : e4[i][e];
+      st4(Bs + (kr0 + i) * C::BS + C::LB::col(kr0 + i, n4 * 4), o);
+    }
+  }
+};
+
 // HWCN, N % 4 == 0: each thread owns one 4-wide batch vector of one output
 // pixel (a fixed column group) and NV rows of the KT x NT tile.
 template <class C, int NT, int KT>
@@ -612,6 +696,8 @@ template <class C, int MT, int KT, int BM>
 struct ASel<kHWCN, kAVecM, C, MT, KT, BM> { using type = AVecM<C, MT, KT>; };
 template <class C, int MT, int KT>
 struct ASel<kHWCN, kAVecM, C, MT, KT, kBVecNTap> { using type = AVecMTap<C, MT, KT>; };
+template <class C, int MT, int KT>
+struct ASel<kNCHW, kAVecM, C, MT, KT, kBVecWTap> { using type = AVecMTap<C, MT, KT>; };
 template <class C, int MT, int KT, int BM>
 struct ASel<kNCHW, kAVecK, C, MT, KT, BM> { using type = AVecK<C, MT, KT>; };
 template <int LAYOUT, class C, int MT, int KT, int BM>
@@ -627,6 +713,8 @@ template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecC, C, NT, KT> { using type = BVecC<C, NT, KT>; };
 template <class C, int NT, int KT>
 struct BSel<kNCHW, kBVecW, C, NT, KT> { using type = BVecW<C, NT, KT>; };
+template <class C, int NT, int KT>
+struct BSel<kNCHW, kBVecWTap, C, NT, KT> { using type = BVecWTap<C, NT, KT>; };
 template <int LAYOUT, class C, int NT, int KT>
 struct BSel<LAYOUT, kBScalar, C, NT, KT> { using type = BScalar<LAYOUT, C, NT, KT>; };
 

@@ -86,6 +86,7 @@ static KernelFn kernel_for(int variant, int tile) {
     case kVarHwcnScalar: return conv_kernel_hwcn_scalar(tile);
     case kVarNchwVecA:
     case kVarNchwScalar: return conv_kernel_nchw(variant, tile);
+    case kVarNchwTap: return conv_kernel_nchw_tap(tile);
     default: return nullptr;
   }
 }
@@ -99,6 +100,7 @@ static KernelFn kernel_fused_for(int variant, int tile) {
     case kVarHwcnScalar: return conv_kernel_hwcn_other_fused(variant, tile);
     case kVarNchwVecA:
     case kVarNchwScalar: return conv_kernel_nchw_fused(variant, tile);
+    case kVarNchwTap: return conv_kernel_nchw_tap_fused(tile);
     default: return nullptr;
   }
 }
@@ -111,7 +113,8 @@ static KernelFn kernel64_for(int variant, int tile) {
     case kVarHwcnVecA:
     case kVarHwcnScalar: return conv_kernel64_hwcn(variant, tile);
     case kVarNchwVecA:
-    case kVarNchwScalar: return conv_kernel64_nchw(variant, tile);
+    case kVarNchwScalar:
+    case kVarNchwTap: return conv_kernel64_nchw(variant, tile);
     default: return nullptr;
   }
 }
@@ -137,6 +140,38 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  return MG3M_OK;
+}
+
+// wt[((r*S + s)*C + c)*K + k] = w[((k*C + c)*R + r)*S + s]: one thread per
+// element of wt, so the writes are coalesced along K; the reads gather from a
+// filter that is small next to the convolution's traffic.
+__global__ __launch_bounds__(256) void filter_kcrs_to_rsck(const float* w, float* wt, int K, int C,
+                                                           int R, int S) {
+  const long long total = (long long)K * C * R * S;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int k = (int)(i % K);
+  const long long rsc = i / K;
+  const int c = (int)(rsc % C);
+  const int rs = (int)(rsc / C);
+  wt[i] = w[((long long)k * C + c) * (R * S) + rs];
+}
+
+int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
+                          std::string* err) {
+  const long long blocks = ((long long)K * C * R * S + 255) / 256;
+  if (blocks < 1 || blocks > 0x7fffffffLL) {
+    *err = "internal: filter copy out of range";
+    return MG3M_ERR_PLAN;
+  }
+  hipLaunchKernelGGL(filter_kcrs_to_rsck, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     w, wt, K, C, R, S);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("filter copy launch: ") + hipGetErrorString(e);
     return MG3M_ERR_HIP;
   }
   return MG3M_OK;

@@ -22,8 +22,11 @@ enum Layout : int { kHWCN = 0, kNCHW = 1 };
 //                      kBScalar single elements                 (HWCN, any)
 //                      kBVecW   16-byte vectors along W where four columns of one
 //                               output row allow it, else per-column elements (NCHW)
+//                      kBVecWTap the same with one filter tap per staged slab of
+//                               channels (NCHW, C % kt == 0; the filter is first
+//                               copied to [R][S][C][K] and read by kAVecM)
 enum AMode : int { kAVecM = 0, kAVecK = 1, kAScalar = 2 };
-enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3, kBVecW = 4 };
+enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3, kBVecW = 4, kBVecWTap = 5 };
 // The loader pairs that are instantiated.
 enum Variant : int {
   kVarHwcnVecN = 0,     // HWCN, A vec-M, B vec-N
@@ -33,7 +36,8 @@ enum Variant : int {
   kVarNchwVecA = 4,     // NCHW, A vec-K, B vec-W
   kVarNchwScalar = 5,   // NCHW, A scalar, B vec-W
   kVarHwcnVecNTap = 6,  // HWCN, A vec-M, B vec-N with one tap per slab (the tuned path)
-  kNumVariants = 7
+  kVarNchwTap = 7,      // NCHW, A vec-M on the [R][S][C][K] filter copy, B vec-W one tap per slab
+  kNumVariants = 8
 };
 // Epilogue store: single elements, or 16-byte vectors of four consecutive
 // output channels (HWCN with N == 1 and K % 4 == 0, where they are contiguous).
@@ -144,7 +148,8 @@ struct Plan {
   long long grid;           // dp_tiles + tail_tiles * split
   int a_mode, b_mode, e_mode;
   int variant;
-  size_t ws_bytes;          // tail_tiles * split * mt * nt partials (4 or 8 bytes each)
+  size_t ws_bytes;          // workspace: the filter copy (wt_bytes), then the partials
+  size_t wt_bytes;          // [R][S][C][K] copy of an NCHW filter (kVarNchwTap), 256-byte rounded; else 0
   int lds_bytes;
   double pad_eff;
   double est_us;
@@ -221,6 +226,8 @@ KernelFn conv_kernel_hwcn_vecn_tap_fused(int tile);
 KernelFn conv_kernel_hwcn_vecn_fused(int tile);
 KernelFn conv_kernel_hwcn_other_fused(int variant, int tile);
 KernelFn conv_kernel_nchw_fused(int variant, int tile);
+KernelFn conv_kernel_nchw_tap(int tile);            // conv_nchw_tap.hip
+KernelFn conv_kernel_nchw_tap_fused(int tile);      // conv_nchw_tap_fused.hip
 // fp64-accumulating kernels by (variant, tile): conv_acc64_*.hip.
 KernelFn conv_kernel64_hwcn_vecn_tap(int tile);
 KernelFn conv_kernel64_hwcn(int variant, int tile);
@@ -230,6 +237,9 @@ KernelFn conv_kernel64_nchw(int variant, int tile);
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
 int launch_tail_reduce(const RArgs& r, void* stream, std::string* err);
 int launch_maxpool(const PArgs& p, void* stream, std::string* err);
+// wt[R][S][C][K] = w[K][C][R][S] (conv_launch.hip).
+int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
+                          std::string* err);
 
 // Shared by the C entry points and the network executor (abi.cpp): validate,
 // plan and launch one convolution (y = act(conv + add)).  own_workspace: take

@@ -58,6 +58,7 @@ int resident_wgs(const TileDesc& t, bool acc64) {
 double variant_factor(int variant) {
   switch (variant) {
     case kVarHwcnVecNTap: return 1.0;
+    case kVarNchwTap: return 0.9;
     case kVarHwcnVecN: return 0.85;
     case kVarHwcnVecC: case kVarHwcnVecA: case kVarNchwVecA: return 0.7;
     default: return 0.5;
@@ -206,13 +207,14 @@ double predict_us(const ConvShape& s, const Plan& p) {
   const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase((long long)p.tail_tiles * p.split, p.kps);
   const double y_bytes = 4.0 * (double)s.Mg * (double)s.Ng;
   const double xw_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
-  const double part_bytes = (double)p.ws_bytes;
+  const double part_bytes = (double)(p.ws_bytes - p.wt_bytes);
   const double t_mem = (xw_bytes + y_bytes + part_bytes) / kStreamBytesPerS * 1e6;
   double est = std::max(t_comp, t_mem) + kLaunchUs;
   if (p.tail_tiles > 0) {
     const double tail_out = 4.0 * (double)p.tail_tiles * t.mt * t.nt;
     est += (part_bytes + tail_out) / kStreamBytesPerS * 1e6 + kLaunchUs;
   }
+  if (p.wt_bytes > 0) est += 2.0 * (double)p.wt_bytes / kStreamBytesPerS * 1e6 + kLaunchUs;
   return est;
 }
 
@@ -276,10 +278,23 @@ void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
       p->b_mode = kBScalar;
       p->variant = kVarHwcnScalar;
     }
+  } else if (s.C % p->t.kt == 0 && s.K % 4 == 0 && s.R * s.S > 1 && s.sw == 1) {
+    // tap-major on a [R][S][C][K] copy of the filter (in the workspace).  A 1x1
+    // filter has one tap (both orders coincide, the copy would be pure cost),
+    // and other strides never take the 16-byte runs along W.
+    p->a_mode = kAVecM;
+    p->b_mode = kBVecWTap;
+    p->variant = kVarNchwTap;
   } else {
     p->b_mode = kBVecW;
     if (s.Kg % 4 == 0 && w16) p->a_mode = kAVecK, p->variant = kVarNchwVecA;
     else p->a_mode = kAScalar, p->variant = kVarNchwScalar;
+  }
+  // The filter copy goes first in the workspace, the partials after it.
+  p->wt_bytes = 0;
+  if (p->variant == kVarNchwTap) {
+    p->wt_bytes = ((size_t)4 * (size_t)s.Mg * (size_t)s.Kg + 255) / 256 * 256;
+    p->ws_bytes += p->wt_bytes;
   }
   // Four consecutive output channels are contiguous only in HWCN with N == 1;
   // the split-K workspace is 256-byte aligned and has the output's layout.
@@ -347,7 +362,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
 
 std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* an[] = {"vec_m", "vec_k", "scalar"};
-  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap", "vec_w"};
+  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap", "vec_w", "vec_w_tap"};
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,

@@ -79,6 +79,15 @@ def test_alias():
     assert _call(*GOOD, x=X, y=X + 64) == 5
 
 
+def test_nchw_tap_major_plan_needs_the_filter_copy_workspace():
+    lib = mg3m.load_library()
+    shape = (4, 32, 10, 10, 64, 3, 3, 1, 1)
+    p = mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "split=1")
+    assert p["b_mode"] == 5 and p["a_mode"] == 0
+    assert mg3m.conv2d_fwd_f32_workspace_bytes(*shape, "NCHW", "split=1") == 4 * 64 * 288
+    assert lib.conv2d_fwd_f32_ex(X, Wp, Y, *shape, 1, None, 0, b"split=1", None) == 6
+
+
 def test_workspace_and_plan_errors():
     lib = mg3m.load_library()
     shape = (4, 64, 14, 14, 96, 3, 3, 1, 1)
@@ -124,7 +133,11 @@ def _check_plan(shape, layout, plan=None):
     else:
         assert p["split"] == 1 and p["k_tiles_per_split"] == kt
     assert p["grid"] == p["dp_tiles"] + p["tail_tiles"] * p["split"] <= 2**31 - 1
-    assert p["workspace_bytes"] == 4 * p["tail_tiles"] * p["split"] * p["mt"] * p["nt"]
+    # partials, plus the [R][S][C][K] filter copy of a tap-major NCHW plan (b_mode 5)
+    copy = -(-4 * Mg * Kg // 256) * 256 if p["b_mode"] == 5 else 0
+    assert p["b_mode"] != 5 or (layout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
+                                and (st if isinstance(st, int) else st[1]) == 1)
+    assert p["workspace_bytes"] == 4 * p["tail_tiles"] * p["split"] * p["mt"] * p["nt"] + copy
     assert 0 < p["lds_bytes"] <= 160 * 1024
     assert 0 < p["pad_efficiency"] <= 1.0
     assert p["est_us"] > 0
@@ -247,7 +260,8 @@ def _acc64_plan(shape, layout, plan=None):
     assert dp + tail == tm * tn
     assert int(f["grid"]) == dp + tail * split
     assert (split >= 2) if tail else (split == 1)
-    assert int(f["ws"]) == 8 * tail * split * mt * nt
+    copy = -(-4 * Mg * Kg // 256) * 256 if f["b"] == "vec_w_tap" else 0
+    assert int(f["ws"]) == 8 * tail * split * mt * nt + copy
     assert f["e"] == "elem"
     assert 0 < int(f["lds"]) <= 160 * 1024
     return f

@@ -41,6 +41,7 @@ VARIANTS = [
     ((3, 5, 9, 9, 7, 3, 3, 1, 1), "HWCN", "scalar", "scalar"),
     ((2, 4, 9, 9, 16, 3, 3, 1, 1), "NCHW", "vec_k", "vec_w"),
     ((3, 5, 9, 9, 7, 3, 3, 1, 1), "NCHW", "scalar", "vec_w"),
+    ((2, 32, 9, 9, 16, 3, 3, 1, 1), "NCHW", "vec_m", "vec_w_tap"),
 ]
 
 

@@ -70,6 +70,23 @@ def test_every_tile_and_split(tile, mode):
 
 
 @pytest.mark.parametrize("tile", TILES)
+def test_every_tile_nchw_tap_major(tile):
+    """NCHW with C a multiple of kt: the filter is copied to [R][S][C][K] in
+    the workspace and every stage is one tap over a channel slab; the
+    partials of split plans sit after the copy.  Integer data: exact."""
+    shape = (3, 32, 10, 9, 40, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 81, "NCHW", dist="int")
+    acc, _ = oracle.conv2d(x, w, st, pd, "NCHW")
+    for split in (1, 3):
+        plan = f"tile={tile},split={split}"
+        info = mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", plan)
+        assert info["b_mode"] == 5, info
+        say(f"forced NCHW tap-major {plan}: workspace {info['workspace_bytes']}")
+        y = run_gpu(x, w, st, pd, "NCHW", plan=plan)
+        assert np.array_equal(y, acc.astype(np.float32)), plan
+
+
+@pytest.mark.parametrize("tile", TILES)
 def test_every_tile_nchw(tile):
     shape = (2, 6, 11, 9, 37, 3, 3, 1, 1)
     x, w, st, pd = make(shape, 78, "NCHW")
