@@ -38,8 +38,10 @@
  * at most 4 GiB - 64 bytes (the kernels use 32-bit byte offsets), y not
  * overlapping x or w, a known layout, a large enough workspace, a valid plan
  * override.  HIP launch failures return
- * MG3M_ERR_HIP with the HIP error text in mg3m_last_error().  No C++
- * exception crosses this interface.  Calls on different streams may run
+ * MG3M_ERR_HIP with the HIP error text in mg3m_last_error(); setting the
+ * environment variable MG3M_TEST_FAIL_LAUNCH=1 makes every convolution
+ * launch fail that way (nothing is launched), for testing callers' error
+ * paths.  No C++ exception crosses this interface.  Calls on different streams may run
  * concurrently from different host threads.
  */
 #ifndef MG3M_H

@@ -2,6 +2,7 @@
 // tile, and the deterministic split-K reduction.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
 #include <string>
 
 #include "mg3m.h"
@@ -119,7 +120,20 @@ static KernelFn kernel64_for(int variant, int tile) {
   }
 }
 
+// Test hook: MG3M_TEST_FAIL_LAUNCH=1 makes every convolution launch fail as a
+// rejected launch would (nothing is launched), so callers' error paths --
+// the status, the message, the release of a stream-ordered workspace -- can
+// be exercised without a faulty kernel.
+static bool launch_failure_injected() {
+  const char* v = std::getenv("MG3M_TEST_FAIL_LAUNCH");
+  return v != nullptr && v[0] == '1' && v[1] == 0;
+}
+
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
+  if (launch_failure_injected()) {
+    *err = "kernel launch: failure injected by MG3M_TEST_FAIL_LAUNCH";
+    return MG3M_ERR_HIP;
+  }
   const bool fused = (a.add != nullptr) | (a.relu != 0);
   if (p.acc64 && fused) {
     *err = "internal: the fp64-accumulating kernel has no fused output stage";

@@ -389,3 +389,14 @@ def test_fused_conv_argument_errors():
     assert lib.conv2d_fwd_f32_fused(X, Wp, Y, None, 2, *shape, None, 0, None, None) == 10   # relu
     assert lib.conv2d_fwd_f32_fused(X, Wp, Y, Y + 8, 1, *shape, None, 0, None, None) == 5   # add overlaps y
     assert lib.conv2d_fwd_f32_fused(X, Wp, Y, Y + 2, 1, *shape, None, 0, None, None) == 9   # misaligned add
+
+
+def test_injected_launch_failure(monkeypatch):
+    """MG3M_TEST_FAIL_LAUNCH=1: validation passes, the launch reports failure."""
+    lib = mg3m.load_library()
+    monkeypatch.setenv("MG3M_TEST_FAIL_LAUNCH", "1")
+    rc = lib.conv2d_fwd_f32_ex(X, Wp, Y, *GOOD, 0, None, 0, b"split=1", None)
+    assert rc == 8
+    assert "injected" in mg3m.mg3m_last_error()
+    monkeypatch.setenv("MG3M_TEST_FAIL_LAUNCH", "0")
+    assert lib.conv2d_fwd_f32_ex(X, Wp, Y, 0, *GOOD[1:], 0, None, 0, b"split=1", None) == 2

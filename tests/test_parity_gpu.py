@@ -8,7 +8,7 @@ import pytest
 import oracle
 import workloads
 from paper_2307_04941_amd import mg3m
-from tests.gpu_util import assert_parity, make, run_gpu, say
+from tests.gpu_util import assert_parity, make, run_gpu, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -250,6 +250,74 @@ def test_guard_bands_and_determinism():
     assert np.array_equal(outs[0], outs[1])
     acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
     assert_parity(outs[0].reshape(Ho, Wo, 96, 4), acc, mag, "guard")
+
+
+@pytest.mark.parametrize("layout,plan", [("HWCN", "split=4"), ("NCHW", "tile=128x128,split=3")])
+def test_workspace_guard_bands(layout, plan):
+    """A caller workspace is written only inside the bytes the plan asks for
+    (NCHW: the filter copy, then the partials)."""
+    import torch
+    shape = (4, 32, 14, 14, 96, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 83, layout)
+    N, C, H, W, K, R, S = mg3m.dims_of(x, w, layout)
+    need = mg3m.conv2d_fwd_f32_workspace_bytes(N, C, H, W, K, R, S, 1, 1, layout, plan)
+    assert need > 0
+    pad = 1024
+    buf = torch.full((need // 4 + 2 * pad,), float("nan"), device="cuda")
+    ws = buf[pad:pad + need // 4]
+    Ho, Wo = mg3m.conv2d_out_dims(H, W, R, S, 1, 1)
+    y = torch.empty((Ho, Wo, K, N) if layout == "HWCN" else (N, K, Ho, Wo), device="cuda")
+    mg3m.conv2d_fwd_f32_ex(to_dev(x), to_dev(w), y, N, C, H, W, K, R, S, 1, 1, layout, ws, need, plan)
+    torch.cuda.synchronize()
+    b = buf.cpu().numpy()
+    assert np.isnan(b[:pad]).all() and np.isnan(b[pad + need // 4:]).all(), "write outside the workspace"
+    acc, mag = oracle.conv2d(x, w, st, pd, layout)
+    assert_parity(y.cpu().numpy(), acc, mag, f"{layout} {plan}")
+
+
+def test_injected_launch_failure_leaves_y_untouched(monkeypatch):
+    import torch
+    shape = (4, 16, 12, 12, 32, 3, 3, 1, 1)
+    x, w, st, pd = make(shape, 84, "HWCN")
+    y = torch.full((12, 12, 32, 4), float("nan"), device="cuda")
+    monkeypatch.setenv("MG3M_TEST_FAIL_LAUNCH", "1")
+    for plan in (None, "split=3"):
+        with pytest.raises(mg3m.Mg3mError) as ei:
+            mg3m.conv2d_fwd(to_dev(x), to_dev(w), st, pd, "HWCN", plan=plan, out=y)
+        assert ei.value.status == 8
+    torch.cuda.synchronize()
+    assert torch.isnan(y).all().item()
+    monkeypatch.delenv("MG3M_TEST_FAIL_LAUNCH")
+    mg3m.conv2d_fwd(to_dev(x), to_dev(w), st, pd, "HWCN", out=y)        # the stream still works
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    assert_parity(y.cpu().numpy(), acc, mag, "after injected failure")
+
+
+def test_vgg_conv9_performance_floor():
+    """The hot path keeps at least 60% of the fp32 MFMA peak (94.4 TFLOPS) on
+    VGG-16 conv9 (N=64, 512 channels, 28x28), the configuration the
+    benchmark's dominant kernel serves."""
+    import time
+    import torch
+    L = workloads.workload("vgg16_n64")[8]
+    layer, x, w = workloads.layer_tensors("vgg16_n64", 8, "HWCN")
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    y = mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN")
+    t_end = time.perf_counter() + 0.2
+    while time.perf_counter() < t_end:
+        mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", out=y)
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", out=y)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / 10
+    Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
+    tflops = 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo / us / 1e6
+    say(f"VGG conv9: {us:.1f} us, {tflops:.1f} TFLOPS")
+    assert tflops >= 0.6 * 157.3
 
 
 def test_non_default_stream():
