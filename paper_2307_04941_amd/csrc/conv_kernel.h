@@ -1,6 +1,9 @@
-// Implicit-GEMM forward convolution on fp32 MFMA for gfx950 (MI355X): the
-// device template.  Included by the instantiation files (conv_hwcn_*.hip,
-// conv_nchw.hip); not part of the public interface.
+// Implicit-GEMM forward convolution for gfx950 (MI355X): the device templates
+// -- conv_igemm_f32 on fp32 MFMA (plain, or with the fused output stage
+// y = act(conv + add)) and conv_igemm_acc64 on fp64 MFMA (the paper's fp64
+// arithmetic on fp32 data).  Included by the instantiation files
+// (conv_hwcn_*.hip, conv_nchw*.hip, conv_acc64_*.hip); not part of the
+// public interface.
 //
 // The convolution of Eq. 1 (Sec. 2.1) is computed as the matrix product of
 // Eq. 2 / Alg. 1 (Sec. 4.1.1), without materialising the patch matrix:
@@ -14,7 +17,8 @@
 // Kg x OC matrix A^T (each FLT_mtx of Alg. 1 is one IC x OC slab of it, k
 // ordered (fh, fw, ic)), and column n of B at row k is one element of the
 // IN_mtx at pixel (ih, iw), so a k-slab of B is a gather of contiguous IN_mtx
-// rows.  In NCHW the reduction runs in (ic, fh, fw) order.
+// rows.  In NCHW the reduction runs in (ic, fh, fw) order, or tap-major like
+// HWCN on a [R][S][C][K] copy of the filter when C is a multiple of kt.
 //
 // How the paper's design maps onto CDNA4:
 //  * Multi-grained mapping (Sec. 4.1.2): the work-group tile (mt x nt) and the
@@ -25,7 +29,9 @@
 //    staged A and B tiles through LDS instead of register broadcasts.
 //  * Filter reuse (Alg. 2): one staged A tile serves all nt columns.
 //  * Double buffering (Alg. 3): two LDS stages; the next tile's global loads
-//    are in flight while the MFMAs consume the current stage.
+//    are in flight while the MFMAs consume the current stage.  Staged rows
+//    are XOR-swizzled rather than padded, so each lane reads its fragments
+//    without bank conflicts from one base address.
 //  * Register blocking (Sec. 4.4.1, Eq. 9): each wave holds a (mt/wm) x
 //    (nt/wn) accumulator block as 32x32 MFMA blocks in AccVGPRs; each lane
 //    reads one A and one B value from LDS per 4096-flop MFMA.
