@@ -14,8 +14,15 @@ the ratio of the copy's known size to what the same counter read for the copy.
 
 Writes <out>/<kernel tag>_<workload>_kernel_stats.txt,
 <out>/<kernel tag>_<workload>_traffic.txt and <out>/traffic_<workload>.json
-(the figure bench.py reports as roofline.traffic while the library sources
-are unchanged).
+(the figure bench.py reports as roofline.traffic while the dominant kernel's
+code and launches are unchanged).
+
+    python -m paper_2307_04941_amd.rocprof_summary --stats-only NAME --trace DIR \
+        --out DIR --command-trace "..."
+
+writes <out>/NAME_kernel_stats.txt only: the kernel-time table of any traced
+program (e.g. a network forward through the executor), with the time grouped
+by kernel family.
 """
 from __future__ import annotations
 
@@ -61,19 +68,64 @@ def copy_scale(rows, known_kib: float):
     return known_kib / v, v
 
 
+FAMILIES = [("conv_igemm_f32<", ", false>", "convolution (fp32, plain output)"),
+            ("conv_igemm_f32<", ", true>", "convolution (fp32, fused add/ReLU)"),
+            ("conv_igemm_acc64<", "", "convolution (fp64 accumulation)"),
+            ("maxpool", "", "max pooling"),
+            ("tail_reduce", "", "split-K reduction"),
+            ("filter_kcrs_to_rsck", "", "NCHW filter copy")]
+
+
+def family(name: str) -> str:
+    for head, tail, label in FAMILIES:
+        if head in name and tail in name:
+            return label
+    return "other"
+
+
+def stats_only(a):
+    stats = _csv(a.trace, "kernel_stats.csv")
+    total = sum(float(r["TotalDurationNs"]) for r in stats)
+    lines = [f"rocprofv3 kernel statistics: {a.stats_only}", f"command: {a.command_trace}", "",
+             "time by kernel family:"]
+    fam = {}
+    for r in stats:
+        f = family(r["Name"])
+        calls, ns = fam.get(f, (0, 0.0))
+        fam[f] = (calls + int(r["Calls"]), ns + float(r["TotalDurationNs"]))
+    for f, (calls, ns) in sorted(fam.items(), key=lambda kv: -kv[1][1]):
+        lines.append(f"  {f:36s} {calls:7d} calls {ns / 1e6:10.3f} ms {100 * ns / total:6.2f}%")
+    lines += ["", " calls     avg_us   total_ms    pct  kernel"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append(f"{int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.2f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:10.3f} {float(r['Percentage']):6.2f}  {r['Name']}")
+    os.makedirs(a.out, exist_ok=True)
+    path = os.path.join(a.out, f"{a.stats_only}_kernel_stats.txt")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[:12]))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
-    ap.add_argument("--workload", required=True)
+    ap.add_argument("--stats-only", default=None, metavar="NAME")
+    ap.add_argument("--workload")
     ap.add_argument("--trace", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
-    ap.add_argument("--bench-log", required=True)
-    ap.add_argument("--copy-mib", type=float, required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--bench-log")
+    ap.add_argument("--copy-mib", type=float)
     ap.add_argument("--out", required=True)
     ap.add_argument("--command-trace", default="")
     ap.add_argument("--command-fetch", default="")
     ap.add_argument("--command-write", default="")
     a = ap.parse_args(argv)
+    if a.stats_only:
+        return stats_only(a)
+    for need in ("workload", "fetch", "write", "bench_log", "copy_mib"):
+        if getattr(a, need) is None:
+            ap.error(f"--{need.replace('_', '-')} is required without --stats-only")
 
     with open(a.bench_log) as f:
         bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
