@@ -77,20 +77,21 @@ enum mg3m_status {
 int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, int *Wo);
 
 /* y = conv(x, w) in `layout`.  Plan chosen by the per-shape selector.  When
- * the plan splits the Kg reduction of some output tiles into chunks (all
- * tiles, or only those left over after whole rounds of work-groups), the
- * chunks' partial sums go to a workspace that this call takes from HIP's
- * stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`) and a
- * second kernel sums them in chunk order, so results are deterministic run
- * to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
+ * the plan shares the Kg reduction of some output tiles out among several
+ * work-groups (all tiles, or only those left over after whole rounds of
+ * work-groups; each work-group takes an equal run of their k-tiles, stream-K
+ * fashion), the pieces' partial sums go to a workspace that this call takes
+ * from HIP's stream-ordered allocator (hipMallocAsync / hipFreeAsync on
+ * `stream`) and a second kernel sums them in a fixed order, so results are
+ * deterministic run to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
  * a filter of more than one tap and stride_w 1 take the reduction tap-major: a
  * first kernel copies the filter to [R][S][C][K] in that workspace. */
 int conv2d_fwd_f32(const float *x, const float *w, float *y,
                    int N, int C, int H, int W, int K, int R, int S,
                    int stride, int pad, int layout, void *stream);
 
-/* Bytes of workspace the plan for this shape needs: the chunk partials when
- * tiles are split, plus, for NCHW plans taken tap-major (C a multiple of the
+/* Bytes of workspace the plan for this shape needs: the piece partials when
+ * tiles' reductions are shared out, plus, for NCHW plans taken tap-major (C a multiple of the
  * plan's kt, K a multiple of 4, R*S > 1, stride_w 1), a [R][S][C][K] copy of
  * the filter that the call makes first; 0 when neither applies.
  * plan: NULL for the selector's choice, or an override string (below).
@@ -105,10 +106,17 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  * override.  Override syntax: comma-separated key=value pairs,
  *   tile=<MT>x<NT>   one of the kernel tile shapes (e.g. 128x128, 64x256)
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
- *   split=<n>        split every tile's reduction into n chunks (1..64, clamped so
- *                    no chunk is empty; 1 = no split)
- *   tail=<n>         split only the tiles left over after whole rounds of resident
- *                    work-groups, into n chunks (2..64); the other tiles run whole
+ *   split=<n>        share every tile's reduction out over n work-groups per tile
+ *                    (1..64, clamped to the tile's k-tiles; 1 = no split)
+ *   tail=<n>         the same for the tiles left over after whole rounds of resident
+ *                    work-groups only (2..64); the other tiles run whole
+ *   sk=<g>           the left-over tiles' k-tiles dealt out to g work-groups in equal
+ *                    runs (stream-K); g from the number of left-over tiles to their
+ *                    k-tiles in total, else MG3M_ERR_PLAN.  Runs that span two tiles
+ *                    need the one-tap HWCN loader (HWCN, N and K multiples of 4, C a
+ *                    multiple of kt, aligned buffers) of this fp32 call; other
+ *                    shapes accept only g that cuts every left-over tile into equal
+ *                    runs (a split), else MG3M_ERR_PLAN
  * e.g. "tile=128x128,kt=32,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
 int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
                       int N, int C, int H, int W, int K, int R, int S,
@@ -143,14 +151,14 @@ int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, 
  * double and computes in double).  Each output is therefore within one fp32
  * rounding of its fp64 sum.  On fp64 MFMA (half the fp32 peak).  Separate
  * vertical and horizontal stride and padding as in conv2d_fwd_f32_hw.  When
- * the plan splits the reduction of some tiles, their chunks' fp64 partial
+ * the plan shares out the reduction of some tiles, their pieces' fp64 partial
  * sums go to a workspace taken from HIP's stream-ordered allocator
  * (hipMallocAsync / hipFreeAsync on `stream`) and a second kernel adds them
- * in chunk order in fp64 before the one rounding, so results are
+ * in a fixed order in fp64 before the one rounding, so results are
  * deterministic run to run.  plan: NULL, or an override with the keys of
  * conv2d_fwd_f32_ex: tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
- * 64x128, 128x64, 64x64, 32x64, 64x32), split=<n>, tail=<n>; kt other than
- * 16 -> MG3M_ERR_PLAN.  Pointers, ownership, validation and errors as for
+ * 64x128, 128x64, 64x64, 32x64, 64x32), split=<n>, tail=<n>, sk=<g> (a split
+ * only); kt other than 16 -> MG3M_ERR_PLAN.  Pointers, ownership, validation and errors as for
  * conv2d_fwd_f32. */
 int conv2d_fwd_f32_acc64(const float *x, const float *w, float *y,
                          int N, int C, int H, int W, int K, int R, int S,
@@ -264,11 +272,12 @@ int conv2d_fwd_f32_plan_string(int N, int C, int H, int W, int K, int R, int S,
 typedef struct mg3m_plan_info {
     int mt, nt, kt;           /* work-group tile: rows (OC), columns (B*outH*outW), depth step */
     int waves_m, waves_n;     /* waves per work-group along rows / columns */
-    int split;                /* reduction chunks per split tile (1 = none) */
+    int split;                /* tail work-groups per tail tile, rounded up (1 = no tail) */
     int k_tiles;              /* ceil(Kg / kt) */
-    int k_tiles_per_split;    /* k-tiles per chunk */
-    int dp_tiles;             /* tiles computed whole */
-    int tail_tiles;           /* tiles split into `split` chunks */
+    int k_tiles_per_wg;       /* most k-tiles one work-group computes */
+    int dp_tiles;             /* tiles computed whole, one per work-group */
+    int tail_tiles;           /* tiles whose reduction is shared out (their partials are summed) */
+    int tail_wgs;             /* work-groups sharing the tail tiles' k-tiles in equal runs */
     int tiles_m, tiles_n;     /* ceil(Mg / mt), ceil(Ng / nt) */
     long long grid;           /* work-groups launched by the main kernel */
     long long Mg, Ng, Kg;     /* implicit-GEMM sizes */

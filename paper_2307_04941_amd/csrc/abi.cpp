@@ -144,7 +144,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
   a.Mg = (int)s.Mg; a.Ng = (int)s.Ng; a.Kg = (int)s.Kg;
   a.tiles_m = p.tiles_m; a.k_tiles = p.k_tiles;
-  a.dp_tiles = p.dp_tiles; a.tail_tiles = p.tail_tiles > 0 ? p.tail_tiles : 1; a.kps = p.kps;
+  a.dp_tiles = p.dp_tiles; a.tail_tiles = p.tail_tiles; a.sk_q = p.sk_q; a.sk_r = p.sk_r; a.sk_s = p.sk_s;
   a.e_mode = p.e_mode;
   a.mstride = s.layout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
   a.add = add;
@@ -166,7 +166,8 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   if (rc == MG3M_OK && p.tail_tiles > 0) {
     mg3m::RArgs r{};
     r.ws = part; r.y = y; r.mt = p.t.mt; r.nt = p.t.nt;
-    r.tiles_m = p.tiles_m; r.dp_tiles = p.dp_tiles; r.tail_tiles = p.tail_tiles; r.split = p.split;
+    r.tiles_m = p.tiles_m; r.dp_tiles = p.dp_tiles; r.tail_tiles = p.tail_tiles;
+    r.k_tiles = p.k_tiles; r.sk_q = p.sk_q; r.sk_r = p.sk_r; r.sk_s = p.sk_s;
     r.layout = s.layout; r.N = s.N; r.K = s.K; r.HoWo = s.Ho * s.Wo;
     r.Mg = (int)s.Mg; r.Ng = (int)s.Ng;
     const bool contiguous4 = s.layout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
@@ -421,8 +422,9 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     if (rc) return rc;
     info->mt = p.t.mt; info->nt = p.t.nt; info->kt = p.t.kt;
     info->waves_m = p.t.wm; info->waves_n = p.t.wn;
-    info->split = p.split; info->k_tiles = p.k_tiles; info->k_tiles_per_split = p.kps;
-    info->dp_tiles = p.dp_tiles; info->tail_tiles = p.tail_tiles;
+    info->split = p.split; info->k_tiles = p.k_tiles;
+    info->k_tiles_per_wg = p.tail_wgs > 0 ? p.sk_q + (p.sk_r > 0 ? 1 : 0) : p.k_tiles;
+    info->dp_tiles = p.dp_tiles; info->tail_tiles = p.tail_tiles; info->tail_wgs = p.tail_wgs;
     info->tiles_m = p.tiles_m; info->tiles_n = p.tiles_n; info->grid = p.grid;
     info->Mg = s.Mg; info->Ng = s.Ng; info->Kg = s.Kg;
     info->workspace_bytes = p.ws_bytes; info->lds_bytes = p.lds_bytes;

@@ -69,6 +69,11 @@ __device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, unsigned off) 
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 __device__ __forceinline__ void st4(float* p, f32x4 v) { *reinterpret_cast<f32x4*>(p) = v; }
+// Buffer store at byte offset voff + soff: one per-lane offset register
+// serves a whole tile of stores, the constant part riding in soff.
+__device__ __forceinline__ void bstore1(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, voff, soff, 0);
+}
 
 // Placement of one staged operand tile (rows of DIM floats) in LDS: the row
 // stride, and the column swizzle that keeps the rows one fragment read
@@ -842,6 +847,62 @@ __device__ __forceinline__ int xcd_group(int L, int G) {
   return (xcd < r8) ? xcd * (q8 + 1) + loc : r8 * (q8 + 1) + (xcd - r8) * q8 + loc;
 }
 
+// Tail work.  The reduction steps of the tail tiles (tail_tiles * k_tiles
+// of them, tile by tile) are dealt out to the tail work-groups as runs of
+// consecutive steps, in one of two ways:
+//  * split (sk_s > 0): each tail tile's k_tiles steps are cut into sk_s runs
+//    of sk_q steps, one more for the first sk_r of them; run w is piece
+//    w % sk_s of tail tile w / sk_s.  A run never leaves its tile.
+//  * stream-K (sk_s == 0): all the steps are cut into tail_wgs runs of sk_q
+//    steps, one more for the first sk_r; run w starts at w*sk_q + min(w,
+//    sk_r).  No run is longer than a tile, so a run holds the end of one tail
+//    tile and the start of the next at most.
+struct TailRun {
+  int it, end;   // current step and end of the run (steps counted from the first tail tile)
+};
+
+// Run taken by the tail work-group launched w-th.  Split: consecutive
+// work-groups take the same piece of consecutive tiles, so they work on the
+// same k-slab at the same time and neighbouring tiles share input rows and
+// filter columns in L2.  Stream-K: launch order.
+__device__ __forceinline__ int tail_wg(const KArgs& a, int w) {
+  return a.sk_s > 0 ? (w % a.tail_tiles) * a.sk_s + w / a.tail_tiles : w;
+}
+
+__device__ __forceinline__ TailRun tail_run(const KArgs& a, int w) {
+  if (a.sk_s > 0) {
+    const int t = w / a.sk_s, j = w - t * a.sk_s;
+    const int it = t * a.k_tiles + j * a.sk_q + min(j, a.sk_r);
+    return TailRun{it, it + a.sk_q + (j < a.sk_r ? 1 : 0)};
+  }
+  const int it = w * a.sk_q + min(w, a.sk_r);
+  return TailRun{it, it + a.sk_q + (w < a.sk_r ? 1 : 0)};
+}
+
+// The piece of a run in one tail tile: tile index relative to the first
+// tail tile, its first k-tile and its length.
+__device__ __forceinline__ void tail_piece(const KArgs& a, const TailRun& r, int* rel, int* kt0, int* nk) {
+  *rel = r.it / a.k_tiles;
+  *kt0 = r.it - *rel * a.k_tiles;
+  *nk = min(r.end - r.it, a.k_tiles - *kt0);
+}
+
+// Split plans only: the run of the tail work-group launched L-th is piece j
+// = L / tail_tiles of tail tile rel = L % tail_tiles (tail_wg), run number
+// w = rel * sk_s + j; the same as tail_run and tail_piece, computed directly.
+__device__ __forceinline__ void split_piece(const KArgs& a, int L, int* w, int* rel, int* kt0, int* nk) {
+  const int j = L / a.tail_tiles;
+  *rel = L - j * a.tail_tiles;
+  *w = *rel * a.sk_s + j;
+  *kt0 = j * a.sk_q + min(j, a.sk_r);
+  *nk = a.sk_q + (j < a.sk_r ? 1 : 0);
+}
+
+// Partial slot of the piece of run w in tail tile rel.  Along the order of
+// the steps both w and rel never decrease and one of them grows from piece to
+// piece, so w + rel is unique; the slots run to tail_wgs + tail_tiles - 2.
+__device__ __forceinline__ long long tail_slot(int w, int rel) { return (long long)w + rel; }
+
 // Output element (m, n) sits at out_colbase(n) + m * mstride in either layout.
 template <int LAYOUT>
 __device__ __forceinline__ int out_colbase(const KArgs& a, int n) {
@@ -860,40 +921,15 @@ __device__ __forceinline__ float finish1(const KArgs& a, float v, int idx) {
   return (a.relu != 0 && v < 0.f) ? 0.f : v;
 }
 
-// ------------------------------------------------------------------ kernel
-// FUSE: the output stage applies y = act(conv + add) (KArgs::add, relu).  A
-// separate instantiation: the fused stage works on the accumulators in VGPRs,
-// and the compiler copies all of them out of the AGPRs at once, which in a
-// shared kernel would cost the plain convolution a wave per SIMD.
-template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
-__global__ __launch_bounds__(WM * WN * 64)
-void conv_igemm_f32(KArgs a) {
+// ----------------------------------------------------------------- kernels
+// One tile's product over the k-tiles [kt0, kt0 + nk): stage the operands
+// through LDS, run the MFMAs, and hand the accumulators to store(acc, m0, n0,
+// wm, wn, hh, q) with the tile's origin and the lane's place in it.  Every
+// per-lane value is derived here from the thread index t.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, class Store>
+__device__ __forceinline__ void tile_product_f32(const KArgs& a, float* lds, int t, int tile, int kt0,
+                                                 int nk, Store&& store) {
   using C = Cfg<MT, NT, KT, WM, WN>;
-  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
-
-  const int t = threadIdx.x;
-
-  // Work-group -> (tile, range of k-tiles).  Work-groups [0, dp_tiles) each
-  // compute one whole tile; the rest compute one chunk of kps k-tiles of a
-  // tail tile, consecutive work-groups taking different tiles of the same
-  // chunk.
-  // The whole tiles are regrouped per XCD; the tail chunks keep their place
-  // at the end of the dispatch order (dp_tiles is a multiple of 8 whenever
-  // there is a tail).
-  const int L = xcd_group(blockIdx.x, a.dp_tiles);
-  int tile, kt0, nk, chunk = 0;
-  const bool partial = L >= a.dp_tiles;
-  if (!partial) {
-    tile = L;
-    kt0 = 0;
-    nk = a.k_tiles;
-  } else {
-    const int j = L - a.dp_tiles;
-    chunk = j / a.tail_tiles;
-    tile = a.dp_tiles + (j - chunk * a.tail_tiles);
-    kt0 = chunk * a.kps;
-    nk = min(a.kps, a.k_tiles - kt0);
-  }
   const int tm = tile % a.tiles_m;
   const int tn = tile / a.tiles_m;
   const int m0 = tm * MT, n0 = tn * NT;
@@ -925,57 +961,126 @@ void conv_igemm_f32(KArgs a) {
   run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
     mma_stage<C, KT>(acc, As, Bs, wm, wn, hh, q);
   });
+  store(acc, m0, n0, wm, wn, hh, q);
+}
 
-  // Epilogue, straight from the accumulators.  32x32 accumulator layout:
-  // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
-  if (partial) {
-    // tile-local partial sums, row-major mt x nt, chunk-major over the tail
-    float* const part = a.ws + ((long long)chunk * a.tail_tiles + (tile - a.dp_tiles)) * (MT * NT);
+// Tail work-groups: the one launched `launched`-th computes its run and
+// stores each piece's tile-local partial sums (row-major mt x nt) in the
+// piece's slot; the tail reduction adds them up and applies any fused output
+// stage.  MULTI (one-tap HWCN loader, tail_runs_multi): stream-K runs, one
+// piece per tail tile the run touches (two at most), taken in a loop whose
+// thread index is made opaque per piece (hoisted out of the loop, the
+// loaders' and stores' per-lane offsets would stay live across the main loop
+// and cost occupancy).  Otherwise: split plans, one piece per run.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool MULTI>
+__device__ __forceinline__ void tail_runs_f32(const KArgs& a, float* lds, int launched) {
+  using C = Cfg<MT, NT, KT, WM, WN>;
+  if constexpr (!MULTI) {
+    int w, rel, kt0, nk;
+    split_piece(a, launched, &w, &rel, &kt0, &nk);
+    float* const part = a.ws + tail_slot(w, rel) * (MT * NT);
+    tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+        a, lds, threadIdx.x, a.dp_tiles + rel, kt0, nk,
+        [&](floatx16 (&acc)[C::TM][C::TN], int, int, int wm, int wn, int hh, int q) {
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j) {
-      const int col = wn * C::WTN + j * 32 + q;
+          for (int j = 0; j < C::TN; ++j) {
+            const int col = wn * C::WTN + j * 32 + q;
 #pragma unroll
-      for (int i = 0; i < C::TM; ++i)
+            for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = wm * C::WTM + i * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          part[row * NT + col] = acc[i][j][e];
-        }
+              for (int e = 0; e < 16; ++e)
+                part[(wm * C::WTM + i * 32 + 8 * (e >> 2) + 4 * hh + (e & 3)) * NT + col] = acc[i][j][e];
+          }
+        });
+  } else {
+    const int w = tail_wg(a, launched);
+    TailRun run = tail_run(a, w);
+    for (;;) {
+      int rel, kt0, nk;
+      tail_piece(a, run, &rel, &kt0, &nk);
+      int t = threadIdx.x;
+      asm volatile("" : "+v"(t));
+      // buffer stores: one per-lane offset register serves all of the piece's
+      // stores (with plain stores the loop keeps a 64-bit address per store)
+      const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.ws + tail_slot(w, rel) * (MT * NT), MT * NT * 4);
+      tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+          a, lds, t, a.dp_tiles + rel, kt0, nk,
+          [&](floatx16 (&acc)[C::TM][C::TN], int, int, int wm, int wn, int hh, int q) {
+            const unsigned lane_b = 4u * ((wm * C::WTM + 4 * hh) * NT + wn * C::WTN + q);
+#pragma unroll
+            for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+              for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                  bstore1(pr, lane_b, 4u * ((i * 32 + 8 * (e >> 2) + (e & 3)) * NT + j * 32), acc[i][j][e]);
+          });
+      run.it += nk;
+      if (run.it >= run.end) return;
+      __syncthreads();   // the next piece restages the LDS buffers
     }
+  }
+}
+
+// Work-groups [0, dp_tiles) compute whole tiles (tile xcd_group(i)) over
+// the full reduction and store them to y; the work-groups after them run the
+// tail (tail_runs_f32) in the same launch, starting as the last round of
+// whole tiles drains.  Stream-K runs (a loop over pieces) only with the
+// one-tap HWCN loader (tail_runs_multi): for the other loaders the loop would
+// cost the whole tiles registers and occupancy.  FUSE: the output stage
+// applies y = act(conv + add) (KArgs::add, relu).  A separate instantiation:
+// the fused stage works on the accumulators in VGPRs, and the compiler copies
+// all of them out of the AGPRs at once, which in a shared kernel would cost
+// the plain convolution a wave per SIMD.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_f32(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  if ((int)blockIdx.x >= a.dp_tiles) {
+    tail_runs_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN, tail_runs_multi(BM)>(a, lds, blockIdx.x - a.dp_tiles);
     return;
   }
-  float* const out = a.y;
+  const int tile = xcd_group(blockIdx.x, a.dp_tiles);
+  tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+      a, lds, threadIdx.x, tile, 0, a.k_tiles,
+      [&](floatx16 (&acc)[C::TM][C::TN], int m0, int n0, int wm, int wn, int hh, int q) {
+        // Epilogue, straight from the accumulators.  32x32 accumulator layout:
+        // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
+        float* const out = a.y;
 #pragma unroll
-  for (int j = 0; j < C::TN; ++j) {
-    const int n = n0 + wn * C::WTN + j * 32 + q;
-    if (n >= a.Ng) continue;
-    const int colbase = out_colbase<LAYOUT>(a, n);
+        for (int j = 0; j < C::TN; ++j) {
+          const int n = n0 + wn * C::WTN + j * 32 + q;
+          if (n >= a.Ng) continue;
+          const int colbase = out_colbase<LAYOUT>(a, n);
 #pragma unroll
-    for (int i = 0; i < C::TM; ++i)
+          for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
-        if (a.e_mode == kEVecM) {
-          // four consecutive output channels, contiguous when mstride == 1
-          if (row0 < a.Mg) {
-            f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-            if constexpr (FUSE) {
+            for (int g = 0; g < 4; ++g) {
+              const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
+              if (a.e_mode == kEVecM) {
+                // four consecutive output channels, contiguous when mstride == 1
+                if (row0 < a.Mg) {
+                  f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+                  if constexpr (FUSE) {
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
-            }
-            st4(out + colbase + row0, v);
-          }
-        } else {
+                    for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
+                  }
+                  st4(out + colbase + row0, v);
+                }
+              } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (row0 + e < a.Mg) {
-              const int idx = colbase + (row0 + e) * a.mstride;
-              if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][4 * g + e], idx);
-              else out[idx] = acc[i][j][4 * g + e];
+                for (int e = 0; e < 4; ++e)
+                  if (row0 + e < a.Mg) {
+                    const int idx = colbase + (row0 + e) * a.mstride;
+                    if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][4 * g + e], idx);
+                    else out[idx] = acc[i][j][4 * g + e];
+                  }
+              }
             }
         }
-      }
-  }
+      });
 }
 
 template <int LAYOUT, int AM, int BM, bool FUSE, int TI>
@@ -997,34 +1102,17 @@ KernelFn kernel_for_tile(int tile) {
   return pick_tile<LAYOUT, AM, BM, FUSE>(tile, std::make_integer_sequence<int, kNumTiles>{});
 }
 
-// ------------------------------------------------- fp64-accumulating kernel
-// Same operand staging and tile schedule as conv_igemm_f32 (fp32 tiles in
-// LDS; whole tiles, then chunks of the split tail tiles); the MFMAs take the
+// ------------------------------------------------- fp64-accumulating kernels
+// Same operand staging and tile schedule as the fp32 kernels (fp32 tiles in
+// LDS; whole tiles, then runs over the tail tiles); the MFMAs take the
 // operands widened to fp64 and accumulate in fp64.  A whole tile rounds each
-// output to fp32 once, at the store.  A chunk stores its fp64 partial sums,
+// output to fp32 once, at the store.  A piece stores its fp64 partial sums,
 // which the tail reduction adds in fp64 and then rounds once, so the sum
 // never leaves fp64 before that one rounding.
-template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
-__global__ __launch_bounds__(WM * WN * 64)
-void conv_igemm_acc64(KArgs a) {
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, class Store>
+__device__ __forceinline__ void tile_product_f64(const KArgs& a, float* lds, int t, int tile, int kt0,
+                                                 int nk, Store&& store) {
   using C = Cfg<MT, NT, KT, WM, WN, true>;
-  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
-
-  const int t = threadIdx.x;
-  const int L = xcd_group(blockIdx.x, a.dp_tiles);
-  int tile, kt0, nk, chunk = 0;
-  const bool partial = L >= a.dp_tiles;
-  if (!partial) {
-    tile = L;
-    kt0 = 0;
-    nk = a.k_tiles;
-  } else {
-    const int j = L - a.dp_tiles;
-    chunk = j / a.tail_tiles;
-    tile = a.dp_tiles + (j - chunk * a.tail_tiles);
-    kt0 = chunk * a.kps;
-    nk = min(a.kps, a.k_tiles - kt0);
-  }
   const int tm = tile % a.tiles_m;
   const int tn = tile / a.tiles_m;
   const int m0 = tm * MT, n0 = tn * NT;
@@ -1053,38 +1141,60 @@ void conv_igemm_acc64(KArgs a) {
   run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
     mma_stage64<C, KT>(acc, As, Bs, wm, wn, g, q);
   });
+  store(acc, m0, n0, wm, wn, g, q);
+}
 
-  // 16x16 fp64 accumulator layout: element e of lane (g, q) holds row
-  // g + 4*e, column q.  A lane's four rows are not adjacent, so the stores
-  // are single elements (lanes g = 0..3 together cover four adjacent rows).
-  if (partial) {
-    // tile-local fp64 partial sums, row-major mt x nt, chunk-major over the tail
-    double* const part = reinterpret_cast<double*>(a.ws) +
-                         ((long long)chunk * a.tail_tiles + (tile - a.dp_tiles)) * (MT * NT);
-#pragma unroll
-    for (int j = 0; j < C::TN16; ++j) {
-      const int col = wn * C::WTN + j * 16 + q;
-#pragma unroll
-      for (int i = 0; i < C::TM16; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) part[(wm * C::WTM + i * 16 + g + 4 * e) * NT + col] = acc[i][j][e];
-    }
-    return;
+// Work-groups [0, dp_tiles): whole tiles rounded to fp32 at the store; the
+// rest: one split piece each (tail plans of the fp64 kernel are always
+// split), stored as fp64 partials.  16x16 fp64 accumulator layout: element e
+// of lane (g, q) holds row g + 4*e, column q.  A lane's four rows are not
+// adjacent, so the stores are single elements (lanes g = 0..3 together cover
+// four adjacent rows).
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_acc64(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN, true>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  int tile, kt0 = 0, nk = a.k_tiles, w = 0, rel = 0;
+  const bool partial = (int)blockIdx.x >= a.dp_tiles;
+  if (!partial) {
+    tile = xcd_group(blockIdx.x, a.dp_tiles);
+  } else {
+    split_piece(a, blockIdx.x - a.dp_tiles, &w, &rel, &kt0, &nk);
+    tile = a.dp_tiles + rel;
   }
-  float* const out = a.y;
+  tile_product_f64<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+      a, lds, threadIdx.x, tile, kt0, nk,
+      [&](f64x4 (&acc)[C::TM16][C::TN16], int m0, int n0, int wm, int wn, int g, int q) {
+        if (partial) {
+          // tile-local fp64 partial sums, row-major mt x nt, in the piece's slot
+          double* const part = reinterpret_cast<double*>(a.ws) + tail_slot(w, rel) * (MT * NT);
 #pragma unroll
-  for (int j = 0; j < C::TN16; ++j) {
-    const int n = n0 + wn * C::WTN + j * 16 + q;
-    if (n >= a.Ng) continue;
-    const int colbase = out_colbase<LAYOUT>(a, n);
+          for (int j = 0; j < C::TN16; ++j) {
+            const int col = wn * C::WTN + j * 16 + q;
 #pragma unroll
-    for (int i = 0; i < C::TM16; ++i)
+            for (int i = 0; i < C::TM16; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = m0 + wm * C::WTM + i * 16 + g + 4 * e;
-        if (row < a.Mg) out[colbase + row * a.mstride] = (float)acc[i][j][e];
-      }
-  }
+              for (int e = 0; e < 4; ++e) part[(wm * C::WTM + i * 16 + g + 4 * e) * NT + col] = acc[i][j][e];
+          }
+          return;
+        }
+        float* const out = a.y;
+#pragma unroll
+        for (int j = 0; j < C::TN16; ++j) {
+          const int n = n0 + wn * C::WTN + j * 16 + q;
+          if (n >= a.Ng) continue;
+          const int colbase = out_colbase<LAYOUT>(a, n);
+#pragma unroll
+          for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int row = m0 + wm * C::WTM + i * 16 + g + 4 * e;
+              if (row < a.Mg) out[colbase + row * a.mstride] = (float)acc[i][j][e];
+            }
+        }
+      });
 }
 
 template <int LAYOUT, int AM, int BM, int TI>

@@ -13,12 +13,20 @@ namespace mg3m {
 typedef float f32x4r __attribute__((ext_vector_type(4)));
 typedef double f64x2r __attribute__((ext_vector_type(2)));
 
-// Tail reduction: for every element of every tail tile, y = sum of the
-// tile's chunk partials in chunk order 0, 1, ..., split-1, so the result does
-// not depend on scheduling.  F64: the partials are fp64 (from the
-// fp64-accumulating kernel), summed in fp64 and rounded to fp32 once.  One
-// thread per four consecutive columns of one tile row; rows and columns past
-// the output are skipped.
+// Stream-K plans: the run (see the kernel's tail_run) holding reduction
+// step x of the tail; the first sk_r runs are sk_q + 1 steps long, the rest
+// sk_q.
+__device__ __forceinline__ int run_of_step(const RArgs& r, int x) {
+  const int long_steps = r.sk_r * (r.sk_q + 1);
+  return x < long_steps ? x / (r.sk_q + 1) : r.sk_r + (x - long_steps) / r.sk_q;
+}
+
+// Tail reduction: for every element of every tail tile, y = the sum of the
+// tile's piece partials in run order (the runs covering the tile's steps,
+// first to last), so the result does not depend on scheduling.  F64: the
+// partials are fp64 (from the fp64-accumulating kernel), summed in fp64 and
+// rounded to fp32 once.  One thread per four consecutive columns of one tile
+// row; rows and columns past the output are skipped.
 template <bool F64>
 __global__ __launch_bounds__(256) void tail_reduce(RArgs r) {
   const long long tile_elems = (long long)r.mt * r.nt;
@@ -28,21 +36,28 @@ __global__ __launch_bounds__(256) void tail_reduce(RArgs r) {
   const int t = (int)(i / per_tile4);
   const int e = (int)(i - (long long)t * per_tile4) * 4;
   const int row = e / r.nt, col = e - row * r.nt;
-  const long long off = (long long)t * tile_elems + e;
-  const long long chunk_stride = (long long)r.tail_tiles * tile_elems;
+  // runs covering the tile: split plans give tile t the runs t*sk_s ... t*sk_s + sk_s - 1
+  const int w0 = r.sk_s > 0 ? t * r.sk_s : run_of_step(r, t * r.k_tiles);
+  const int w1 = r.sk_s > 0 ? w0 + r.sk_s - 1 : run_of_step(r, (t + 1) * r.k_tiles - 1);
+  // the piece of run w in tail tile t sits in slot w + t
+  const long long off = ((long long)w0 + t) * tile_elems + e;
   f32x4r sum;
   if constexpr (F64) {
     const double* p = static_cast<const double*>(r.ws) + off;
     f64x2r lo = *reinterpret_cast<const f64x2r*>(p), hi = *reinterpret_cast<const f64x2r*>(p + 2);
-    for (int c = 1; c < r.split; ++c) {
-      lo += *reinterpret_cast<const f64x2r*>(p + c * chunk_stride);
-      hi += *reinterpret_cast<const f64x2r*>(p + c * chunk_stride + 2);
+    for (int w = w0 + 1; w <= w1; ++w) {
+      p += tile_elems;
+      lo += *reinterpret_cast<const f64x2r*>(p);
+      hi += *reinterpret_cast<const f64x2r*>(p + 2);
     }
     sum = f32x4r{(float)lo[0], (float)lo[1], (float)hi[0], (float)hi[1]};
   } else {
     const float* p = static_cast<const float*>(r.ws) + off;
     sum = *reinterpret_cast<const f32x4r*>(p);
-    for (int c = 1; c < r.split; ++c) sum += *reinterpret_cast<const f32x4r*>(p + c * chunk_stride);
+    for (int w = w0 + 1; w <= w1; ++w) {
+      p += tile_elems;
+      sum += *reinterpret_cast<const f32x4r*>(p);
+    }
   }
   const int tile = r.dp_tiles + t;
   const int tm = tile % r.tiles_m, tn = tile / r.tiles_m;
@@ -129,6 +144,7 @@ static bool launch_failure_injected() {
   return v != nullptr && v[0] == '1' && v[1] == 0;
 }
 
+// One launch: dp_tiles work-groups of whole tiles, then tail_wgs of tail runs.
 int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
   if (launch_failure_injected()) {
     *err = "kernel launch: failure injected by MG3M_TEST_FAIL_LAUNCH";
@@ -139,18 +155,24 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
     *err = "internal: the fp64-accumulating kernel has no fused output stage";
     return MG3M_ERR_PLAN;
   }
+  // stream-K runs need the kernel's loop over pieces; other kernels take one
+  // piece per work-group
+  if (p.tail_wgs > 0 && p.sk_s == 0 && (p.acc64 || !tail_runs_multi(p.b_mode))) {
+    *err = "internal: stream-K tail plan for a kernel without multi-piece runs";
+    return MG3M_ERR_PLAN;
+  }
+  if (p.dp_tiles < 0 || p.tail_wgs < 0 || p.grid != (long long)p.dp_tiles + p.tail_wgs || p.grid < 1 ||
+      p.grid > 0x7fffffffLL || (p.tail_wgs > 0 && (a.ws == nullptr || p.sk_q < 1))) {
+    *err = "internal: grid out of range or inconsistent";
+    return MG3M_ERR_PLAN;
+  }
   KernelFn fn = p.acc64 ? kernel64_for(p.variant, p.tile)
                         : (fused ? kernel_fused_for(p.variant, p.tile) : kernel_for(p.variant, p.tile));
   if (fn == nullptr) {
     *err = "internal: no kernel for this loader variant and tile";
     return MG3M_ERR_PLAN;
   }
-  if (p.grid < 1 || p.grid > 0x7fffffffLL) {
-    *err = "internal: grid size out of range";
-    return MG3M_ERR_PLAN;
-  }
-  hipLaunchKernelGGL(fn, dim3((unsigned)p.grid), dim3(p.t.wm * p.t.wn * 64), 0,
-                     (hipStream_t)stream, a);
+  hipLaunchKernelGGL(fn, dim3((unsigned)p.grid), dim3(p.t.wm * p.t.wn * 64), 0, (hipStream_t)stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(e);

@@ -126,15 +126,17 @@ inline constexpr TileDesc kTiles64[kNumTiles64] = {
 constexpr long long kMaxTensorBytes = 0xFFFFFFC0LL;
 
 // How the output tiles are scheduled.  Tiles are numbered tm + tiles_m * tn.
-// The first dp_tiles tiles are computed whole, one work-group each, and
-// written to y.  The remaining tail_tiles tiles are split along the reduction
-// into `split` chunks of k_tiles_per_split k-tiles, one work-group each;
-// those write tile-local partials to the workspace and a second kernel sums
-// each tile's chunks in chunk order into y (deterministic).  Pure data
-// parallel: tail_tiles = 0.  Classic split-K: dp_tiles = 0.  Hybrid: dp_tiles
-// is a whole number of rounds of resident work-groups and only the leftover
-// tiles are split, so the last round is filled with short chunks instead of
-// running mostly empty.
+// One launch: its first dp_tiles work-groups compute one whole tile each and
+// write it to y; the remaining tail_wgs work-groups share the reduction steps
+// of the other tail_tiles tiles (tail_tiles * k_tiles steps, tile by tile) in
+// contiguous runs, each piece of a run (its part in one tile) writing
+// tile-local partials to the workspace; a second kernel sums each tile's
+// pieces in run order into y (deterministic).  Split plans (sk_s > 0) cut
+// every tail tile into sk_s runs; stream-K plans (sk_s == 0) cut all the
+// steps into tail_wgs equal runs, a run then spanning up to two tiles.  Pure
+// data parallel: tail_tiles = 0.  Split-K: dp_tiles = 0.  Hybrid: dp_tiles is
+// a whole number of rounds of resident work-groups and the leftover tiles'
+// steps fill the last round evenly instead of leaving it mostly empty.
 struct Plan {
   int layout;
   int acc64;                // 1: the fp64-accumulating kernel (tile indexes kTiles64)
@@ -143,9 +145,11 @@ struct Plan {
   int k_tiles;              // ceil(Kg / kt)
   int tiles_m, tiles_n;
   int dp_tiles, tail_tiles;
-  int split;                // chunks per tail tile (1 when there is no tail)
-  int kps;                  // k-tiles per chunk
-  long long grid;           // dp_tiles + tail_tiles * split
+  int tail_wgs;             // work-groups sharing the tail tiles' reduction steps (0 without a tail)
+  int sk_s;                 // split plans: runs per tail tile (tail_wgs = sk_s * tail_tiles); stream-K: 0
+  int sk_q, sk_r;           // steps per run: sk_q, one more for the first sk_r (of each tile when split)
+  int split;                // tail work-groups per tail tile, rounded up (1 without a tail)
+  long long grid;           // dp_tiles + tail_wgs
   int a_mode, b_mode, e_mode;
   int variant;
   size_t ws_bytes;          // workspace: the filter copy (wt_bytes), then the partials
@@ -166,7 +170,9 @@ struct KArgs {
   int sh, sw, ph, pw, Ho, Wo;
   int Mg, Ng, Kg;
   int tiles_m, k_tiles;
-  int dp_tiles, tail_tiles, kps;
+  int dp_tiles, tail_tiles;
+  int sk_q, sk_r;           // tail runs (see Plan)
+  int sk_s;                 // split plans: runs per tail tile; stream-K plans: 0
   int e_mode;
   int mstride;              // output elements between output channels m and m+1
   const float* add;         // added to each output before the activation (y's layout), or null
@@ -178,7 +184,8 @@ struct RArgs {
   const void* ws;           // fp32 partials, or fp64 ones when f64
   float* y;
   int mt, nt;               // tile shape
-  int tiles_m, dp_tiles, tail_tiles, split;
+  int tiles_m, dp_tiles, tail_tiles;
+  int k_tiles, sk_q, sk_r, sk_s;  // the tail runs, as in KArgs
   int layout, N, K, HoWo, Mg, Ng;
   int vec4;                 // four consecutive columns are contiguous in y
   int f64;                  // the partials are fp64
@@ -212,6 +219,12 @@ int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride_h, in
 int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x16, bool w16,
               bool y16, Plan* p, std::string* err);
 std::string plan_to_string(const ConvShape& s, const Plan& p);
+
+// Whether the fp32 kernel of a patch loader runs stream-K tail plans (runs
+// spanning two tiles, taken in a loop).  Only the one-tap HWCN loader does
+// so without losing occupancy on its whole tiles; the others, and the
+// fp64-accumulating kernel, take split tail plans (one piece per run).
+constexpr bool tail_runs_multi(int b_mode) { return b_mode == kBVecNTap; }
 
 // Kernel entry points by (variant, tile): conv_hwcn_*.hip, conv_nchw.hip.
 using KernelFn = void (*)(KArgs);

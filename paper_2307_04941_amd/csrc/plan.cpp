@@ -67,6 +67,7 @@ double variant_factor(int variant) {
 
 struct Override {
   int mt = 0, nt = 0, kt = 0, split = 0, tail = 0;
+  long long sk = 0;
 };
 
 int parse_override(const char* text, Override* o, std::string* err) {
@@ -122,21 +123,43 @@ int parse_override(const char* text, Override* o, std::string* err) {
         return MG3M_ERR_PLAN;
       }
       o->tail = (int)v;
+    } else if (key == "sk") {
+      long long v = std::strtoll(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || v < 1 || v > 0x7fffffffLL) {
+        *err = "plan override: sk must be 1..2^31-1";
+        return MG3M_ERR_PLAN;
+      }
+      o->sk = v;
     } else {
       *err = "plan override: unknown key '" + key + "'";
       return MG3M_ERR_PLAN;
     }
     if (end == s.size()) break;
   }
+  if ((o->split > 0) + (o->tail > 0) + (o->sk > 0) > 1) {
+    *err = "plan override: give at most one of split, tail and sk";
+    return MG3M_ERR_PLAN;
+  }
   return MG3M_OK;
 }
 
-// How a candidate schedules its tiles (see Plan).
-enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2 };
+// How a candidate schedules its tiles (see Plan).  kSplitAll and kSplitTail
+// cut each tail tile's reduction into `param` runs; kStreamK deals the
+// left-over tiles' k-tiles out to `param` work-groups in all (a split when
+// the runs fall on tile boundaries).
+enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2, kStreamK = 3 };
 
-// Fill the shape-dependent parts of a plan for one (tile, schedule, split)
-// choice.  Returns false when the tile count does not fit a launch.
-bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, int split_req, Plan* p) {
+// Partials the tail work-groups write: one per run, plus (stream-K) one for
+// each tail tile boundary that falls inside a run.
+long long tail_pieces(const Plan& p) {
+  if (p.tail_wgs == 0) return 0;
+  if (p.sk_s > 0) return p.tail_wgs;
+  return (long long)p.tail_wgs + p.tail_tiles - 1;
+}
+
+// Fill the shape-dependent parts of a plan for one (tile, schedule, param)
+// choice.  Returns false when the choice does not apply to the shape.
+bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, long long param, Plan* p) {
   const TileDesc& t = tile_desc(acc64, tile);
   p->layout = s.layout;
   p->acc64 = acc64 ? 1 : 0;
@@ -147,44 +170,65 @@ bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, int split_r
   p->tiles_n = (int)cdiv(s.Ng, t.nt);
   const long long tiles = (long long)p->tiles_m * p->tiles_n;
   if (tiles > 0x7fffffffLL) return false;
-  if (sched == kDataParallel || split_req <= 1) {
-    p->dp_tiles = (int)tiles;
-    p->tail_tiles = 0;
-  } else if (sched == kSplitAll) {
-    p->dp_tiles = 0;
-    p->tail_tiles = (int)tiles;
-  } else {
+  long long dp = tiles, tail = 0;
+  if (sched == kSplitAll && param > 1) {
+    dp = 0;
+    tail = tiles;
+  } else if ((sched == kSplitTail && param > 1) || sched == kStreamK) {
     // whole rounds of resident work-groups run unsplit (none if the tiles do
-    // not fill one round: then every tile is split)
+    // not fill one round: then every tile is shared out)
     const long long slots = (long long)kCUs * resident_wgs(t, acc64);
-    const long long dp = tiles / slots * slots;
-    p->dp_tiles = (int)dp;
-    p->tail_tiles = (int)(tiles - dp);
+    dp = tiles / slots * slots;
+    tail = tiles - dp;
   }
-  p->kps = p->k_tiles;
-  p->split = 1;
-  if (p->tail_tiles > 0) {
-    p->kps = (int)cdiv(p->k_tiles, std::max(1, std::min(split_req, p->k_tiles)));
-    p->split = (int)cdiv(p->k_tiles, p->kps);       // no empty chunk
-    if (p->split < 2) {                              // too short to split: run whole
-      p->dp_tiles = (int)tiles;
-      p->tail_tiles = 0;
-      p->kps = p->k_tiles;
-      p->split = 1;
+  const long long k = p->k_tiles;
+  long long wgs = 0, runs = 0, q = 0, r = 0;    // runs: per tail tile (split), 0 (stream-K)
+  if (tail > 0) {
+    const long long steps = tail * k;
+    if (steps > 0x7fffffffLL) return false;          // int step numbers in the kernels
+    if (sched == kStreamK) {
+      if (param < tail || param > steps) return false;
+      wgs = param;
+      if (wgs % tail == 0 && k % (wgs / tail) == 0) {
+        runs = wgs / tail;                           // equal runs inside each tile: a split
+        q = k / runs;
+      } else {
+        q = steps / wgs;
+        r = steps % wgs;
+      }
+    } else {
+      runs = std::min<long long>(param, k);         // no empty run
+      wgs = tail * runs;
+      q = k / runs;
+      r = k % runs;
+    }
+    if (runs == 1) {                                 // one run per tile: run them whole
+      dp = tiles;
+      tail = wgs = q = r = runs = 0;
     }
   }
-  p->grid = (long long)p->dp_tiles + (long long)p->tail_tiles * p->split;
+  if (dp + wgs > 0x7fffffffLL) return false;
+  p->dp_tiles = (int)dp;
+  p->tail_tiles = (int)tail;
+  p->tail_wgs = (int)wgs;
+  p->sk_s = (int)runs;
+  p->sk_q = (int)q;
+  p->sk_r = (int)r;
+  p->split = tail > 0 ? (int)cdiv(wgs, tail) : 1;
+  p->grid = dp + wgs;
   p->lds_bytes = lds_bytes(t, acc64);
   const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
                         (double)p->k_tiles * t.kt;
   p->pad_eff = (double)s.Mg * (double)s.Ng * (double)s.Kg / padded;
-  p->ws_bytes = (size_t)p->tail_tiles * p->split * t.mt * t.nt * (acc64 ? sizeof(double) : sizeof(float));
+  // partial slots: run w's piece in tail tile j goes to slot w + j
+  const long long slots = wgs > 0 ? wgs + tail - 1 : 0;
+  p->ws_bytes = (size_t)slots * t.mt * t.nt * (acc64 ? sizeof(double) : sizeof(float));
   p->est_us = 0.0;
   return true;
 }
 
 // The selector's predicted time for a plan (microseconds).  Work-groups are
-// dispatched in order, whole tiles first and tail chunks after them.  In each
+// dispatched in order, whole tiles first and tail runs after them.  In each
 // phase the busiest CU runs ceil(work-groups / 256) of them, each costing its
 // padded MFMA flops at the tile's measured efficiency, scaled down when that
 // CU holds too few waves to hide latency, plus a fixed cost per round of
@@ -204,10 +248,12 @@ double predict_us(const ConvShape& s, const Plan& p) {
     return (double)per_cu * tile_flops * k_tiles / (rate * kClockHz * eff) * 1e6 +
            (double)cdiv(per_cu, occ) * kRoundUs;
   };
-  const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase((long long)p.tail_tiles * p.split, p.kps);
+  const int run_k = p.tail_wgs > 0 ? p.sk_q + (p.sk_r > 0 ? 1 : 0) : 0;
+  const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase(p.tail_wgs, run_k);
   const double y_bytes = 4.0 * (double)s.Mg * (double)s.Ng;
   const double xw_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
-  const double part_bytes = (double)(p.ws_bytes - p.wt_bytes);
+  const double part_bytes =
+      (double)tail_pieces(p) * t.mt * t.nt * (p.acc64 ? sizeof(double) : sizeof(float));
   const double t_mem = (xw_bytes + y_bytes + part_bytes) / kStreamBytesPerS * 1e6;
   double est = std::max(t_comp, t_mem) + kLaunchUs;
   if (p.tail_tiles > 0) {
@@ -296,10 +342,10 @@ void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
     p->wt_bytes = ((size_t)4 * (size_t)s.Mg * (size_t)s.Kg + 255) / 256 * 256;
     p->ws_bytes += p->wt_bytes;
   }
-  // Four consecutive output channels are contiguous only in HWCN with N == 1;
-  // the split-K workspace is 256-byte aligned and has the output's layout.
-  const bool out16 = p->split > 1 ? true : y16;
-  p->e_mode = (s.layout == kHWCN && s.N == 1 && s.K % 4 == 0 && out16) ? kEVecM : kEElem;
+  // Four consecutive output channels are contiguous only in HWCN with N == 1
+  // (whole tiles store them with one 16-byte store; partials are stored per
+  // element, so only y's alignment matters).
+  p->e_mode = (s.layout == kHWCN && s.N == 1 && s.K % 4 == 0 && y16) ? kEVecM : kEElem;
   // the fp64 accumulator holds no four adjacent rows in one lane
   if (p->acc64) p->e_mode = kEElem;
 }
@@ -318,10 +364,12 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   Plan best_plan{};
   // the split factors the cost model was calibrated on
   const int splits[] = {2, 3, 4, 6, 8, 16};
-  auto consider = [&](int ti, int sched, int sp) {
+  auto consider = [&](int ti, int sched, long long sp) {
     Plan c{};
     if (!shape_plan(s, acc64, ti, sched, sp, &c)) return;
     choose_modes(s, x16, w16, y16, &c);
+    // runs spanning two tiles need the kernel's loop over pieces
+    if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || !tail_runs_multi(c.b_mode))) return;
     c.est_us = predict_us(s, c);
     // ties: less workspace traffic, then the larger tile
     const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
@@ -342,18 +390,26 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       consider(ti, o.split > 1 ? kSplitAll : kDataParallel, o.split);
     } else if (o.tail) {
       consider(ti, kSplitTail, o.tail);
+    } else if (o.sk) {
+      consider(ti, kStreamK, o.sk);
     } else {
       consider(ti, kDataParallel, 1);
       for (int sp : splits) {
         consider(ti, kSplitAll, sp);
         consider(ti, kSplitTail, sp);
       }
+      // stream-K over the left-over tiles with one to all resident work-groups per CU
+      for (int j = 1, occ = resident_wgs(td, acc64); j <= occ; ++j) consider(ti, kStreamK, (long long)j * kCUs);
     }
   }
   if (best < 0) {
     *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
            (o.kt ? " kt=" + std::to_string(o.kt) : std::string()) +
-           (o.tail ? " tail=" + std::to_string(o.tail) : std::string());
+           (o.tail ? " tail=" + std::to_string(o.tail) : std::string()) +
+           (o.sk ? " sk=" + std::to_string(o.sk) +
+                       " (from the left-over tiles to their k-tiles in total; runs spanning two tiles"
+                       " only with the fp32 kernel's one-tap HWCN loader)"
+                 : std::string());
     return MG3M_ERR_PLAN;
   }
   *p = best_plan;
@@ -366,10 +422,10 @@ std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
-                "%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,grid=%lld,"
+                "%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,tail_wgs=%d,grid=%lld,"
                 "tiles=%dx%d,k_tiles=%d,a=%s,b=%s,e=%s,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
                 "Mg=%lld,Ng=%lld,Kg=%lld",
-                p.acc64 ? "acc=f64," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.grid,
+                p.acc64 ? "acc=f64," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.tail_wgs, p.grid,
                 p.tiles_m, p.tiles_n, p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode],
                 p.lds_bytes, p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
   return buf;

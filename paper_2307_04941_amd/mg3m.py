@@ -36,8 +36,8 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [
         ("mt", ctypes.c_int), ("nt", ctypes.c_int), ("kt", ctypes.c_int),
         ("waves_m", ctypes.c_int), ("waves_n", ctypes.c_int),
-        ("split", ctypes.c_int), ("k_tiles", ctypes.c_int), ("k_tiles_per_split", ctypes.c_int),
-        ("dp_tiles", ctypes.c_int), ("tail_tiles", ctypes.c_int),
+        ("split", ctypes.c_int), ("k_tiles", ctypes.c_int), ("k_tiles_per_wg", ctypes.c_int),
+        ("dp_tiles", ctypes.c_int), ("tail_tiles", ctypes.c_int), ("tail_wgs", ctypes.c_int),
         ("tiles_m", ctypes.c_int), ("tiles_n", ctypes.c_int),
         ("grid", ctypes.c_longlong), ("Mg", ctypes.c_longlong), ("Ng", ctypes.c_longlong),
         ("Kg", ctypes.c_longlong), ("workspace_bytes", ctypes.c_size_t), ("lds_bytes", ctypes.c_int),
@@ -71,6 +71,15 @@ def load_library(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2307_04941_amd.build`")
+    # torch ships its own HIP and HSA runtimes under the same sonames as
+    # ROCm's.  Loaded first, they satisfy the library's dependencies and one
+    # runtime serves the process; loaded after the library, they come in as
+    # second copies, and whichever runtime initialises the device second finds
+    # none (hipErrorNoDevice at the first launch).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     i, p, sz, cp = ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_char_p
     shape = [i] * 10                     # N, C, H, W, K, R, S, stride, pad, layout

@@ -6,6 +6,7 @@ metric reproduces the paper's printed example."""
 import json
 import os
 import re
+import sys
 
 import numpy as np
 import pytest
@@ -121,23 +122,28 @@ def _check_plan(shape, layout, plan=None):
     # tiles cover the output exactly once
     assert (p["tiles_m"] - 1) * p["mt"] < Mg <= p["tiles_m"] * p["mt"]
     assert (p["tiles_n"] - 1) * p["nt"] < Ng <= p["tiles_n"] * p["nt"]
-    # whole tiles and split tail tiles partition the tiles; chunks partition
-    # the k-tiles, none empty
+    # whole tiles and tail tiles partition the tiles; the tail work-groups'
+    # runs partition the tail tiles' k-tiles, none empty and none longer than
+    # a tile
     kt = p["k_tiles"]
     assert kt == -(-Kg // p["kt"])
     tiles = p["tiles_m"] * p["tiles_n"]
     assert p["dp_tiles"] + p["tail_tiles"] == tiles
-    if p["tail_tiles"]:
-        assert p["split"] >= 2
-        assert (p["split"] - 1) * p["k_tiles_per_split"] < kt <= p["split"] * p["k_tiles_per_split"]
+    tail, wgs = p["tail_tiles"], p["tail_wgs"]
+    if tail:
+        assert tail < wgs <= tail * kt < 2**31
+        assert p["k_tiles_per_wg"] == -(-tail * kt // wgs) <= kt
+        assert p["split"] == -(-wgs // tail) >= 2
     else:
-        assert p["split"] == 1 and p["k_tiles_per_split"] == kt
-    assert p["grid"] == p["dp_tiles"] + p["tail_tiles"] * p["split"] <= 2**31 - 1
-    # partials, plus the [R][S][C][K] filter copy of a tap-major NCHW plan (b_mode 5)
+        assert wgs == 0 and p["split"] == 1 and p["k_tiles_per_wg"] == kt
+    assert p["grid"] == p["dp_tiles"] + wgs <= 2**31 - 1
+    # partials (slots up to wgs + tail - 2), plus the [R][S][C][K] filter copy
+    # of a tap-major NCHW plan (b_mode 5)
     copy = -(-4 * Mg * Kg // 256) * 256 if p["b_mode"] == 5 else 0
     assert p["b_mode"] != 5 or (layout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
                                 and (st if isinstance(st, int) else st[1]) == 1)
-    assert p["workspace_bytes"] == 4 * p["tail_tiles"] * p["split"] * p["mt"] * p["nt"] + copy
+    slots = wgs + tail - 1 if tail else 0
+    assert p["workspace_bytes"] == 4 * slots * p["mt"] * p["nt"] + copy
     assert 0 < p["lds_bytes"] <= 160 * 1024
     assert 0 < p["pad_efficiency"] <= 1.0
     assert p["est_us"] > 0
@@ -171,6 +177,62 @@ def test_plans_random_grid_and_overrides():
         assert f"{p['mt']}x{p['nt']}" == t.split(",")[0]
         assert p["kt"] == (32 if "kt=32" in t else 16)
         assert p["split"] <= sp
+
+
+def test_one_hip_runtime_per_process():
+    """torch bundles HIP and HSA runtimes under ROCm's sonames: the binding
+    loads torch first so that the library binds to those, and the process
+    holds one HIP runtime whichever of the two the caller touches first."""
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("from paper_2307_04941_amd import mg3m; mg3m.load_library(); import torch; "
+            "m = open('/proc/self/maps').read(); "
+            "print(len({l.split()[-1] for l in m.splitlines() if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "1"
+
+
+def test_stream_k_override():
+    """sk=<g>: the tiles left over after whole rounds, their k-tiles dealt
+    out to g work-groups; g must lie between the tail tiles and their
+    k-tiles in total (g equal to the tail tiles runs them whole)."""
+    small = (4, 64, 14, 14, 256, 3, 3, 1, 1)          # 256x64: 13 tiles, below one round
+    base = _check_plan(small, "HWCN", "tile=256x64,tail=2")
+    tail, kt = base["tail_tiles"], base["k_tiles"]
+    assert (base["dp_tiles"], tail, kt) == (0, 13, 36)
+    for g in (tail + 1, 27, 100, 467, tail * kt):
+        p = _check_plan(small, "HWCN", f"tile=256x64,sk={g}")
+        assert (p["dp_tiles"], p["tail_tiles"], p["tail_wgs"]) == (0, tail, g)
+    p = _check_plan(small, "HWCN", f"tile=256x64,sk={tail}")
+    assert (p["dp_tiles"], p["tail_wgs"]) == (13, 0)
+    rounds = (24, 16, 111, 111, 32, 3, 3, 1, 1)       # whole rounds first
+    r = _check_plan(rounds, "HWCN", "tile=256x64,tail=2")
+    assert r["dp_tiles"] > 0 and r["tail_tiles"] > 0
+    p = _check_plan(rounds, "HWCN", f"tile=256x64,sk={r['tail_tiles'] + 100}")
+    assert (p["dp_tiles"], p["tail_tiles"], p["tail_wgs"]) == (r["dp_tiles"], r["tail_tiles"], r["tail_tiles"] + 100)
+    # runs spanning two tiles only with the one-tap HWCN loader (b_mode 3) of
+    # the fp32 kernel; runs that fall on tile boundaries are a split anywhere
+    for layout, shape in (("NCHW", small), ("HWCN", (3, 64, 14, 14, 256, 3, 3, 1, 1))):
+        with pytest.raises(mg3m.Mg3mError) as ei:
+            mg3m.conv2d_fwd_f32_plan_info(*shape, layout, f"tile=256x64,sk={tail + 1}")
+        assert ei.value.status == 7 and "one-tap HWCN" in mg3m.mg3m_last_error()
+    p = _check_plan(small, "NCHW", f"tile=256x64,sk={4 * tail}")
+    assert (p["tail_wgs"], p["split"], p["k_tiles_per_wg"]) == (4 * tail, 4, 9)
+    for bad in (f"tile=256x64,sk={tail - 1}", f"tile=256x64,sk={tail * kt + 1}", "sk=0", "sk=x",
+                "split=2,sk=20", "tail=2,sk=20", "split=2,tail=3"):
+        with pytest.raises(mg3m.Mg3mError) as ei:
+            mg3m.conv2d_fwd_f32_plan_info(*small, "HWCN", bad)
+        assert ei.value.status == 7, bad
+
+
+def test_selector_uses_full_rounds_for_small_layers():
+    """A layer with fewer tiles than one round of resident work-groups
+    (VGG-16's 14x14 layers at N=64) gets its reduction shared out over one
+    full round, not a split that leaves part of a second round."""
+    p = _check_plan((64, 512, 14, 14, 512, 3, 3, 1, 1), "HWCN")
+    assert p["dp_tiles"] == 0 and p["tail_tiles"] > 0
+    assert p["tail_wgs"] % 256 == 0
 
 
 def test_plan_string_roundtrip():
@@ -254,14 +316,15 @@ def _acc64_plan(shape, layout, plan=None):
     mt, nt = (int(v) for v in f["tile"].split("x"))
     tm, tn = (int(v) for v in f["tiles"].split("x"))
     assert (tm - 1) * mt < Mg <= tm * mt and (tn - 1) * nt < Ng <= tn * nt
-    # whole tiles and split tail tiles partition the tiles; fp64 partials
+    # whole tiles and tail tiles partition the tiles; fp64 partials
     kt, split, dp, tail = int(f["k_tiles"]), int(f["split"]), int(f["dp_tiles"]), int(f["tail_tiles"])
+    wgs = int(f["tail_wgs"])
     assert f["kt"] == "16" and kt == -(-Kg // 16)
     assert dp + tail == tm * tn
-    assert int(f["grid"]) == dp + tail * split
-    assert (split >= 2) if tail else (split == 1)
+    assert int(f["grid"]) == dp + wgs
+    assert (split >= 2 and tail < wgs <= tail * kt) if tail else (split == 1 and wgs == 0)
     copy = -(-4 * Mg * Kg // 256) * 256 if f["b"] == "vec_w_tap" else 0
-    assert int(f["ws"]) == 8 * tail * split * mt * nt + copy
+    assert int(f["ws"]) == 8 * ((wgs + tail - 1) if tail else 0) * mt * nt + copy
     assert f["e"] == "elem"
     assert 0 < int(f["lds"]) <= 160 * 1024
     return f
