@@ -81,8 +81,9 @@ int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, in
  * work-groups (all tiles, or only those left over after whole rounds of
  * work-groups; each work-group takes an equal run of their k-tiles, stream-K
  * fashion), the pieces' partial sums go to a workspace that this call takes
- * from HIP's stream-ordered allocator (hipMallocAsync / hipFreeAsync on
- * `stream`) and a second kernel sums them in a fixed order, so results are
+ * from the library's stream-ordered pool for the stream's device (taken and
+ * given back on `stream`; see mg3m_trim_workspace_pool) and a second kernel
+ * sums them in a fixed order, so results are
  * deterministic run to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
  * a filter of more than one tap and stride_w 1 take the reduction tap-major: a
  * first kernel copies the filter to [R][S][C][K] in that workspace. */
@@ -152,8 +153,8 @@ int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, 
  * rounding of its fp64 sum.  On fp64 MFMA (half the fp32 peak).  Separate
  * vertical and horizontal stride and padding as in conv2d_fwd_f32_hw.  When
  * the plan shares out the reduction of some tiles, their pieces' fp64 partial
- * sums go to a workspace taken from HIP's stream-ordered allocator
- * (hipMallocAsync / hipFreeAsync on `stream`) and a second kernel adds them
+ * sums go to a workspace taken from the library's stream-ordered pool (as
+ * for conv2d_fwd_f32) and a second kernel adds them
  * in a fixed order in fp64 before the one rounding, so results are
  * deterministic run to run.  plan: NULL, or an override with the keys of
  * conv2d_fwd_f32_ex: tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
@@ -317,6 +318,16 @@ const char *mg3m_status_string(int status);
 
 /* Detail of the last error on the calling host thread ("" if none). */
 const char *mg3m_last_error(void);
+
+/* The workspaces that conv2d_fwd_f32 and conv2d_fwd_f32_acc64 take for
+ * themselves come from one stream-ordered memory pool per device, which the library creates at the first such call
+ * on that device.  Freed blocks stay in the pool for the next call (mapping
+ * tens of MB afresh per call costs microseconds), so a pool holds the most
+ * that calls on its device had in use at once.  This call returns to the
+ * system every block of every pool that no call is using, and keeps the pools
+ * for later calls.  Host call; work already queued is unaffected.  Returns
+ * MG3M_OK, or MG3M_ERR_HIP with the HIP error text in mg3m_last_error(). */
+int mg3m_trim_workspace_pool(void);
 
 #ifdef __cplusplus
 }

@@ -96,6 +96,60 @@ int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16
   return MG3M_OK;
 }
 
+// The plain entry points take their partials from one stream-ordered pool per
+// device, made on first use.  Its release threshold is the maximum, so a freed
+// block stays mapped in the pool and the next call on that device reuses it.
+// With the default pool (threshold 0) every call mapped its 20-100 MB of
+// partials afresh, which cost 5-16 us per call on the VGG-16 layers.  A pool
+// holds the most that calls on its device had live at once, until the process
+// ends or mg3m_trim_workspace_pool() gives back what no call is using.
+struct WsPools {
+  std::mutex mu;
+  std::unordered_map<int, hipMemPool_t> pools;
+};
+WsPools& ws_pools() {
+  static WsPools* p = new WsPools();   // never destroyed, like the plan cache
+  return *p;
+}
+
+int workspace_pool(void* stream, hipMemPool_t* pool, std::string* err) {
+  int dev = 0;
+  hipError_t e = stream != nullptr ? hipStreamGetDevice(static_cast<hipStream_t>(stream), &dev)
+                                   : hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *err = std::string("device of the stream: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  WsPools& wp = ws_pools();
+  std::lock_guard<std::mutex> lock(wp.mu);
+  auto it = wp.pools.find(dev);
+  if (it != wp.pools.end()) {
+    *pool = it->second;
+    return MG3M_OK;
+  }
+  hipMemPoolProps props{};
+  props.allocType = hipMemAllocationTypePinned;
+  props.handleTypes = hipMemHandleTypeNone;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = dev;
+  hipMemPool_t p = nullptr;
+  e = hipMemPoolCreate(&p, &props);
+  if (e != hipSuccess) {
+    *err = std::string("hipMemPoolCreate: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  uint64_t keep = UINT64_MAX;
+  e = hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
+  if (e != hipSuccess) {
+    hipMemPoolDestroy(p);
+    *err = std::string("hipMemPoolSetAttribute: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  wp.pools.emplace(dev, p);
+  *pool = p;
+  return MG3M_OK;
+}
+
 int run(const float* x, const float* w, float* y, const Geom& g, void* workspace,
         size_t workspace_bytes, bool own_workspace, const char* plan, void* stream,
         const float* add = nullptr, int relu = 0) {
@@ -120,9 +174,12 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   float* ws = nullptr;
   if (p.ws_bytes > 0) {
     if (own_workspace) {
-      hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), p.ws_bytes,
-                                    static_cast<hipStream_t>(stream));
-      if (e != hipSuccess) return fail(MG3M_ERR_HIP, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+      hipMemPool_t pool = nullptr;
+      std::string perr;
+      if (int prc = workspace_pool(stream, &pool, &perr)) return fail(prc, perr);
+      hipError_t e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), p.ws_bytes, pool,
+                                            static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return fail(MG3M_ERR_HIP, std::string("hipMallocFromPoolAsync: ") + hipGetErrorString(e));
     } else {
       if (workspace == nullptr || workspace_bytes < p.ws_bytes)
         return fail(MG3M_ERR_WORKSPACE, "plan needs " + std::to_string(p.ws_bytes) + " workspace bytes");
@@ -476,5 +533,17 @@ const char* mg3m_status_string(int status) {
 }
 
 const char* mg3m_last_error(void) { return g_last_error.c_str(); }
+
+int mg3m_trim_workspace_pool(void) {
+  g_last_error.clear();
+  WsPools& wp = ws_pools();
+  std::lock_guard<std::mutex> lock(wp.mu);
+  for (auto& kv : wp.pools) {
+    hipError_t e = hipMemPoolTrimTo(kv.second, 0);
+    if (e != hipSuccess)
+      return fail(MG3M_ERR_HIP, "hipMemPoolTrimTo (device " + std::to_string(kv.first) + "): " + hipGetErrorString(e));
+  }
+  return MG3M_OK;
+}
 
 }  // extern "C"

@@ -111,6 +111,7 @@ def load_library(path: str = LIB_PATH):
     lib.mg3m_status_string.restype = ctypes.c_char_p
     lib.mg3m_last_error.argtypes = []
     lib.mg3m_last_error.restype = ctypes.c_char_p
+    lib.mg3m_trim_workspace_pool.argtypes = []
     for name in ("conv2d_out_dims", "conv2d_out_dims_hw", "conv2d_fwd_f32_hw",
                  "conv2d_fwd_f32_hw_workspace_bytes", "conv2d_fwd_f32_acc64",
                  "conv2d_fwd_f32_acc64_plan_string", "conv2d_fwd_f32_fused", "maxpool2d_f32",
@@ -388,6 +389,10 @@ def mg3m_padding_overhead(M, N, C, mt, nt):
     f, d = ctypes.c_double(), ctypes.c_double()
     _check(load_library().mg3m_padding_overhead(M, N, C, mt, nt, ctypes.byref(f), ctypes.byref(d)))
     return f.value, d.value
+
+
+def mg3m_trim_workspace_pool():
+    _check(load_library().mg3m_trim_workspace_pool())
 
 
 # ------------------------------------------------------- tensor convenience

@@ -132,3 +132,26 @@ def test_split_runs_acc64(plan, layout):
     acc, mag = oracle.conv2d(x, w, st, pd, layout)
     y = run_gpu(x, w, st, pd, layout, plan=plan, acc64=True)
     assert_parity_acc64(y, acc, mag, 9 * 64, f"{plan} {layout}")
+
+
+# Plain calls whose selector plan shares tiles out: their partials come from
+# the library's per-device pool, which keeps freed blocks for the next call.
+POOL_SEQ = [SK_SMALL, (8, 256, 14, 14, 256, 3, 3, 1, 1), SK_SCALAR, (8, 256, 14, 14, 256, 3, 3, 1, 1)]
+
+
+def test_workspace_pool_reuse_and_trim():
+    for i, shape in enumerate(POOL_SEQ):
+        info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN")
+        say(f"pool call {i}: {shape} tail_wgs {info['tail_wgs']} ws {info['workspace_bytes']}")
+        assert info["tail_wgs"] > 0 and info["workspace_bytes"] > 0
+        x, w, st, pd = make(shape, 780 + i, "HWCN")
+        acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+        y = run_gpu(x, w, st, pd, "HWCN")          # plan None: conv2d_fwd_f32, own workspace
+        assert_parity(y, acc, mag, f"pool call {i} {shape}")
+        if i == 1:
+            mg3m.mg3m_trim_workspace_pool()
+    x, w, st, pd = make(SK_SMALL, 790, "HWCN")
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    Kg = SK_SMALL[1] * SK_SMALL[5] * SK_SMALL[6]
+    assert_parity_acc64(run_gpu(x, w, st, pd, "HWCN", acc64=True), acc, mag, Kg, "acc64 after trim")
+    mg3m.mg3m_trim_workspace_pool()
