@@ -36,7 +36,7 @@ constexpr int kMaxWavesPerSimd = 8;
 // how MFMA utilisation falls when fewer than ~2 waves per SIMD are resident.
 constexpr double kStreamBytesPerS = 4.0e12;
 constexpr double kLaunchUs = 3.0;
-constexpr double kRoundUs = 3.0;
+constexpr double kRoundUs = 2.0;
 constexpr double kUtilBase = 0.5, kUtilPerWave = 0.1;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
