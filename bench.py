@@ -169,24 +169,28 @@ def main():
     def one_step(evs=None):
         for j, ((L, Ho, Wo), (xd, wd, yd)) in enumerate(zip(layers, dev_bufs)):
             if evs is not None:
-                evs[j][0].record(stream)
-                mg3m.mg3m_time_next_kernel(evs[j][2], evs[j][3])
+                mg3m.mg3m_time_next_kernel(evs[j][0], evs[j][1])
             if args.plan:
                 mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", plan=args.plan, out=yd)
             else:
                 mg3m.conv2d_fwd_f32(xd, wd, yd, L.N, L.C, L.H, L.W, L.K, L.R, L.S,
                                     L.stride, L.pad, "HWCN", sp)
-            if evs is not None:
-                evs[j][1].record(stream)
+        if evs is not None:
+            evs[-1][0].record(stream)
 
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly K steps.  Per layer and step: events around
-    # the C-ABI call, and (through mg3m_time_next_kernel) around its main
-    # convolution kernel alone, recorded on the stream the kernel runs on.
-    evs = [[tuple(new_event() for _ in range(4)) for _ in layers] for _ in range(args.steps)]
+    # ---- timed region: exactly K steps.  Per layer and step, two events
+    # around the main convolution kernel alone (mg3m_time_next_kernel records
+    # them on the stream the kernel runs on), and one event at the end of the
+    # step.  A layer's time runs from its main kernel's start to the next
+    # layer's (the end of the step for the last layer): its kernels, any tail
+    # reduction and the launch gaps.  Events around each whole call as well
+    # cost about 0.1 ms per step.
+    evs = [[tuple(new_event() for _ in range(2)) for _ in layers] + [(new_event(),)]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -199,8 +203,8 @@ def main():
 
     per_layer = []
     for j, (L, Ho, Wo) in enumerate(layers):
-        us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j][1]) for k in range(args.steps)])) * 1e3
-        kus = float(np.mean([evs[k][j][2].elapsed_time(evs[k][j][3]) for k in range(args.steps)])) * 1e3
+        us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j + 1][0]) for k in range(args.steps)])) * 1e3
+        kus = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j][1]) for k in range(args.steps)])) * 1e3
         fl = layer_flops(L, Ho, Wo)
         by = layer_alg_bytes(L, Ho, Wo)
         plan = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad,

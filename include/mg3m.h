@@ -301,8 +301,10 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,
  * next compute call (conv2d_fwd_f32, _ex, _hw or _acc64) made on the calling host thread
  * records start on its stream immediately before launching its main kernel
  * and stop immediately after it -- before any split-K reduction -- and then
- * clears the hook; a call rejected by validation leaves it set.  Returns
- * MG3M_OK, or MG3M_ERR_ARG if exactly one handle is NULL. */
+ * clears the hook; a call rejected by validation leaves it set.  The library
+ * keeps only the handles: both events must stay alive until that call has
+ * returned (or the hook is cleared).  Returns MG3M_OK, or MG3M_ERR_ARG if
+ * exactly one handle is NULL. */
 int mg3m_time_next_kernel(void *start, void *stop);
 
 /* Padding overhead of computing an M x N (x C deep) product in whole
