@@ -105,7 +105,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  * the plan needs none; must be 16-byte aligned and at least
  * conv2d_fwd_f32_workspace_bytes() long otherwise) and an optional plan
  * override.  Override syntax: comma-separated key=value pairs,
- *   tile=<MT>x<NT>   one of the kernel tile shapes (e.g. 128x128, 64x256)
+ *   tile=<MT>x<NT>   one of the kernel tile shapes: 128x128, 64x256, 256x64,
+ *                    64x128, 128x64, 64x64, 32x128, 32x64, 128x32, 64x32,
+ *                    256x128, 128x256, 128x128 with kt=32, and 16x64 (16x16x4
+ *                    MFMAs; the selector takes it only when K mod 32 is 1..16)
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
  *   split=<n>        share every tile's reduction out over n work-groups per tile
  *                    (1..64, clamped to the tile's k-tiles; 1 = no split)
@@ -115,7 +118,8 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    runs (stream-K); g from the number of left-over tiles to their
  *                    k-tiles in total, else MG3M_ERR_PLAN.  Runs that span two tiles
  *                    need the one-tap HWCN loader (HWCN, N and K multiples of 4, C a
- *                    multiple of kt, aligned buffers) of this fp32 call; other
+ *                    multiple of kt, aligned buffers) of this fp32 call and a
+ *                    32x32x2-MFMA tile (not 16x64); other
  *                    shapes accept only g that cuts every left-over tile into equal
  *                    runs (a split), else MG3M_ERR_PLAN
  * e.g. "tile=128x128,kt=32,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */

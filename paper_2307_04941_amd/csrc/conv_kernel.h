@@ -788,6 +788,34 @@ __device__ __forceinline__ void mma_stage64(f64x4 (&acc)[C::TM16][C::TN16], cons
   }
 }
 
+// fp32 16x16x4 MFMA, for 16-row tiles: the same operand layout as the fp64
+// 16x16x4 (lane (g, q) supplies A[row q][k = g] and B[k = g][column q]) on
+// the same LDS layout, with fp32 operands and accumulators.
+template <class C, int KT>
+__device__ __forceinline__ void mma_stage16(f32x4 (&acc)[C::TM16][C::TN16], const float* As,
+                                            const float* Bs, int wm, int wn, int g, int q) {
+  int ca[C::TM16], cb[C::TN16];
+#pragma unroll
+  for (int i = 0; i < C::TM16; ++i) ca[i] = g * C::AS + C::LA::col(g, wm * C::WTM + i * 16) + q;
+#pragma unroll
+  for (int j = 0; j < C::TN16; ++j) cb[j] = g * C::BS + C::LB::col(g, wn * C::WTN + j * 16) + q;
+  float av[KT / 4][C::TM16], bv[KT / 4][C::TN16];
+#pragma unroll
+  for (int kk = 0; kk < KT / 4; ++kk) {
+#pragma unroll
+    for (int i = 0; i < C::TM16; ++i) av[kk][i] = As[ca[i] + 4 * kk * C::AS];
+#pragma unroll
+    for (int j = 0; j < C::TN16; ++j) bv[kk][j] = Bs[cb[j] + 4 * kk * C::BS];
+  }
+#pragma unroll
+  for (int kk = 0; kk < KT / 4; ++kk)
+#pragma unroll
+    for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN16; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
+}
+
 // ------------------------------------------------------ stage pipeline
 // Runs nk stages of the reduction through the two LDS buffers, calling
 // compute(As, Bs) on each staged pair.  The loads of stage it+1 are issued
@@ -1083,10 +1111,108 @@ void conv_igemm_f32(KArgs a) {
       });
 }
 
+// ------------------------------------------------------ 16-row tiles
+// Layers with 16 or 48 output channels leave a half or a quarter of every
+// 32x32 MFMA block idle.  Their tiles run on 16x16x4 MFMAs instead, with the
+// operands staged in the 16x16-block LDS layout (as the fp64-accumulating
+// kernel does).  16x16x4 fp32 accumulator layout: element e of lane (g, q)
+// holds row 4*g + e, column q.
+__device__ __forceinline__ constexpr int m16_row(int g, int e) { return 4 * g + e; }
+
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, class Store>
+__device__ __forceinline__ void tile_product_f32m16(const KArgs& a, float* lds, int t, int tile, int kt0,
+                                                    int nk, Store&& store) {
+  using C = Cfg<MT, NT, KT, WM, WN, true>;
+  const int tm = tile % a.tiles_m;
+  const int tn = tile / a.tiles_m;
+  const int m0 = tm * MT, n0 = tn * NT;
+  const int kbeg = kt0 * KT;
+
+  float* const As0 = lds;
+  float* const Bs0 = lds + 2 * C::A_STAGE;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+
+  typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
+  typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
+  al.init(a, t, m0, kbeg);
+  bl.init(a, t, n0, kbeg);
+
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave % WM, wn = wave / WM;
+  const int g = lane >> 4, q = lane & 15;
+
+  f32x4 acc[C::TM16][C::TN16];
+#pragma unroll
+  for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN16; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
+    mma_stage16<C, KT>(acc, As, Bs, wm, wn, g, q);
+  });
+  store(acc, m0, n0, wm, wn, g, q);
+}
+
+// Work-groups [0, dp_tiles): whole tiles, stored to y (with the fused output
+// stage when FUSE); the rest: one split piece each, whose tile-local partial
+// sums (row-major mt x nt, fp32) the tail reduction adds up.  Runs crossing a
+// tile boundary (stream-K) are not taken by these tiles.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_f32_m16(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN, true>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  int tile, kt0 = 0, nk = a.k_tiles, w = 0, rel = 0;
+  const bool partial = (int)blockIdx.x >= a.dp_tiles;
+  if (!partial) {
+    tile = xcd_group(blockIdx.x, a.dp_tiles);
+  } else {
+    split_piece(a, blockIdx.x - a.dp_tiles, &w, &rel, &kt0, &nk);
+    tile = a.dp_tiles + rel;
+  }
+  tile_product_f32m16<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+      a, lds, threadIdx.x, tile, kt0, nk,
+      [&](f32x4 (&acc)[C::TM16][C::TN16], int m0, int n0, int wm, int wn, int g, int q) {
+        if (partial) {
+          float* const part = a.ws + tail_slot(w, rel) * (MT * NT);
+#pragma unroll
+          for (int j = 0; j < C::TN16; ++j) {
+            const int col = wn * C::WTN + j * 16 + q;
+#pragma unroll
+            for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) part[(wm * C::WTM + i * 16 + m16_row(g, e)) * NT + col] = acc[i][j][e];
+          }
+          return;
+        }
+        float* const out = a.y;
+#pragma unroll
+        for (int j = 0; j < C::TN16; ++j) {
+          const int n = n0 + wn * C::WTN + j * 16 + q;
+          if (n >= a.Ng) continue;
+          const int colbase = out_colbase<LAYOUT>(a, n);
+#pragma unroll
+          for (int i = 0; i < C::TM16; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int row = m0 + wm * C::WTM + i * 16 + m16_row(g, e);
+              if (row < a.Mg) {
+                const int idx = colbase + row * a.mstride;
+                if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][e], idx);
+                else out[idx] = acc[i][j][e];
+              }
+            }
+        }
+      });
+}
+
 template <int LAYOUT, int AM, int BM, bool FUSE, int TI>
 constexpr KernelFn kernel_at() {
   constexpr TileDesc d = kTiles[TI];
-  return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
+  if constexpr (d.m16 != 0) return &conv_igemm_f32_m16<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
+  else return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
 }
 
 template <int LAYOUT, int AM, int BM, bool FUSE, int... TI>

@@ -63,15 +63,22 @@ struct ConvShape {
 // model's pick per layer came closest to the fastest measured plan (summed
 // per-workload excess time 8.8% -> 4.8%; VGG-16 1.2% -> 0.5%).  128x32 keeps its
 // measured value: a lower one traded it for 32x128 on ResNet-50 layers where
-// interleaved re-timing showed 32x128 1-5% slower.
+// interleaved re-timing showed 32x128 1-5% slower.  The 16-row tile's eff was
+// fitted the same way after its plans were timed on those layers and on the
+// 48 channel scenes (IC, OC from 16 to 1024 at N=128): the model then gives
+// it exactly the K=16 layers (1.4-1.65x faster at N >= 32); with 48 output
+// channels the 32-row tiles measured faster.
+// m16: the tile runs on 16x16x4 fp32 MFMAs (16-row blocks; otherwise
+// 32x32x2) and stages its operands in the 16x16-block LDS layout.
 struct TileDesc {
   int mt, nt, kt, wm, wn;
   int regs;
   double eff;
+  int m16 = 0;
 };
 
 // The tile menu.  Every entry is instantiated for every loader variant.
-constexpr int kNumTiles = 13;
+constexpr int kNumTiles = 14;
 inline constexpr TileDesc kTiles[kNumTiles] = {
     {128, 128, 16, 2, 2, 108, 0.913},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
     {64, 256, 16, 1, 4, 112, 0.865},    // 1: four waves sharing one filter tile (TB(1,8)-like)
@@ -86,6 +93,7 @@ inline constexpr TileDesc kTiles[kNumTiles] = {
     {256, 128, 16, 4, 2, 104, 0.886},   // 10: eight waves
     {128, 256, 16, 2, 4, 104, 0.832},   // 11: eight waves
     {128, 128, 32, 2, 2, 124, 0.785},   // 12: deeper reduction step
+    {16, 64, 16, 1, 1, 88, 0.50, 1},    // 13: 16-row tile (16x16x4 MFMAs): 16 output channels
 };
 
 // LDS row strides (floats) of the staged operand tiles.  An MFMA fragment

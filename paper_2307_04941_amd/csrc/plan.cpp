@@ -42,7 +42,7 @@ constexpr double kUtilBase = 0.5, kUtilPerWave = 0.1;
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
 const TileDesc& tile_desc(bool acc64, int i) { return acc64 ? kTiles64[i] : kTiles[i]; }
-int lds_bytes(const TileDesc& t, bool acc64) { return acc64 ? lds_bytes_for64(t) : lds_bytes_for(t); }
+int lds_bytes(const TileDesc& t, bool acc64) { return (acc64 || t.m16) ? lds_bytes_for64(t) : lds_bytes_for(t); }
 
 // Work-groups of this tile resident on one CU, limited by LDS and registers.
 int resident_wgs(const TileDesc& t, bool acc64) {
@@ -368,8 +368,9 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     Plan c{};
     if (!shape_plan(s, acc64, ti, sched, sp, &c)) return;
     choose_modes(s, x16, w16, y16, &c);
-    // runs spanning two tiles need the kernel's loop over pieces
-    if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || !tail_runs_multi(c.b_mode))) return;
+    // runs spanning two tiles need the kernel's loop over pieces (only the
+    // 32x32x2 fp32 kernel with the one-tap HWCN loader has it)
+    if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || c.t.m16 || !tail_runs_multi(c.b_mode))) return;
     c.est_us = predict_us(s, c);
     // ties: less workspace traffic, then the larger tile
     const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
@@ -384,6 +385,9 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   for (int ti = 0; ti < (acc64 ? kNumTiles64 : kNumTiles); ++ti) {
     const TileDesc& td = tile_desc(acc64, ti);
     if (o.mt && !(td.mt == o.mt && td.nt == o.nt)) continue;
+    // The selector takes a 16-row tile only where it saves padding, i.e. a
+    // 32-row block would be at most half full (the case it was timed on).
+    if (!o.mt && td.m16 && !(s.Mg % 32 != 0 && s.Mg % 32 <= 16)) continue;
     // a forced tile without a depth means the default depth of 16
     if ((o.kt || o.mt) && td.kt != (o.kt ? o.kt : 16)) continue;
     if (o.split) {

@@ -160,7 +160,7 @@ def test_plans_for_every_catalogue_layer():
 def test_plans_random_grid_and_overrides():
     rng = np.random.Generator(np.random.PCG64(2))
     tiles = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x128", "32x64",
-             "128x32", "64x32", "256x128", "128x256", "128x128,kt=32"]
+             "128x32", "64x32", "256x128", "128x256", "128x128,kt=32", "16x64"]
     for _ in range(200):
         N = int(rng.integers(1, 65))
         C, K = (int(v) for v in rng.integers(1, 600, 2))
@@ -463,3 +463,19 @@ def test_injected_launch_failure(monkeypatch):
     assert "injected" in mg3m.mg3m_last_error()
     monkeypatch.setenv("MG3M_TEST_FAIL_LAUNCH", "0")
     assert lib.conv2d_fwd_f32_ex(X, Wp, Y, 0, *GOOD[1:], 0, None, 0, b"split=1", None) == 2
+
+
+def test_sixteen_row_tile_selection():
+    """The 16x16x4-MFMA tile (16x64) serves layers whose output channels would
+    leave a 32-row block at most half full; it takes split plans but no
+    stream-K runs; a forced 16x64 plan applies to any shape."""
+    k16 = mg3m.conv2d_fwd_f32_plan_info(128, 16, 56, 56, 16, 3, 3, 1, 1, "HWCN")
+    assert (k16["mt"], k16["nt"]) == (16, 64)
+    for K in (32, 64, 256):
+        p = mg3m.conv2d_fwd_f32_plan_info(4, 64, 14, 14, K, 3, 3, 1, 1, "HWCN")
+        assert p["mt"] != 16, K
+    forced = mg3m.conv2d_fwd_f32_plan_info(4, 64, 14, 14, 256, 3, 3, 1, 1, "HWCN", "tile=16x64,split=3")
+    assert (forced["mt"], forced["nt"], forced["split"]) == (16, 64, 3)
+    # 13 tail tiles of 36 k-tiles: 40 work-groups would cross tile boundaries
+    with pytest.raises(RuntimeError, match="MG3M_ERR_PLAN"):
+        mg3m.conv2d_fwd_f32_plan_info(4, 64, 14, 14, 16, 3, 3, 1, 1, "HWCN", "tile=16x64,sk=40")
