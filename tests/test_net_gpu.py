@@ -66,6 +66,8 @@ def _fused_ref(acc, mag, add, relu):
     (None, (4, 16, 12, 12, 32, 3, 3, 1, 1)),
     ("tile=128x128,split=3", (4, 16, 12, 12, 32, 3, 3, 1, 1)),      # finished in the split reduction
     (None, (1, 12, 9, 9, 24, 3, 3, 1, 1)),                           # N = 1: 16-byte channel stores
+    (None, (8, 16, 14, 14, 16, 3, 3, 1, 1)),                         # K = 16: 16x64 tile, 16x16x4 MFMAs
+    ("tile=16x64,split=3", (4, 16, 12, 12, 48, 3, 3, 1, 1)),        # 16x64 pieces, finished in the reduction
 ])
 def test_fused_add_relu(layout, plan, shape):
     import torch
