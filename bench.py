@@ -51,7 +51,8 @@ def kernel_name(plan) -> str:
     """The main kernel's symbol as rocprofv3 prints it (its template arguments:
     layout, filter loader, patch loader, tile rows, columns, depth, waves, and
     false for the plain output stage the benchmark uses)."""
-    return (f"void mg3m::conv_igemm_f32<{plan['layout']}, {plan['a_mode']}, {plan['b_mode']}, "
+    fn = "conv_igemm_f32_m16" if plan["mt"] == 16 else "conv_igemm_f32"   # 16-row tiles: 16x16x4 MFMAs
+    return (f"void mg3m::{fn}<{plan['layout']}, {plan['a_mode']}, {plan['b_mode']}, "
             f"{plan['mt']}, {plan['nt']}, {plan['kt']}, {plan['waves_m']}, {plan['waves_n']}, false>"
             f"(mg3m::KArgs)")
 

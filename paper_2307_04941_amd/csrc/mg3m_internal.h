@@ -269,8 +269,8 @@ int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S,
 
 // Shared by the C entry points and the network executor (abi.cpp): validate,
 // plan and launch one convolution (y = act(conv + add)).  own_workspace: take
-// a split plan's partials from hipMallocAsync on `stream` instead of
-// `workspace`.  Returns an mg3m_status and records the message for
+// a split plan's partials from the library's stream-ordered pool for the
+// stream's device (allocated and freed on `stream`) instead of `workspace`.  Returns an mg3m_status and records the message for
 // mg3m_last_error().
 int conv_run(const float* x, const float* w, float* y, const ConvGeom& g, void* workspace,
              size_t workspace_bytes, bool own_workspace, const char* plan, const float* add, int relu,
