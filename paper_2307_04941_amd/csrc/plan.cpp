@@ -54,13 +54,17 @@ int resident_wgs(const TileDesc& t, bool acc64) {
   return std::min(by_regs, by_lds);
 }
 
-// Relative speed of the loader variants against the tuned one.
+// Relative speed of the loader variants against the tuned one.  The NCHW
+// vec-K and element-wise factors were fitted to timings of every NCHW plan on
+// the VGG-16, ResNet-50 and AlexNet/inception layers (ResNet-50's NCHW excess
+// over the fastest plan per layer 9.2% -> 3.3%; its 7x7 stem 231 -> 146 us).
 double variant_factor(int variant) {
   switch (variant) {
     case kVarHwcnVecNTap: return 1.0;
     case kVarNchwTap: return 0.9;
+    case kVarNchwVecA: return 1.0;
     case kVarHwcnVecN: return 0.85;
-    case kVarHwcnVecC: case kVarHwcnVecA: case kVarNchwVecA: return 0.7;
+    case kVarHwcnVecC: case kVarHwcnVecA: case kVarNchwScalar: return 0.7;
     default: return 0.5;
   }
 }
