@@ -23,6 +23,13 @@ code and launches are unchanged).
 writes <out>/NAME_kernel_stats.txt only: the kernel-time table of any traced
 program (e.g. a network forward through the executor), with the time grouped
 by kernel family.
+
+    python -m paper_2307_04941_amd.rocprof_summary --mfma DIR --workload vgg16_n64 \
+        --bench-log FILE --out DIR --command-mfma "..."
+
+writes <out>/<kernel tag>_<workload>_mfma.txt: the dominant kernel's MFMA
+utilisation per launch from a ``rocprofv3 --pmc GRBM_GUI_ACTIVE
+SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES`` run, and its HBM GB/s.
 """
 from __future__ import annotations
 
@@ -109,11 +116,69 @@ def stats_only(a):
     return 0
 
 
+def mfma_summary(a):
+    """MFMA utilisation of the dominant kernel from a ``rocprofv3 --pmc
+    GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES`` run: per
+    launch, MFMA-busy SIMD cycles over the SIMD cycles the GPU clocked while
+    the kernel ran (the counters are summed over the XCDs), the effective
+    clock, and the HBM bytes of the traffic summary over the launch time."""
+    with open(a.bench_log) as f:
+        bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
+    kernel = bench["roofline"]["kernel"]
+    agent = next(r for r in _csv(a.mfma, "agent_info.csv") if int(r.get("Simd_Count") or 0) > 0)
+    xcc, simds = int(agent["Num_Xcc"]), int(agent["Simd_Count"])
+    clk_max = float(agent["Max_Engine_Clk_Fcompute"]) * 1e6
+    acc = {}
+    for r in _csv(a.mfma, "counter_collection.csv"):
+        if r["Kernel_Name"] != kernel:
+            continue
+        d = acc.setdefault(int(r["Dispatch_Id"]), {"ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    if not acc:
+        raise ValueError(f"no dispatch of {kernel} in {a.mfma}")
+    traffic = None
+    tpath = os.path.join(a.out, f"traffic_{a.workload}.json")
+    if os.path.exists(tpath):
+        with open(tpath) as f:
+            t = json.load(f)
+        if t.get("kernel") == kernel:
+            traffic = t["hbm_bytes_per_launch"]
+    args = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").split(",")
+    tag = "conv_igemm_" + "_".join(v for v in args if v.lstrip("-").isdigit())
+    lines = [f"MFMA utilisation of {kernel}, workload {a.workload}",
+             f"command: {a.command_mfma}", "",
+             f"GPU: {xcc} XCDs, {simds} SIMDs, {clk_max / 1e9:.2f} GHz maximum engine clock",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / XCDs x SIMDs); "
+             "clock = GRBM_GUI_ACTIVE / XCDs / kernel time", "",
+             f"{'dispatch':>8} {'us':>9} {'clock GHz':>10} {'MFMA busy':>10} {'x clock/max':>12}"]
+    tot_busy = tot_cyc = tot_ns = 0.0
+    for d, v in sorted(acc.items()):
+        cyc = v["GRBM_GUI_ACTIVE"] / xcc
+        busy = v["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * simds)
+        clk = cyc / (v["ns"] * 1e-9)
+        lines.append(f"{d:8d} {v['ns'] / 1e3:9.1f} {clk / 1e9:10.3f} {100 * busy:9.1f}% {100 * busy * clk / clk_max:11.1f}%")
+        tot_busy += v["SQ_VALU_MFMA_BUSY_CYCLES"]; tot_cyc += cyc; tot_ns += v["ns"]
+    busy = tot_busy / (tot_cyc * simds)
+    clk = tot_cyc / (tot_ns * 1e-9)
+    lines += ["", f"all {len(acc)} dispatches: MFMA busy {100 * busy:.1f}% of the clocked SIMD cycles at "
+              f"{clk / 1e9:.3f} GHz on average = {100 * busy * clk / clk_max:.1f}% of the MFMA cycles at "
+              f"{clk_max / 1e9:.2f} GHz (the fp32 MFMA peak's clock)"]
+    if traffic is not None:
+        gbs = traffic / (tot_ns / len(acc) * 1e-9) / 1e9
+        lines.append(f"HBM traffic {traffic / 1e6:.1f} MB per launch (traffic_{a.workload}.json) over the "
+                     f"mean launch time here: {gbs:.0f} GB/s = {100 * gbs / 8000:.1f}% of the 8.0 TB/s HBM peak "
+                     f"(counter runs serialise dispatches; the benchmark's own launches run faster)")
+    with open(os.path.join(a.out, f"{tag}_{a.workload}_mfma.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[-3:]))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--stats-only", default=None, metavar="NAME")
     ap.add_argument("--workload")
-    ap.add_argument("--trace", required=True)
+    ap.add_argument("--trace")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--bench-log")
@@ -122,9 +187,17 @@ def main(argv=None):
     ap.add_argument("--command-trace", default="")
     ap.add_argument("--command-fetch", default="")
     ap.add_argument("--command-write", default="")
+    ap.add_argument("--mfma", default=None, metavar="DIR",
+                    help="rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES ... directory: "
+                         "write <kernel>_<workload>_mfma.txt (needs --workload, --bench-log)")
+    ap.add_argument("--command-mfma", default="")
     a = ap.parse_args(argv)
     if a.stats_only:
         return stats_only(a)
+    if a.mfma:
+        return mfma_summary(a)
+    if a.trace is None:
+        ap.error("--trace is required without --mfma")
     for need in ("workload", "fetch", "write", "bench_log", "copy_mib"):
         if getattr(a, need) is None:
             ap.error(f"--{need.replace('_', '-')} is required without --stats-only")
