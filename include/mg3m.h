@@ -107,8 +107,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  * override.  Override syntax: comma-separated key=value pairs,
  *   tile=<MT>x<NT>   one of the kernel tile shapes: 128x128, 64x256, 256x64,
  *                    64x128, 128x64, 64x64, 32x128, 32x64, 128x32, 64x32,
- *                    256x128, 128x256, 128x128 with kt=32, and 16x64 (16x16x4
- *                    MFMAs; the selector takes it only when K mod 32 is 1..16)
+ *                    256x128, 128x256, 128x128 with kt=32, 16x64 (16x16x4
+ *                    MFMAs; the selector takes it only when K mod 32 is 1..16),
+ *                    and 64x64 with kt=32 (four 32x32 waves; reached only
+ *                    through this override, never by the selector)
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
  *   split=<n>        share every tile's reduction out over n work-groups per tile
  *                    (1..64, clamped to the tile's k-tiles; 1 = no split)

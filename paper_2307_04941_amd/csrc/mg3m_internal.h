@@ -75,10 +75,11 @@ struct TileDesc {
   int regs;
   double eff;
   int m16 = 0;
+  int forced_only = 0;   // reached only through a plan override, never by the selector
 };
 
 // The tile menu.  Every entry is instantiated for every loader variant.
-constexpr int kNumTiles = 14;
+constexpr int kNumTiles = 15;
 inline constexpr TileDesc kTiles[kNumTiles] = {
     {128, 128, 16, 2, 2, 108, 0.913},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
     {64, 256, 16, 1, 4, 112, 0.865},    // 1: four waves sharing one filter tile (TB(1,8)-like)
@@ -94,6 +95,7 @@ inline constexpr TileDesc kTiles[kNumTiles] = {
     {128, 256, 16, 2, 4, 104, 0.832},   // 11: eight waves
     {128, 128, 32, 2, 2, 124, 0.785},   // 12: deeper reduction step
     {16, 64, 16, 1, 1, 88, 0.50, 1},    // 13: 16-row tile (16x16x4 MFMAs): 16 output channels
+    {64, 64, 32, 2, 2, 88, 0.78, 0, 1}, // 14: four 32x32 waves, deep step (override only)
 };
 
 // LDS row strides (floats) of the staged operand tiles.  An MFMA fragment

@@ -392,6 +392,8 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     // The selector takes a 16-row tile only where it saves padding, i.e. a
     // 32-row block would be at most half full (the case it was timed on).
     if (!o.mt && td.m16 && !(s.Mg % 32 != 0 && s.Mg % 32 <= 16)) continue;
+    // A tile the cost model does not yet rank correctly is left to overrides.
+    if (!o.mt && td.forced_only) continue;
     // a forced tile without a depth means the default depth of 16
     if ((o.kt || o.mt) && td.kt != (o.kt ? o.kt : 16)) continue;
     if (o.split) {

@@ -13,7 +13,7 @@ from tests.gpu_util import assert_parity, make, run_gpu, say, to_dev
 pytestmark = pytest.mark.gpu
 
 TILES = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x128", "32x64",
-         "128x32", "64x32", "256x128", "128x256", "128x128,kt=32", "16x64"]
+         "128x32", "64x32", "256x128", "128x256", "128x128,kt=32", "16x64", "64x64,kt=32"]
 
 
 def _small_grid():
