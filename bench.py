@@ -114,6 +114,9 @@ def main():
     ap.add_argument("--workload", default="vgg16_n64")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU work budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--layers", default=None,
+                    help="comma-separated layer names of the workload to run (default: all); "
+                         "for profiling single layers")
     ap.add_argument("--plan", default=None, help="plan override for every layer (diagnostics)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the warm-up, copy a buffer of this many MiB once (a plain copy "
@@ -135,10 +138,18 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     layers_def = workloads.workload(args.workload)
+    if args.layers:
+        want = args.layers.split(",")
+        unknown = [n for n in want if n not in {L.name for L in layers_def}]
+        if unknown:
+            print(f"unknown layer(s) {unknown} in workload {args.workload}", file=sys.stderr)
+            sys.exit(2)
+    # the seeds follow each layer's place in the whole workload
+    chosen = [(i, L) for i, L in enumerate(layers_def) if not args.layers or L.name in args.layers.split(",")]
 
     # ---- inputs: seeded, generated on the host, resident in HBM before timing
     layers, tensors, dev_bufs = [], [], []
-    for i, L in enumerate(layers_def):
+    for i, L in chosen:
         sx, sw = workloads.seeds(args.workload, i)
         x, w = workloads.make_tensors(L, sx, sw, "HWCN")
         Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)

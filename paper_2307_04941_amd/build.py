@@ -49,6 +49,12 @@ def _compile(src: str, obj: str, extra=()):
 
 LLVM_BIN = "/opt/rocm/llvm/bin"
 DIGESTS = os.path.join(PKG, "kernel_digests.json")
+# Per kernel (demangled name): registers and LDS as the gfx950 code object's
+# metadata states them.  vgpr_count is the whole per-lane register file a wave
+# takes (arch VGPRs rounded up to 4, then AGPRs), agpr_count the AGPR part.
+RESOURCES = os.path.join(PKG, "kernel_resources.json")
+_RESOURCE_KEYS = {".vgpr_count": "vgpr_count", ".agpr_count": "agpr_count", ".sgpr_count": "sgpr_count",
+                  ".group_segment_fixed_size": "lds_bytes", ".private_segment_fixed_size": "scratch_bytes"}
 
 
 def _device_code_object(obj: str, tmp: str) -> str:
@@ -63,9 +69,10 @@ def _device_code_object(obj: str, tmp: str) -> str:
     return co
 
 
-def _kernel_digests(co: str) -> dict:
+def _kernel_digests(co: str, resources: dict) -> dict:
     """Per kernel (mangled name): sha256 of its instructions (addresses and
-    encodings dropped) and of its resource metadata (registers, LDS, ...)."""
+    encodings dropped) and of its resource metadata (registers, LDS, ...).
+    Also fills resources[mangled name] from that metadata."""
     dis = subprocess.run([f"{LLVM_BIN}/llvm-objdump", "-d", "--no-show-raw-insn", "--no-leading-addr", co],
                          check=True, capture_output=True, text=True).stdout
     code, name = {}, None
@@ -89,9 +96,14 @@ def _kernel_digests(co: str) -> dict:
     if block:
         meta.update(_meta_block(block))
     for k, block in meta.items():
+        res = {}
         for line in block:
+            key, _, val = line.partition(":")
+            if key in _RESOURCE_KEYS:
+                res[_RESOURCE_KEYS[key]] = int(val)
             if line.startswith(".private_segment_fixed_size:") and int(line.split(":")[1]) != 0:
                 raise RuntimeError(f"kernel {k} uses scratch memory ({line}); keep it in registers")
+        resources[k] = res
     out = {}
     for k, lines in code.items():
         h = hashlib.sha256("\n".join(lines).encode() + b"\0" + "\n".join(meta.get(k, [])).encode())
@@ -107,18 +119,21 @@ def _meta_block(block):
 def write_kernel_digests(objs, tmp) -> dict:
     """kernel_digests.json: demangled kernel name (as rocprofv3 prints it) ->
     digest of its machine code, so that a profile taken on a kernel is reused
-    exactly as long as that kernel's code is unchanged."""
-    digests = {}
+    exactly as long as that kernel's code is unchanged.  kernel_resources.json:
+    demangled name -> its registers and LDS (the planner's occupancy model is
+    checked against these)."""
+    digests, resources = {}, {}
     for obj in objs:
         if obj.endswith(".hip.o"):
-            digests.update(_kernel_digests(_device_code_object(obj, tmp)))
+            digests.update(_kernel_digests(_device_code_object(obj, tmp), resources))
     names = sorted(digests)
     dem = subprocess.run(["c++filt"], input="\n".join(names), capture_output=True, text=True,
                          check=True).stdout.splitlines()
     table = {d: digests[n] for n, d in zip(names, dem)}
-    with open(DIGESTS + ".tmp", "w") as f:
-        json.dump(table, f, indent=0, sort_keys=True)
-    os.replace(DIGESTS + ".tmp", DIGESTS)
+    for path, obj in ((DIGESTS, table), (RESOURCES, {d: resources.get(n, {}) for n, d in zip(names, dem)})):
+        with open(path + ".tmp", "w") as f:
+            json.dump(obj, f, indent=0, sort_keys=True)
+        os.replace(path + ".tmp", path)
     return table
 
 

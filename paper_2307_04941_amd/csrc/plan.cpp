@@ -100,8 +100,17 @@ int parse_override(const char* text, Override* o, std::string* err) {
         *err = "plan override: tile must be <MT>x<NT>";
         return MG3M_ERR_PLAN;
       }
-      o->mt = (int)std::strtol(val.substr(0, x).c_str(), &tail, 10);
-      o->nt = (int)std::strtol(val.substr(x + 1).c_str(), &tail, 10);
+      // each half must be a whole decimal number (so "64x64;kt=32" is rejected,
+      // not read as 64x64 with the default depth)
+      auto whole = [](const std::string& t, long* v) {
+        char* e = nullptr;
+        *v = std::strtol(t.c_str(), &e, 10);
+        return !t.empty() && e == t.c_str() + t.size();
+      };
+      long mt = 0, nt = 0;
+      const bool ok = whole(val.substr(0, x), &mt) && whole(val.substr(x + 1), &nt);
+      o->mt = ok && mt <= 4096 ? (int)mt : 0;
+      o->nt = ok && nt <= 4096 ? (int)nt : 0;
       if (o->mt <= 0 || o->nt <= 0) {
         *err = "plan override: bad tile '" + val + "'";
         return MG3M_ERR_PLAN;

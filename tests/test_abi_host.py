@@ -479,3 +479,17 @@ def test_sixteen_row_tile_selection():
     # 13 tail tiles of 36 k-tiles: 40 work-groups would cross tile boundaries
     with pytest.raises(RuntimeError, match="MG3M_ERR_PLAN"):
         mg3m.conv2d_fwd_f32_plan_info(4, 64, 14, 14, 16, 3, 3, 1, 1, "HWCN", "tile=16x64,sk=40")
+
+
+@pytest.mark.parametrize("bad", ["tile=64x64;kt=32", "tile=64x", "tile=x64", "tile=64x64x", "tile=6 4x64",
+                                 "tile=64x64 ", "tile=0x64", "tile=-64x64", "tile=64x99999999999"])
+def test_override_tile_halves_must_be_whole_numbers(bad):
+    """Both halves of tile=<MT>x<NT> must be whole decimal numbers: a stray
+    separator (';' for ',') must not be read as a tile with the default
+    depth."""
+    with pytest.raises(mg3m.Mg3mError) as ei:
+        mg3m.conv2d_fwd_f32_plan_info(32, 512, 7, 7, 2048, 1, 1, 1, 0, "HWCN", bad)
+    assert ei.value.status == 7, bad
+    # the well-formed spelling of the same request is accepted
+    p = mg3m.conv2d_fwd_f32_plan_info(32, 512, 7, 7, 2048, 1, 1, 1, 0, "HWCN", "tile=64x64,kt=32")
+    assert (p["mt"], p["nt"], p["kt"]) == (64, 64, 32)

@@ -69,6 +69,45 @@ def test_every_tile_and_split(tile, mode):
         assert_parity(y, acc, mag, f"{shape} {plan}")
 
 
+# The tuned HWCN loader (one filter tap per staged slab: N % 4 == 0 and C a
+# multiple of every tile's kt, 16 and 32): a ragged 3x3 shape and a 1x1 shape
+# (every GEMM dimension has a tail), and a shape with more tiles than one
+# round of resident work-groups of any tile, so that tail=3 leaves whole
+# tiles and split tail tiles in one launch.  Integer data: exact.
+TAP_SHAPES = [(4, 64, 13, 11, 68, 3, 3, 1, 1), (4, 64, 9, 7, 68, 1, 1, 1, 0)]
+TAP_HYBRID = (32, 32, 95, 95, 64, 3, 3, 1, 1)
+_oracle_cache = {}
+
+
+def _int_case(shape, seed):
+    key = (shape, seed)
+    if key not in _oracle_cache:
+        x, w, st, pd = make(shape, seed, "HWCN", dist="int")
+        acc, _ = oracle.conv2d(x, w, st, pd, "HWCN")
+        _oracle_cache[key] = (x, w, st, pd, acc.astype(np.float32))
+    return _oracle_cache[key]
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_every_tile_vec_n_tap(tile):
+    for si, shape in enumerate(TAP_SHAPES):
+        x, w, st, pd, exact = _int_case(shape, 90 + si)
+        for split in (1, 2, 5):
+            plan = f"tile={tile},split={split}"
+            info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
+            assert info["b_mode"] == 3, info
+            say(f"forced vec_n_tap {plan} shape={shape}")
+            y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+            assert np.array_equal(y, exact), f"{shape} {plan}: not bit-exact"
+    x, w, st, pd, exact = _int_case(TAP_HYBRID, 95)
+    plan = f"tile={tile},tail=3"
+    info = mg3m.conv2d_fwd_f32_plan_info(*TAP_HYBRID, "HWCN", plan)
+    assert info["b_mode"] == 3 and info["dp_tiles"] > 0 and info["tail_tiles"] > 0, info
+    say(f"forced vec_n_tap hybrid {plan}: dp_tiles {info['dp_tiles']} tail_tiles {info['tail_tiles']}")
+    y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+    assert np.array_equal(y, exact), f"{TAP_HYBRID} {plan}: not bit-exact"
+
+
 @pytest.mark.parametrize("tile", TILES)
 def test_every_tile_nchw_tap_major(tile):
     """NCHW with C a multiple of kt: the filter is copied to [R][S][C][K] in
