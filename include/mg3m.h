@@ -327,6 +327,27 @@ const char *mg3m_status_string(int status);
 /* Detail of the last error on the calling host thread ("" if none). */
 const char *mg3m_last_error(void);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * convolution as conv2d_fwd_f32 (same arguments, layouts, validation and
+ * errors), but it allocates nothing: a plan's workspace (split-K partials,
+ * the [R][S][C][K] filter copy of tap-major NCHW plans) lives in a fixed
+ * device array of MG3M_NOALLOC_SCRATCH_BYTES that each device holds from the
+ * first such call on it (the array's address is looked up then) until the
+ * process ends.  The selector only considers plans whose workspace fits, so
+ * a plan may differ from conv2d_fwd_f32's (results then differ by rounding
+ * only, and agree exactly on small-integer data).  No plan fits only when a
+ * tap-major NCHW filter copy alone exceeds the array: MG3M_ERR_WORKSPACE,
+ * with nothing launched.  Nothing in the array needs clearing: every value a
+ * call reads there was written earlier by the same call.  All calls on one
+ * device share its array, so calls that may overlap in time on one device
+ * (other streams, other host threads) race and must be ordered by the
+ * caller; calls on one stream are ordered already. */
+#define MG3M_NOALLOC_SCRATCH_BYTES (128ull * 1024ull * 1024ull)
+int conv2d_fwd_f32_noalloc(const float *x, const float *w, float *y,
+                           int N, int C, int H, int W, int K, int R, int S,
+                           int stride, int pad, int layout, void *stream);
+
 /* The workspaces that conv2d_fwd_f32 and conv2d_fwd_f32_acc64 take for
  * themselves come from one stream-ordered memory pool per device, which the library creates at the first such call
  * on that device.  Freed blocks stay in the pool for the next call (mapping

@@ -47,7 +47,7 @@ Geom geom(int N, int C, int H, int W, int K, int R, int S, int sh, int sw, int p
 // small layers of a network is as long as the kernel.  Bounded; cleared when
 // full.  Guarded by a mutex: calls may come from several host threads.
 struct PlanKey {
-  int v[14];
+  int v[16];
   std::string override_text;
   bool operator==(const PlanKey& o) const {
     return std::memcmp(v, o.v, sizeof v) == 0 && override_text == o.override_text;
@@ -73,7 +73,8 @@ constexpr size_t kPlanCacheMax = 4096;
 int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16,
                    mg3m::ConvShape* s, mg3m::Plan* p) {
   PlanKey key{{g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout,
-               (g.acc64 ? 1 : 0), (x16 ? 4 : 0) | (w16 ? 2 : 0) | (y16 ? 1 : 0)},
+               (g.acc64 ? 1 : 0), (x16 ? 4 : 0) | (w16 ? 2 : 0) | (y16 ? 1 : 0),
+               (int)(uint32_t)((uint64_t)g.ws_cap >> 32), (int)(uint32_t)g.ws_cap},
               plan ? std::string(plan) : std::string("\x01")};
   PlanCache& cache = plan_cache();
   {
@@ -88,7 +89,7 @@ int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16
   std::string err;
   int rc = mg3m::make_shape(g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout, s, &err);
   if (rc) return fail(rc, err);
-  rc = mg3m::make_plan(*s, plan, g.acc64, x16, w16, y16, p, &err);
+  rc = mg3m::make_plan(*s, plan, g.acc64, x16, w16, y16, p, &err, g.ws_cap);
   if (rc) return fail(rc, err);
   std::lock_guard<std::mutex> lock(cache.mu);
   if (cache.map.size() >= kPlanCacheMax) cache.map.clear();

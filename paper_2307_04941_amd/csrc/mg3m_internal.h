@@ -227,14 +227,17 @@ struct ConvGeom {
   int sh, sw, ph, pw;
   int layout;
   bool acc64;
+  size_t ws_cap = SIZE_MAX;   // largest workspace a plan may use (the no-allocation entry point's scratch)
 };
 
 // Planner (host only, no HIP calls).  Returns 0 or an mg3m_status code and
 // fills *err with a message on failure.
 int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride_h, int stride_w,
                int pad_h, int pad_w, int layout, ConvShape* s, std::string* err);
+// ws_cap: only plans whose workspace fits are considered; when none does,
+// MG3M_ERR_WORKSPACE.
 int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x16, bool w16,
-              bool y16, Plan* p, std::string* err);
+              bool y16, Plan* p, std::string* err, size_t ws_cap = SIZE_MAX);
 std::string plan_to_string(const ConvShape& s, const Plan& p);
 
 // Whether the fp32 kernel of a patch loader runs stream-K tail plans (runs

@@ -364,7 +364,7 @@ void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
 }
 
 int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x16, bool w16,
-              bool y16, Plan* p, std::string* err) {
+              bool y16, Plan* p, std::string* err, size_t ws_cap) {
   Override o;
   int rc = parse_override(override_text, &o, err);
   if (rc) return rc;
@@ -375,6 +375,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
 
   int best = -1;
   Plan best_plan{};
+  size_t least_over_cap = SIZE_MAX;     // smallest workspace among the candidates over ws_cap
   // the split factors the cost model was calibrated on
   const int splits[] = {2, 3, 4, 6, 8, 16};
   auto consider = [&](int ti, int sched, long long sp) {
@@ -384,6 +385,10 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     // runs spanning two tiles need the kernel's loop over pieces (only the
     // 32x32x2 fp32 kernel with the one-tap HWCN loader has it)
     if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || c.t.m16 || !tail_runs_multi(c.b_mode))) return;
+    if (c.ws_bytes > ws_cap) {
+      least_over_cap = std::min(least_over_cap, c.ws_bytes);
+      return;
+    }
     c.est_us = predict_us(s, c);
     // ties: less workspace traffic, then the larger tile
     const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
@@ -420,6 +425,11 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       // stream-K over the left-over tiles with one to all resident work-groups per CU
       for (int j = 1, occ = resident_wgs(td, acc64); j <= occ; ++j) consider(ti, kStreamK, (long long)j * kCUs);
     }
+  }
+  if (best < 0 && least_over_cap != SIZE_MAX) {
+    *err = "every applicable plan needs more workspace than the " + std::to_string(ws_cap) +
+           " bytes available (the smallest needs " + std::to_string(least_over_cap) + ")";
+    return MG3M_ERR_WORKSPACE;
   }
   if (best < 0) {
     *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +

@@ -101,6 +101,7 @@ def load_library(path: str = LIB_PATH):
     lib.mg3m_net_destroy.argtypes = [p]
     lib.conv2d_fwd_f32_acc64_plan_string.argtypes = shape_hw + [cp, ctypes.c_char_p, sz]
     lib.conv2d_fwd_f32.argtypes = [p, p, p] + shape + [p]
+    lib.conv2d_fwd_f32_noalloc.argtypes = [p, p, p] + shape + [p]
     lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
     lib.conv2d_fwd_f32_workspace_bytes.argtypes = shape + [cp, ctypes.POINTER(sz)]
     lib.conv2d_fwd_f32_plan_string.argtypes = shape + [cp, ctypes.c_char_p, sz]
@@ -345,6 +346,11 @@ def _device_view(addr, n, torch):
 def conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):
     _check(load_library().conv2d_fwd_f32(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
                                          stride, pad, _layout(layout), _stream(stream)))
+
+
+def conv2d_fwd_f32_noalloc(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):
+    _check(load_library().conv2d_fwd_f32_noalloc(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
+                                                 stride, pad, _layout(layout), _stream(stream)))
 
 
 def conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, stride, pad, layout,

@@ -493,3 +493,19 @@ def test_override_tile_halves_must_be_whole_numbers(bad):
     # the well-formed spelling of the same request is accepted
     p = mg3m.conv2d_fwd_f32_plan_info(32, 512, 7, 7, 2048, 1, 1, 1, 0, "HWCN", "tile=64x64,kt=32")
     assert (p["mt"], p["nt"], p["kt"]) == (64, 64, 32)
+
+
+def test_noalloc_validation_before_any_device_call():
+    """conv2d_fwd_f32_noalloc validates pointers and shape, and rejects a
+    shape whose every plan needs more workspace than its fixed scratch array
+    (a tap-major NCHW filter copy of 151 MB against 128 MiB), before it
+    looks the array up: these calls need no GPU."""
+    lib = mg3m.load_library()
+    shape = (1, 1024, 3, 3, 4096, 3, 3, 1, 1)
+    assert lib.conv2d_fwd_f32_noalloc(None, Wp, Y, *shape, 1, None) == 1
+    assert lib.conv2d_fwd_f32_noalloc(X + 2, Wp, Y, *shape, 1, None) == 9
+    assert lib.conv2d_fwd_f32_noalloc(X, Wp, Y, *shape, 5, None) == 3
+    assert lib.conv2d_fwd_f32_noalloc(X, Wp, Y, 1, 1, 2, 2, 1, 5, 5, 1, 0, 0, None) == 2
+    assert lib.conv2d_fwd_f32_noalloc(X, Wp, Y, *shape, 1, None) == 6
+    msg = mg3m.mg3m_last_error()
+    assert "134217728" in msg and "150994944" in msg, msg
