@@ -116,6 +116,11 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    (1..64, clamped to the tile's k-tiles; 1 = no split)
  *   tail=<n>         the same for the tiles left over after whole rounds of resident
  *                    work-groups only (2..64); the other tiles run whole
+ *   persist=<w>      every tile whole, computed by min(tiles, 256*w) work-groups that
+ *                    each loop over tiles (1..16); the next tile's first loads and
+ *                    MFMAs overlap the previous tile's output stores.  HWCN with the
+ *                    batch-vector patch loaders (N and K multiples of 4, aligned
+ *                    buffers) and 32x32x2-MFMA tiles only, else MG3M_ERR_PLAN
  *   sk=<g>           the left-over tiles' k-tiles dealt out to g work-groups in equal
  *                    runs (stream-K); g from the number of left-over tiles to their
  *                    k-tiles in total, else MG3M_ERR_PLAN.  Runs that span two tiles
@@ -124,7 +129,8 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    32x32x2-MFMA tile (not 16x64); other
  *                    shapes accept only g that cuts every left-over tile into equal
  *                    runs (a split), else MG3M_ERR_PLAN
- * e.g. "tile=128x128,kt=32,split=2".  Unknown keys or shapes -> MG3M_ERR_PLAN. */
+ * e.g. "tile=128x128,kt=32,split=2".  At most one of split, tail, sk and persist.
+ * Unknown keys or shapes -> MG3M_ERR_PLAN. */
 int conv2d_fwd_f32_ex(const float *x, const float *w, float *y,
                       int N, int C, int H, int W, int K, int R, int S,
                       int stride, int pad, int layout,
@@ -295,6 +301,7 @@ typedef struct mg3m_plan_info {
     int layout;               /* MG3M_LAYOUT_* */
     int a_mode, b_mode;       /* operand loader variant of the main kernel (its template arguments) */
     int e_mode;               /* epilogue store mode */
+    int persistent;           /* 1: grid work-groups loop over the dp_tiles whole tiles */
 } mg3m_plan_info;
 
 int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,

@@ -197,7 +197,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   float* const part = ws != nullptr ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.wt_bytes) : nullptr;
   mg3m::KArgs a{};
   a.x = x; a.w = wt != nullptr ? wt : w; a.y = y; a.ws = part;
-  a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb;
+  a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb; a.y_bytes = (unsigned)yb;
   a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
   a.Mg = (int)s.Mg; a.Ng = (int)s.Ng; a.Kg = (int)s.Kg;
@@ -489,6 +489,7 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     info->pad_efficiency = p.pad_eff; info->est_us = p.est_us;
     info->layout = p.layout; info->a_mode = p.a_mode; info->b_mode = p.b_mode;
     info->e_mode = p.e_mode;
+    info->persistent = p.persist;
     return MG3M_OK;
   } catch (...) {
     return fail(MG3M_ERR_HIP, "unknown exception");

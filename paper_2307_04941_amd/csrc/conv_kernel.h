@@ -1069,6 +1069,46 @@ __device__ __forceinline__ void tail_runs_f32(const KArgs& a, float* lds, int la
   }
 }
 
+// Epilogue of a whole tile, straight from the accumulators into y (with the
+// fused output stage when FUSE).  32x32 accumulator layout: register e of
+// lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
+template <int LAYOUT, class C, bool FUSE>
+__device__ __forceinline__ void store_tile_f32(const KArgs& a, floatx16 (&acc)[C::TM][C::TN], int m0, int n0,
+                                               int wm, int wn, int hh, int q) {
+  float* const out = a.y;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int n = n0 + wn * C::WTN + j * 32 + q;
+    if (n >= a.Ng) continue;
+    const int colbase = out_colbase<LAYOUT>(a, n);
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
+        if (a.e_mode == kEVecM) {
+          // four consecutive output channels, contiguous when mstride == 1
+          if (row0 < a.Mg) {
+            f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+            if constexpr (FUSE) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
+            }
+            st4(out + colbase + row0, v);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (row0 + e < a.Mg) {
+              const int idx = colbase + (row0 + e) * a.mstride;
+              if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][4 * g + e], idx);
+              else out[idx] = acc[i][j][4 * g + e];
+            }
+        }
+      }
+  }
+}
+
 // Work-groups [0, dp_tiles) compute whole tiles (tile xcd_group(i)) over
 // the full reduction and store them to y; the work-groups after them run the
 // tail (tail_runs_f32) in the same launch, starting as the last round of
@@ -1093,41 +1133,221 @@ void conv_igemm_f32(KArgs a) {
   tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
       a, lds, threadIdx.x, tile, 0, a.k_tiles,
       [&](floatx16 (&acc)[C::TM][C::TN], int m0, int n0, int wm, int wn, int hh, int q) {
-        // Epilogue, straight from the accumulators.  32x32 accumulator layout:
-        // register e of lane (hh, q) holds row 8*(e/4) + 4*hh + e%4, column q.
-        float* const out = a.y;
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j) {
-          const int n = n0 + wn * C::WTN + j * 32 + q;
-          if (n >= a.Ng) continue;
-          const int colbase = out_colbase<LAYOUT>(a, n);
-#pragma unroll
-          for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const int row0 = m0 + wm * C::WTM + i * 32 + 8 * g + 4 * hh;
-              if (a.e_mode == kEVecM) {
-                // four consecutive output channels, contiguous when mstride == 1
-                if (row0 < a.Mg) {
-                  f32x4 v{acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
-                  if constexpr (FUSE) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = finish1(a, v[e], colbase + row0 + e);
-                  }
-                  st4(out + colbase + row0, v);
-                }
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  if (row0 + e < a.Mg) {
-                    const int idx = colbase + (row0 + e) * a.mstride;
-                    if constexpr (FUSE) out[idx] = finish1(a, acc[i][j][4 * g + e], idx);
-                    else out[idx] = acc[i][j][4 * g + e];
-                  }
-              }
-            }
-        }
+        store_tile_f32<LAYOUT, C, FUSE>(a, acc, m0, n0, wm, wn, hh, q);
       });
+}
+
+// ------------------------------------------------- persistent whole tiles
+// mma_stage over the first nkk k-pairs of a stage only (rows 2*nkk and up are
+// past Kg: their zero-filled products are skipped, not computed).
+template <class C, int KT>
+__device__ __forceinline__ void mma_stage_upto(floatx16 (&acc)[C::TM][C::TN], const float* As,
+                                               const float* Bs, int wm, int wn, int hh, int q, int nkk) {
+  int ca[C::TM], cb[C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i) ca[i] = hh * C::AS + C::LA::col(hh, wm * C::WTM + i * 32) + q;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) cb[j] = hh * C::BS + C::LB::col(hh, wn * C::WTN + j * 32) + q;
+#pragma unroll
+  for (int kk = 0; kk < KT / 2; ++kk) {
+    if (kk < nkk) {   // uniform: a scalar branch per k-pair
+      float av[C::TM], bv[C::TN];
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) av[i] = As[ca[i] + 2 * kk * C::AS];
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) bv[j] = Bs[cb[j] + 2 * kk * C::BS];
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// Epilogue of a whole tile through a buffer resource on y, element stores
+// (the layouts where output channel m and m+1 are mstride apart, any
+// mstride): a per-lane base offset per 32-column block plus the row's part,
+// and elements outside the output sent to the out-of-range offset (with a
+// zero scalar offset, as the loaders do), which the buffer hardware drops --
+// no branches and no 64-bit address per store.
+template <int LAYOUT, class C>
+__device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&acc)[C::TM][C::TN], int m0, int n0,
+                                                   int wm, int wn, int hh, int q) {
+  const __amdgpu_buffer_rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+  // opaque here, so that the row offsets below are formed where the stores
+  // use them (hoisted out of the persistent kernel's loop over tiles, their
+  // products spilled scalar registers)
+  unsigned rs4 = 4u * (unsigned)a.mstride;
+  asm volatile("" : "+s"(rs4));
+  const int row_l = m0 + wm * C::WTM + 4 * hh;      // lane's first row
+  const int rows_left = a.Mg - row_l;                // rows r of the wave tile with r < rows_left exist
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int n = n0 + wn * C::WTN + j * 32 + q;
+    const bool col_ok = n < a.Ng;
+    const unsigned voff = 4u * (unsigned)(out_colbase<LAYOUT>(a, n) + row_l * a.mstride);
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const unsigned o = voff + (unsigned)(i * 32 + 8 * g) * rs4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = i * 32 + 8 * g + e;         // row offset from the lane's first row
+          bstore1(yr, (col_ok & (r < rows_left)) ? o + (unsigned)e * rs4 : kOOB, 0u, acc[i][j][4 * g + e]);
+        }
+      }
+  }
+}
+
+// Persistent whole tiles, for layers whose reduction is only a few stages
+// deep (the three-channel stems: Kg = 27 for a 3x3 filter): there a
+// work-group's life is a stage or two of MFMAs and then a burst of output
+// stores, and work-groups that start together compute together and store
+// together, so the chip alternates between the two instead of overlapping
+// them.  Here gridDim.x work-groups each take tiles slot, slot + G, slot +
+// 2G, ... (G = gridDim.x, slot = xcd_group(blockIdx.x, G): every XCD takes a
+// contiguous block of each G consecutive tiles), and the stages of all of a
+// work-group's tiles form one pipeline, one stage's loads in flight while
+// the previous stage's MFMAs run; the last stage of a tile loads the first
+// stage of the next one.  A tile's output stores are issued one stage later,
+// right after the loads of the next tile's second stage (or of the tile after
+// it when a tile has one stage): the memory counter a wave waits on before it
+// stages its loads counts stores too, in issue order, so stores issued after
+// those loads do not hold up that wait, and a whole stage of MFMAs passes
+// before a later wait needs them finished.  The last stage of each tile
+// computes only the k-pairs that hold rows below Kg.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_f32_pt(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+  const int G = (int)gridDim.x;
+  int tile = xcd_group(blockIdx.x, G);
+  if (tile >= a.dp_tiles) return;
+
+  const int t = threadIdx.x;
+  float* const As0 = lds;
+  float* const Bs0 = lds + 2 * C::A_STAGE;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+  typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
+  typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
+
+  int m0 = (tile % a.tiles_m) * MT, n0 = (tile / a.tiles_m) * NT;
+  al.init(a, t, m0, 0);
+  bl.init(a, t, n0, 0);
+  const int wave = t >> 6, lane = t & 63;
+  const int wm = wave % WM, wn = wave / WM;
+  const int hh = lane >> 5, q = lane & 31;
+  // k-pairs of the last stage that hold a row below Kg
+  const int last_kk = (a.Kg - (a.k_tiles - 1) * KT + 1) / 2;
+  const int nk = a.k_tiles;
+
+  al.load(a, wr);
+  bl.load(a, xr);
+  al.store(As0);
+  bl.store(Bs0);
+  __syncthreads();
+  int cur = 0;
+  int pm0 = 0, pn0 = 0;          // origin of the tile whose stores are pending
+  bool pending = false;
+  floatx16 acc[C::TM][C::TN];
+  auto clear = [&]() {
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  };
+  for (;;) {
+    const int next = tile + G;
+    if (nk > 1) {
+      // stage 0 (staged in buffer cur), stage 1's loads in flight; then the
+      // previous tile's stores
+      al.advance(a);
+      bl.advance(a);
+      al.load(a, wr);
+      bl.load(a, xr);
+      if (pending) store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+      // the stores read acc before it is cleared (else both stay live)
+      __builtin_amdgcn_sched_barrier(0);
+      clear();
+      mma_stage<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q);
+      __builtin_amdgcn_sched_barrier(0);
+      al.store(As0 + (cur ^ 1) * C::A_STAGE);
+      bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
+      __syncthreads();
+      cur ^= 1;
+      // stages 1 .. nk-2
+      for (int it = 1; it + 1 < nk; ++it) {
+        al.advance(a);
+        bl.advance(a);
+        al.load(a, wr);
+        bl.load(a, xr);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_stage<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q);
+        __builtin_amdgcn_sched_barrier(0);
+        al.store(As0 + (cur ^ 1) * C::A_STAGE);
+        bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
+        __syncthreads();
+        cur ^= 1;
+      }
+    }
+    // the last stage: its loads are the next tile's first stage; with one
+    // stage per tile, the previous tile's stores go out after them
+    const bool fetch = next < a.dp_tiles;
+    if (fetch) {
+      al.init(a, t, (next % a.tiles_m) * MT, 0);
+      bl.init(a, t, (next / a.tiles_m) * NT, 0);
+      al.load(a, wr);
+      bl.load(a, xr);
+    }
+    if (nk == 1) {
+      if (pending) store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+      __builtin_amdgcn_sched_barrier(0);
+      clear();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    mma_stage_upto<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q, last_kk);
+    __builtin_amdgcn_sched_barrier(0);
+    if (fetch) {
+      al.store(As0 + (cur ^ 1) * C::A_STAGE);
+      bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
+    }
+    __syncthreads();
+    cur ^= 1;
+    pm0 = m0;
+    pn0 = n0;
+    pending = true;
+    if (!fetch) break;
+    tile = next;
+    m0 = (tile % a.tiles_m) * MT;
+    n0 = (tile / a.tiles_m) * NT;
+  }
+  store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+}
+
+template <int LAYOUT, int AM, int BM, int TI>
+constexpr KernelFn kernel_pt_at() {
+  constexpr TileDesc d = kTiles[TI];
+  if constexpr (d.m16 != 0) return nullptr;     // 16-row tiles: not built persistent
+  else return &conv_igemm_f32_pt<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, false>;
+}
+
+template <int LAYOUT, int AM, int BM, int... TI>
+KernelFn pick_tile_pt(int tile, std::integer_sequence<int, TI...>) {
+  KernelFn fn = nullptr;
+  ((fn = (tile == TI ? kernel_pt_at<LAYOUT, AM, BM, TI>() : fn)), ...);
+  return fn;
+}
+
+template <int LAYOUT, int AM, int BM>
+KernelFn kernel_pt_for_tile(int tile) {
+  if (tile < 0 || tile >= kNumTiles) return nullptr;
+  return pick_tile_pt<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles>{});
 }
 
 // ------------------------------------------------------ 16-row tiles

@@ -161,13 +161,18 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
     *err = "internal: stream-K tail plan for a kernel without multi-piece runs";
     return MG3M_ERR_PLAN;
   }
-  if (p.dp_tiles < 0 || p.tail_wgs < 0 || p.grid != (long long)p.dp_tiles + p.tail_wgs || p.grid < 1 ||
-      p.grid > 0x7fffffffLL || (p.tail_wgs > 0 && (a.ws == nullptr || p.sk_q < 1))) {
+  if (p.persist && (p.acc64 || fused || p.tail_wgs != 0 || p.grid > p.dp_tiles)) {
+    *err = "internal: persistent plans take whole tiles of the plain fp32 kernel only";
+    return MG3M_ERR_PLAN;
+  }
+  if (p.dp_tiles < 0 || p.tail_wgs < 0 || (!p.persist && p.grid != (long long)p.dp_tiles + p.tail_wgs) ||
+      p.grid < 1 || p.grid > 0x7fffffffLL || (p.tail_wgs > 0 && (a.ws == nullptr || p.sk_q < 1))) {
     *err = "internal: grid out of range or inconsistent";
     return MG3M_ERR_PLAN;
   }
-  KernelFn fn = p.acc64 ? kernel64_for(p.variant, p.tile)
-                        : (fused ? kernel_fused_for(p.variant, p.tile) : kernel_for(p.variant, p.tile));
+  KernelFn fn = p.persist ? conv_kernel_pt(p.variant, p.tile)
+                : p.acc64 ? kernel64_for(p.variant, p.tile)
+                          : (fused ? kernel_fused_for(p.variant, p.tile) : kernel_for(p.variant, p.tile));
   if (fn == nullptr) {
     *err = "internal: no kernel for this loader variant and tile";
     return MG3M_ERR_PLAN;

@@ -78,26 +78,33 @@ struct TileDesc {
   double eff;
   int m16 = 0;
   int forced_only = 0;   // reached only through a plan override, never by the selector
+  // factor on eff for layers with more than one filter tap and more than two
+  // kt-deep channel slabs per tap (1 = no difference)
+  double eff_multitap = 1.0;
+  // registers of the persistent kernel (conv_igemm_f32_pt) with the kBVecN and
+  // the kBVecNTap patch loaders, as compiled (0: not built)
+  int regs_pt[2] = {0, 0};
 };
 
 // The tile menu.  Every entry is instantiated for every loader variant.
 constexpr int kNumTiles = 15;
 inline constexpr TileDesc kTiles[kNumTiles] = {
-    {128, 128, 16, 2, 2, 116, 0.913},   // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 116, 0.865},    // 1: four waves sharing one filter tile (TB(1,8)-like)
-    {256, 64, 16, 4, 1, 120, 0.891},    // 2: four waves sharing one patch tile
-    {64, 128, 16, 1, 2, 120, 0.890},    // 3
-    {128, 64, 16, 2, 1, 128, 0.823},    // 4
-    {64, 64, 16, 1, 1, 128, 0.740},     // 5: one wave per work-group (TB(1,1)-like)
-    {32, 128, 16, 1, 2, 88, 0.799},    // 6
-    {32, 64, 16, 1, 1, 92, 0.652},     // 7
-    {128, 32, 16, 2, 1, 88, 0.808},    // 8
-    {64, 32, 16, 1, 1, 92, 0.750},     // 9
-    {256, 128, 16, 4, 2, 111, 0.886},   // 10: eight waves
-    {128, 256, 16, 2, 4, 111, 0.832},   // 11: eight waves
-    {128, 128, 32, 2, 2, 140, 0.785},   // 12: deeper reduction step
-    {16, 64, 16, 1, 1, 88, 0.50, 1},    // 13: 16-row tile (16x16x4 MFMAs): 16 output channels
-    {64, 64, 32, 2, 2, 60, 0.78, 0, 1}, // 14: four 32x32 waves, deep step (override only)
+    // mt,  nt, kt, wm, wn, regs, eff,  m16, forced, eff_multitap, regs_pt {vec_n, vec_n_tap}
+    {128, 128, 16, 2, 2, 116, 0.913, 0, 0, 1.0, {136, 120}},  // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
+    {64, 256, 16, 1, 4, 116, 0.865, 0, 0, 1.0, {157, 125}},   // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {256, 64, 16, 4, 1, 120, 0.891, 0, 0, 1.0, {134, 125}},   // 2: four waves sharing one patch tile
+    {64, 128, 16, 1, 2, 120, 0.890, 0, 0, 1.0, {162, 129}},   // 3
+    {128, 64, 16, 2, 1, 128, 0.823, 0, 0, 1.0, {146, 129}},   // 4
+    {64, 64, 16, 1, 1, 128, 0.740, 0, 0, 1.0, {164, 131}},    // 5: one wave per work-group (TB(1,1)-like)
+    {32, 128, 16, 1, 2, 88, 0.799, 0, 0, 1.0, {125, 92}},     // 6
+    {32, 64, 16, 1, 1, 92, 0.652, 0, 0, 1.0, {127, 94}},      // 7
+    {128, 32, 16, 2, 1, 88, 0.808, 0, 0, 1.0, {100, 92}},     // 8
+    {64, 32, 16, 1, 1, 92, 0.750, 0, 0, 1.0, {110, 94}},      // 9
+    {256, 128, 16, 4, 2, 111, 0.886, 0, 0, 1.0, {127, 119}},  // 10: eight waves
+    {128, 256, 16, 2, 4, 111, 0.832, 0, 0, 1.0, {135, 119}},  // 11: eight waves
+    {128, 128, 32, 2, 2, 140, 0.785, 0, 0, 1.0, {169, 137}},  // 12: deeper reduction step
+    {16, 64, 16, 1, 1, 88, 0.50, 1, 0, 1.0, {0, 0}},          // 13: 16-row tile (16x16x4 MFMAs): 16 output channels
+    {64, 64, 32, 2, 2, 60, 0.78, 0, 0, 0.9, {86, 71}},        // 14: four 32x32 waves, deep step
 };
 
 // LDS row strides (floats) of the staged operand tiles.  An MFMA fragment
@@ -166,7 +173,8 @@ struct Plan {
   int sk_s;                 // split plans: runs per tail tile (tail_wgs = sk_s * tail_tiles); stream-K: 0
   int sk_q, sk_r;           // steps per run: sk_q, one more for the first sk_r (of each tile when split)
   int split;                // tail work-groups per tail tile, rounded up (1 without a tail)
-  long long grid;           // dp_tiles + tail_wgs
+  int persist;              // 1: whole tiles only, grid work-groups looping over them (conv_igemm_f32_pt)
+  long long grid;           // dp_tiles + tail_wgs (persistent plans: at most dp_tiles)
   int a_mode, b_mode, e_mode;
   int variant;
   size_t ws_bytes;          // workspace: the filter copy (wt_bytes), then the partials
@@ -183,6 +191,7 @@ struct KArgs {
   float* y;
   float* ws;                // tile-local partials of the tail tiles (fp64 in the fp64-accumulating kernel)
   unsigned x_bytes, w_bytes;
+  unsigned y_bytes;         // bytes of y (the persistent kernel stores through a buffer resource)
   int N, C, H, W, K, R, S;
   int sh, sw, ph, pw, Ho, Wo;
   int Mg, Ng, Kg;
@@ -260,6 +269,12 @@ KernelFn conv_kernel_hwcn_vecn_fused(int tile);
 KernelFn conv_kernel_hwcn_other_fused(int variant, int tile);
 KernelFn conv_kernel_nchw_fused(int variant, int tile);
 KernelFn conv_kernel_nchw_tap(int tile);            // conv_nchw_tap.hip
+// Persistent whole-tile kernels by (variant, tile): conv_hwcn_persist.hip;
+// null where not built (other variants, 16-row tiles).
+KernelFn conv_kernel_pt(int variant, int tile);
+constexpr bool persist_built(int variant, const TileDesc& t) {
+  return (variant == kVarHwcnVecN || variant == kVarHwcnVecNTap) && t.m16 == 0;
+}
 KernelFn conv_kernel_nchw_tap_fused(int tile);      // conv_nchw_tap_fused.hip
 // fp64-accumulating kernels by (variant, tile): conv_acc64_*.hip.
 KernelFn conv_kernel64_hwcn_vecn_tap(int tile);

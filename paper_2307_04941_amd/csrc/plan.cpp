@@ -38,16 +38,33 @@ constexpr double kStreamBytesPerS = 4.0e12;
 constexpr double kLaunchUs = 3.0;
 constexpr double kRoundUs = 2.0;
 constexpr double kUtilBase = 0.5, kUtilPerWave = 0.1;
+// Persistent plans (conv_igemm_f32_pt), measured on MI355X against the same
+// tile's data-parallel plan: its main loop (run-time LDS buffer parity, one
+// copy of the stage code) runs at 0.92 of the tile's rate on deep reductions
+// (VGG-16 conv2/conv3, 36 and 18 k-tiles: 8-11% slower); it has no per-round
+// cost (a work-group loads its next tile while storing the last); and the
+// overlap of output stores with the next tile's MFMAs lets a write-bound layer
+// stream at 4.8 TB/s (VGG-16 conv1, 860 MB: 207 -> 180 us).
+constexpr double kPersistEff = 0.92;
+constexpr double kStreamBytesPerSPersist = 4.8e12;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
 const TileDesc& tile_desc(bool acc64, int i) { return acc64 ? kTiles64[i] : kTiles[i]; }
 int lds_bytes(const TileDesc& t, bool acc64) { return (acc64 || t.m16) ? lds_bytes_for64(t) : lds_bytes_for(t); }
 
-// Work-groups of this tile resident on one CU, limited by LDS and registers.
-int resident_wgs(const TileDesc& t, bool acc64) {
+// Registers of the kernel a plan runs: the persistent kernel's with its
+// patch loader, else the tile's (tuned loader).
+int kernel_regs(const TileDesc& t, int persist_variant) {
+  if (persist_variant < 0) return t.regs;
+  return t.regs_pt[persist_variant == kVarHwcnVecNTap ? 1 : 0];
+}
+
+// Work-groups of this tile resident on one CU, limited by LDS and registers
+// (persist_variant: the loader variant of a persistent plan, else -1).
+int resident_wgs(const TileDesc& t, bool acc64, int persist_variant = -1) {
   const int waves = t.wm * t.wn;
-  const int regs = (t.regs + 7) / 8 * 8;
+  const int regs = (kernel_regs(t, persist_variant) + 7) / 8 * 8;
   const int waves_per_simd = std::min(kMaxWavesPerSimd, kRegsPerLane / regs);
   const int by_regs = std::max(1, 4 * waves_per_simd / waves);
   const int by_lds = std::max(1, kLdsBytesPerCU / lds_bytes(t, acc64));
@@ -70,7 +87,7 @@ double variant_factor(int variant) {
 }
 
 struct Override {
-  int mt = 0, nt = 0, kt = 0, split = 0, tail = 0;
+  int mt = 0, nt = 0, kt = 0, split = 0, tail = 0, persist = 0;
   long long sk = 0;
 };
 
@@ -136,6 +153,13 @@ int parse_override(const char* text, Override* o, std::string* err) {
         return MG3M_ERR_PLAN;
       }
       o->tail = (int)v;
+    } else if (key == "persist") {
+      long v = std::strtol(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || v < 1 || v > 16) {
+        *err = "plan override: persist must be 1..16 (resident work-groups per CU)";
+        return MG3M_ERR_PLAN;
+      }
+      o->persist = (int)v;
     } else if (key == "sk") {
       long long v = std::strtoll(val.c_str(), &tail, 10);
       if (tail == val.c_str() || *tail != 0 || v < 1 || v > 0x7fffffffLL) {
@@ -149,8 +173,8 @@ int parse_override(const char* text, Override* o, std::string* err) {
     }
     if (end == s.size()) break;
   }
-  if ((o->split > 0) + (o->tail > 0) + (o->sk > 0) > 1) {
-    *err = "plan override: give at most one of split, tail and sk";
+  if ((o->split > 0) + (o->tail > 0) + (o->sk > 0) + (o->persist > 0) > 1) {
+    *err = "plan override: give at most one of split, tail, sk and persist";
     return MG3M_ERR_PLAN;
   }
   return MG3M_OK;
@@ -160,7 +184,7 @@ int parse_override(const char* text, Override* o, std::string* err) {
 // cut each tail tile's reduction into `param` runs; kStreamK deals the
 // left-over tiles' k-tiles out to `param` work-groups in all (a split when
 // the runs fall on tile boundaries).
-enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2, kStreamK = 3 };
+enum Sched { kDataParallel = 0, kSplitAll = 1, kSplitTail = 2, kStreamK = 3, kPersistent = 4 };
 
 // Partials the tail work-groups write: one per run, plus (stream-K) one for
 // each tail tile boundary that falls inside a run.
@@ -221,6 +245,8 @@ bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, long long p
     }
   }
   if (dp + wgs > 0x7fffffffLL) return false;
+  // persistent: every tile whole, `param` resident work-groups per CU looping over them
+  p->persist = sched == kPersistent ? 1 : 0;
   p->dp_tiles = (int)dp;
   p->tail_tiles = (int)tail;
   p->tail_wgs = (int)wgs;
@@ -228,7 +254,7 @@ bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, long long p
   p->sk_q = (int)q;
   p->sk_r = (int)r;
   p->split = tail > 0 ? (int)cdiv(wgs, tail) : 1;
-  p->grid = dp + wgs;
+  p->grid = p->persist ? std::min<long long>(dp, (long long)kCUs * param) : dp + wgs;
   p->lds_bytes = lds_bytes(t, acc64);
   const double padded = (double)p->tiles_m * t.mt * (double)p->tiles_n * t.nt *
                         (double)p->k_tiles * t.kt;
@@ -249,17 +275,19 @@ bool shape_plan(const ConvShape& s, bool acc64, int tile, int sched, long long p
 // partials) once; the tail reduction adds its traffic and a second launch.
 double predict_us(const ConvShape& s, const Plan& p) {
   const TileDesc& t = p.t;
-  const int occ = resident_wgs(t, p.acc64);
+  const int occ = resident_wgs(t, p.acc64, p.persist ? p.variant : -1);
   const double rate = p.acc64 ? kFlopPerClkCU64 : kFlopPerClkCU;
   const double tile_flops = 2.0 * t.mt * t.nt * (double)t.kt;
+  const bool multitap = s.R * s.S > 1 && s.C >= 2 * t.kt;
   auto phase = [&](long long wgs, int k_tiles) {
     if (wgs <= 0) return 0.0;
     const long long per_cu = cdiv(wgs, kCUs);
     const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
     const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
-    const double eff = t.eff * variant_factor(p.variant) * util;
+    const double eff = t.eff * variant_factor(p.variant) * util * (multitap ? t.eff_multitap : 1.0) *
+                       (p.persist ? kPersistEff : 1.0);
     return (double)per_cu * tile_flops * k_tiles / (rate * kClockHz * eff) * 1e6 +
-           (double)cdiv(per_cu, occ) * kRoundUs;
+           (p.persist ? 1.0 : (double)cdiv(per_cu, occ)) * kRoundUs;
   };
   const int run_k = p.tail_wgs > 0 ? p.sk_q + (p.sk_r > 0 ? 1 : 0) : 0;
   const double t_comp = phase(p.dp_tiles, p.k_tiles) + phase(p.tail_wgs, run_k);
@@ -267,7 +295,8 @@ double predict_us(const ConvShape& s, const Plan& p) {
   const double xw_bytes = 4.0 * ((double)s.N * s.C * s.H * s.W + (double)s.Kg * s.Mg);
   const double part_bytes =
       (double)tail_pieces(p) * t.mt * t.nt * (p.acc64 ? sizeof(double) : sizeof(float));
-  const double t_mem = (xw_bytes + y_bytes + part_bytes) / kStreamBytesPerS * 1e6;
+  const double t_mem =
+      (xw_bytes + y_bytes + part_bytes) / (p.persist ? kStreamBytesPerSPersist : kStreamBytesPerS) * 1e6;
   double est = std::max(t_comp, t_mem) + kLaunchUs;
   if (p.tail_tiles > 0) {
     const double tail_out = 4.0 * (double)p.tail_tiles * t.mt * t.nt;
@@ -385,6 +414,15 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     // runs spanning two tiles need the kernel's loop over pieces (only the
     // 32x32x2 fp32 kernel with the one-tap HWCN loader has it)
     if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || c.t.m16 || !tail_runs_multi(c.b_mode))) return;
+    // the persistent kernel is built for the batch-vector HWCN loaders only
+    if (c.persist && (c.acc64 || !persist_built(c.variant, c.t))) return;
+    if (c.persist && sp == 0) {
+      // the selector's persistent plans fill every slot the kernel's
+      // occupancy allows, and only pay off with more tiles than that
+      const long long slots = (long long)kCUs * resident_wgs(c.t, false, c.variant);
+      if (c.dp_tiles <= slots) return;
+      c.grid = slots;
+    }
     if (c.ws_bytes > ws_cap) {
       least_over_cap = std::min(least_over_cap, c.ws_bytes);
       return;
@@ -416,6 +454,8 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       consider(ti, kSplitTail, o.tail);
     } else if (o.sk) {
       consider(ti, kStreamK, o.sk);
+    } else if (o.persist) {
+      consider(ti, kPersistent, o.persist);
     } else {
       consider(ti, kDataParallel, 1);
       for (int sp : splits) {
@@ -424,6 +464,8 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       }
       // stream-K over the left-over tiles with one to all resident work-groups per CU
       for (int j = 1, occ = resident_wgs(td, acc64); j <= occ; ++j) consider(ti, kStreamK, (long long)j * kCUs);
+      // every tile whole, persistent work-groups filling the chip
+      if (!acc64) consider(ti, kPersistent, 0);
     }
   }
   if (best < 0 && least_over_cap != SIZE_MAX) {
@@ -433,6 +475,10 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   }
   if (best < 0) {
     *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
+           (o.persist ? " persist=" + std::to_string(o.persist) +
+                            " (persistent tiles need the fp32 kernel's batch-vector HWCN loaders: HWCN, N and K"
+                            " multiples of 4, aligned buffers; not the 16-row tile)"
+                      : std::string()) +
            (o.kt ? " kt=" + std::to_string(o.kt) : std::string()) +
            (o.tail ? " tail=" + std::to_string(o.tail) : std::string()) +
            (o.sk ? " sk=" + std::to_string(o.sk) +
@@ -451,10 +497,10 @@ std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
-                "%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,tail_wgs=%d,grid=%lld,"
+                "%s%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,tail_wgs=%d,grid=%lld,"
                 "tiles=%dx%d,k_tiles=%d,a=%s,b=%s,e=%s,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
                 "Mg=%lld,Ng=%lld,Kg=%lld",
-                p.acc64 ? "acc=f64," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.tail_wgs, p.grid,
+                p.acc64 ? "acc=f64," : "", p.persist ? "persist," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.tail_wgs, p.grid,
                 p.tiles_m, p.tiles_n, p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode],
                 p.lds_bytes, p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
   return buf;

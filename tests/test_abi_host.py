@@ -136,7 +136,13 @@ def _check_plan(shape, layout, plan=None):
         assert p["split"] == -(-wgs // tail) >= 2
     else:
         assert wgs == 0 and p["split"] == 1 and p["k_tiles_per_wg"] == kt
-    assert p["grid"] == p["dp_tiles"] + wgs <= 2**31 - 1
+    if p["persistent"]:
+        # persistent: every tile whole, fewer work-groups than tiles, each
+        # looping over them
+        assert tail == 0 and 1 <= p["grid"] < p["dp_tiles"] and p["grid"] % 256 == 0 or p["grid"] == p["dp_tiles"]
+        assert p["b_mode"] in (0, 3) and layout == "HWCN" and p["mt"] != 16
+    else:
+        assert p["grid"] == p["dp_tiles"] + wgs <= 2**31 - 1
     # partials (slots up to wgs + tail - 2), plus the [R][S][C][K] filter copy
     # of a tap-major NCHW plan (b_mode 5)
     copy = -(-4 * Mg * Kg // 256) * 256 if p["b_mode"] == 5 else 0
@@ -509,3 +515,25 @@ def test_noalloc_validation_before_any_device_call():
     assert lib.conv2d_fwd_f32_noalloc(X, Wp, Y, *shape, 1, None) == 6
     msg = mg3m.mg3m_last_error()
     assert "134217728" in msg and "150994944" in msg, msg
+
+
+def test_selector_picks_persistent_and_deep_64x64_tiles():
+    """The selector's picks where the cost model's persistent and 64x64 kt=32
+    terms decide (each measured on MI355X against the previous pick): VGG-16
+    conv1 (27-row reduction, 12 rounds of tiles) runs persistent; the
+    ResNet-50 1x1 layers run the four-wave 64x64 tile with a 32-deep step;
+    its 3x3 layers with 128 or more channels do not (the tile's multi-tap
+    factor), nor do VGG-16's deep layers."""
+    p = mg3m.conv2d_fwd_f32_plan_info(64, 3, 224, 224, 64, 3, 3, 1, 1, "HWCN")
+    assert p["persistent"] == 1 and (p["mt"], p["nt"]) == (64, 256), p
+    assert p["grid"] == 256 * 3 and p["dp_tiles"] == 12544, p
+    for L in workloads.workload("resnet50_n32"):
+        p = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
+        deep64 = (p["mt"], p["nt"], p["kt"]) == (64, 64, 32)
+        if L.R == 1 and L.name not in ("rn50_c5_1x1a_first", "rn50_c5_ds_s2"):
+            assert deep64, (L.name, p)
+        if L.R == 3 and L.C >= 128:
+            assert not deep64, (L.name, p)
+    for L in workloads.workload("vgg16_n64")[1:]:
+        p = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
+        assert p["persistent"] == 0 and (p["mt"], p["kt"]) != (64, 32), (L.name, p)

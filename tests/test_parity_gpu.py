@@ -108,6 +108,30 @@ def test_every_tile_vec_n_tap(tile):
     assert np.array_equal(y, exact), f"{TAP_HYBRID} {plan}: not bit-exact"
 
 
+# Persistent whole tiles (persist=<w>: min(tiles, 256*w) work-groups looping
+# over the tiles, the next tile's first stage loaded during the last stage of
+# the current one): both batch-vector loaders, a reduction of 27 rows (the
+# three-channel 3x3 stems: the last stage skips the k-pairs past Kg), a 1x1
+# shape, and a shape with several tiles per work-group.  Integer data: exact.
+PERSIST_SHAPES = [((4, 3, 13, 11, 68, 3, 3, 1, 1), 0), ((4, 64, 13, 11, 68, 3, 3, 1, 1), 3),
+                  ((4, 64, 9, 7, 68, 1, 1, 1, 0), 3), ((32, 3, 64, 64, 64, 3, 3, 1, 1), 0),
+                  (TAP_HYBRID, 3)]
+
+
+@pytest.mark.parametrize("tile", [t for t in TILES if t != "16x64"])
+def test_every_tile_persistent(tile):
+    for si, (shape, b_mode) in enumerate(PERSIST_SHAPES):
+        x, w, st, pd, exact = _int_case(shape, 97 + si)
+        for wgs in (1, 2, 3):
+            plan = f"tile={tile},persist={wgs}"
+            info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
+            assert info["persistent"] == 1 and info["b_mode"] == b_mode, info
+            assert info["grid"] == min(info["dp_tiles"], 256 * wgs) and info["tail_tiles"] == 0, info
+            say(f"persistent {plan} shape={shape}: grid {info['grid']} tiles {info['dp_tiles']}")
+            y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+            assert np.array_equal(y, exact), f"{shape} {plan}: not bit-exact"
+
+
 @pytest.mark.parametrize("tile", TILES)
 def test_every_tile_nchw_tap_major(tile):
     """NCHW with C a multiple of kt: the filter is copied to [R][S][C][K] in
