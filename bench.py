@@ -51,7 +51,8 @@ def kernel_name(plan) -> str:
     """The main kernel's symbol as rocprofv3 prints it (its template arguments:
     layout, filter loader, patch loader, tile rows, columns, depth, waves, and
     false for the plain output stage the benchmark uses)."""
-    fn = "conv_igemm_f32_m16" if plan["mt"] == 16 else "conv_igemm_f32"   # 16-row tiles: 16x16x4 MFMAs
+    fn = ("conv_igemm_f32_pt" if plan.get("persistent") else          # persistent whole tiles
+          "conv_igemm_f32_m16" if plan["mt"] == 16 else "conv_igemm_f32")  # 16-row tiles: 16x16x4 MFMAs
     return (f"void mg3m::{fn}<{plan['layout']}, {plan['a_mode']}, {plan['b_mode']}, "
             f"{plan['mt']}, {plan['nt']}, {plan['kt']}, {plan['waves_m']}, {plan['waves_n']}, false>"
             f"(mg3m::KArgs)")
@@ -106,6 +107,65 @@ def cpu_baseline(layers, tensors, budget_s: float):
     }
 
 
+def launch_floor_us(mg3m, torch, stream, reps=100):
+    """Average time of back-to-back launches of an empty kernel on the stream
+    (the floor under layers that run for a few microseconds)."""
+    for _ in range(10):
+        mg3m.mg3m_launch_empty(stream.cuda_stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        mg3m.mg3m_launch_empty(stream.cuda_stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def ceilings(mg3m, torch, stream, dev):
+    """The chip's sustained fp32-MFMA rate (an MFMA-only kernel, four waves
+    per SIMD) and its streaming HBM bandwidth (16-byte copy and fill of
+    1 GiB): best of five timed launches each, HIP events on the stream."""
+    sp = stream.cuda_stream
+
+    def best_ms(launch, reps=5):
+        launch()
+        torch.cuda.synchronize()
+        out = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1))
+        return min(out)
+
+    blocks, iters = 256 * 4, 20000
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    flops = [0.0]
+
+    def mfma():
+        flops[0] = mg3m.mg3m_probe_mfma_f32(sink, blocks, iters, sp)
+    ms_mfma = best_ms(mfma)
+    nbytes = 1 << 30
+    src = torch.zeros(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    ms_copy = best_ms(lambda: mg3m.mg3m_probe_copy(src, dst, nbytes, sp))
+    ms_fill = best_ms(lambda: mg3m.mg3m_probe_fill(dst, nbytes, sp))
+    del src, dst, sink
+    return {
+        "mfma_f32_tflops": round(flops[0] / ms_mfma / 1e9, 2),
+        "mfma_f32_frac_of_peak": round(flops[0] / ms_mfma / 1e9 / PEAK_TFLOPS, 4),
+        "copy_gbs": round(2 * nbytes / ms_copy / 1e6, 1),
+        "fill_gbs": round(nbytes / ms_fill / 1e6, 1),
+        "hbm_peak_gbs": HBM_GBS,
+        "how": (f"mfma_probe: {blocks} work-groups x 4 waves x {iters} rounds of 8 independent "
+                f"v_mfma_f32_32x32x2_f32 on registers; copy_probe / fill_probe: 16-byte accesses over "
+                f"1 GiB, four in flight per thread, one 16 KB block per work-group (copy counts read + "
+                f"write); best of 5"),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -118,6 +178,13 @@ def main():
                     help="comma-separated layer names of the workload to run (default: all); "
                          "for profiling single layers")
     ap.add_argument("--plan", default=None, help="plan override for every layer (diagnostics)")
+    ap.add_argument("--cold-steps", type=int, default=3,
+                    help="steps of the cold pass: a 512 MiB write before every layer, outside the "
+                         "timed region (0 = skip)")
+    ap.add_argument("--probes", action="store_true",
+                    help="also measure the chip's sustained fp32-MFMA rate and streaming bandwidth")
+    ap.add_argument("--probes-only", action="store_true",
+                    help="only the launch floor and the ceiling probes (for profiling them)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the warm-up, copy a buffer of this many MiB once (a plain copy "
                          "kernel of known size, to scale the HBM byte counters of a profile run)")
@@ -137,6 +204,11 @@ def main():
     mg3m.load_library()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.probes_only:
+        st = torch.cuda.current_stream()
+        print(json.dumps({"launch_floor_us": round(launch_floor_us(mg3m, torch, st), 2),
+                          "ceilings": ceilings(mg3m, torch, st, dev)}), flush=True)
+        return
     layers_def = workloads.workload(args.workload)
     if args.layers:
         want = args.layers.split(",")
@@ -213,6 +285,37 @@ def main():
     step_flops = sum(layer_flops(L, Ho, Wo) for (L, Ho, Wo) in layers)
     value = step_flops * args.steps / elapsed / 1e12
 
+    # ---- cold pass (outside the contract's timed region): before every layer
+    # a 512 MiB write (more than the 256 MB Infinity Cache and the 8 x 4 MB
+    # L2) evicts what earlier work left in the caches; the layer is timed from
+    # its main kernel's start to an event recorded after the call (its
+    # kernels, any tail reduction, their launch gap).
+    cold = None
+    if args.cold_steps > 0:
+        flush = torch.empty((512 << 20) // 4, dtype=torch.float32, device=dev)
+        cold_us = np.zeros((args.cold_steps, len(layers)))
+        for k in range(args.cold_steps):
+            for j, ((L, Ho, Wo), (xd, wd, yd)) in enumerate(zip(layers, dev_bufs)):
+                mg3m.mg3m_probe_fill(flush, flush.numel() * 4, sp)
+                e0, e1, e2 = new_event(), new_event(), new_event()
+                mg3m.mg3m_time_next_kernel(e0, e1)
+                if args.plan:
+                    mg3m.conv2d_fwd(xd, wd, L.stride, L.pad, "HWCN", plan=args.plan, out=yd)
+                else:
+                    mg3m.conv2d_fwd_f32(xd, wd, yd, L.N, L.C, L.H, L.W, L.K, L.R, L.S,
+                                        L.stride, L.pad, "HWCN", sp)
+                e2.record(stream)
+                torch.cuda.synchronize()
+                cold_us[k, j] = e0.elapsed_time(e2) * 1e3
+        del flush
+        cold_layer = np.median(cold_us, axis=0)
+        cold_step_us = float(cold_layer.sum())
+        cold = {"value": round(step_flops / cold_step_us / 1e6, 3), "unit": "TFLOPS",
+                "ms_per_step": round(cold_step_us / 1e3, 3), "steps": args.cold_steps,
+                "flush_mib": 512,
+                "how": "sum over layers of the median (over steps) of each layer's time, main kernel "
+                       "start to the end of its call, each layer after a 512 MiB write"}
+
     per_layer = []
     for j, (L, Ho, Wo) in enumerate(layers):
         us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j + 1][0]) for k in range(args.steps)])) * 1e3
@@ -235,6 +338,8 @@ def main():
             "grid": plan["grid"], "kernel": kernel_name(plan),
             "flops": fl, "alg_bytes": by,
         })
+        if cold is not None:
+            per_layer[-1]["cold_us"] = round(float(cold_layer[j]), 2)
 
     # dominant kernel: the instantiation with the largest share of kernel time
     groups = {}
@@ -264,6 +369,13 @@ def main():
         "avg_launch_us": round(dg["us"] / dg["n"], 2),
     }
 
+    # layers whose roofline time is under 10 us are bound by launch latency:
+    # they are reported against the empty-kernel launch floor
+    floor_us = round(launch_floor_us(mg3m, torch, stream), 2)
+    for r in per_layer:
+        r["roofline_us"] = round(max(r["flops"] / (PEAK_TFLOPS * 1e6), r["alg_bytes"] / (HBM_GBS * 1e3)), 2)
+        r["latency_bound"] = r["roofline_us"] < 10.0
+
     cpu = None
     if args.cpu_seconds > 0:
         cpu = cpu_baseline(layers, tensors, args.cpu_seconds)
@@ -287,9 +399,13 @@ def main():
         "pct_peak": round(100 * value / PEAK_TFLOPS, 2),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "cold": cold,
+        "launch_floor_us": floor_us,
         "layers": per_layer,
         "kernel_digest": digest,
     }
+    if args.probes:
+        out["ceilings"] = ceilings(mg3m, torch, stream, dev)
     print(json.dumps(out), flush=True)
 
 

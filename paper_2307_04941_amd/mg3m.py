@@ -103,6 +103,10 @@ def load_library(path: str = LIB_PATH):
     lib.conv2d_fwd_f32_acc64_plan_string.argtypes = shape_hw + [cp, ctypes.c_char_p, sz]
     lib.conv2d_fwd_f32.argtypes = [p, p, p] + shape + [p]
     lib.conv2d_fwd_f32_noalloc.argtypes = [p, p, p] + shape + [p]
+    lib.mg3m_launch_empty.argtypes = [p]
+    lib.mg3m_probe_mfma_f32.argtypes = [p, i, i, p, ctypes.POINTER(ctypes.c_double)]
+    lib.mg3m_probe_copy.argtypes = [p, p, sz, p]
+    lib.mg3m_probe_fill.argtypes = [p, sz, p]
     lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
     lib.conv2d_fwd_f32_workspace_bytes.argtypes = shape + [cp, ctypes.POINTER(sz)]
     lib.conv2d_fwd_f32_plan_string.argtypes = shape + [cp, ctypes.c_char_p, sz]
@@ -352,6 +356,25 @@ def conv2d_fwd_f32(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=Non
 def conv2d_fwd_f32_noalloc(x, w, y, N, C, H, W, K, R, S, stride, pad, layout, stream=None):
     _check(load_library().conv2d_fwd_f32_noalloc(_ptr(x), _ptr(w), _ptr(y), N, C, H, W, K, R, S,
                                                  stride, pad, _layout(layout), _stream(stream)))
+
+
+def mg3m_launch_empty(stream=None):
+    _check(load_library().mg3m_launch_empty(_stream(stream)))
+
+
+def mg3m_probe_mfma_f32(sink, blocks, iters, stream=None) -> float:
+    """Launch the fp32-MFMA-only probe; returns the flops it performs."""
+    fl = ctypes.c_double()
+    _check(load_library().mg3m_probe_mfma_f32(_ptr(sink), blocks, iters, _stream(stream), ctypes.byref(fl)))
+    return fl.value
+
+
+def mg3m_probe_copy(src, dst, nbytes, stream=None):
+    _check(load_library().mg3m_probe_copy(_ptr(src), _ptr(dst), nbytes, _stream(stream)))
+
+
+def mg3m_probe_fill(dst, nbytes, stream=None):
+    _check(load_library().mg3m_probe_fill(_ptr(dst), nbytes, _stream(stream)))
 
 
 def conv2d_fwd_f32_ex(x, w, y, N, C, H, W, K, R, S, stride, pad, layout,

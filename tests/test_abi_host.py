@@ -3,6 +3,7 @@ exports every function include/mg3m.h declares; validation rejects bad
 arguments with the documented status before anything reaches the GPU; the
 planner's plans cover the output and partition the reduction; the padding
 metric reproduces the paper's printed example."""
+import glob
 import json
 import os
 import re
@@ -23,8 +24,8 @@ GOLDEN = os.path.join(ROOT, "tests", "golden")
 X, Wp, Y = 0x100000, 0x200000, 0x300000
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
 
@@ -33,8 +34,26 @@ def test_library_exports_every_declared_function():
     lib = mg3m.load_library()
     names = declared_functions()
     assert "conv2d_fwd_f32" in names and len(names) >= 9, names
-    for n in names:
-        assert hasattr(lib, n), f"{n} declared in mg3m.h but not exported"
+    headers = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
+    assert len(headers) >= 2, headers
+    for h in headers:
+        for n in declared_functions(h):
+            assert hasattr(lib, n), f"{n} declared in {os.path.basename(h)} but not exported"
+
+
+def test_measurement_calls_validate_before_launching():
+    """The measurement kernels' argument checks (no GPU needed)."""
+    lib = mg3m.load_library()
+    import ctypes
+    fl = ctypes.c_double()
+    assert lib.mg3m_probe_mfma_f32(None, 1, 1, None, ctypes.byref(fl)) == 1
+    assert lib.mg3m_probe_mfma_f32(X, 0, 1, None, ctypes.byref(fl)) == 10
+    assert lib.mg3m_probe_mfma_f32(X, 1, 0, None, ctypes.byref(fl)) == 10
+    assert lib.mg3m_probe_copy(X, Y, 15, None) == 10
+    assert lib.mg3m_probe_copy(X + 4, Y, 64, None) == 9
+    assert lib.mg3m_probe_copy(X, X + 32, 64, None) == 5
+    assert lib.mg3m_probe_fill(None, 64, None) == 1
+    assert lib.mg3m_probe_fill(Y, 0, None) == 10
 
 
 def test_status_strings():
