@@ -5,7 +5,6 @@
     python experiments.py ablation [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
     python experiments.py acc64 [--workloads W,...] [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
     python experiments.py net [--nets vgg16,alexnet,resnet50] [--batch B] [--layout L] [--reps R] [--out FILE]
-    python experiments.py vendor [--workloads W,...] [--reps R] [--out FILE]
 
 adaptability -- Sec. 5.1: the channel-scale scenes (5.1.1), the batch sweep
     (5.1.2), the filter-size sweep (5.1.3) and the padding/stride sweep
@@ -29,12 +28,6 @@ net -- whole convolution stacks of the real networks (Sec. 5.2) through the
     max pooling between blocks.  Per network: forward time run eagerly and
     replayed from a HIP graph, convolution TFLOPS over the whole forward, and
     the activation arena against keeping every activation.
-vendor -- context, not a target: the same layers through the vendor library
-    (``torch.nn.functional.conv2d`` in fp32 on NCHW tensors, i.e. MIOpen with
-    its default solution finding) beside the C-ABI call in NCHW and HWCN, per
-    layer and per workload; the largest relative difference between the two
-    NCHW outputs is printed as a check that both compute the same convolution.
-
 Inputs are the seeded synthetic tensors of ``workloads`` (HWCN, resident on
 the GPU before timing).  Each scene is warmed up for ~100 ms, then timed over
 R calls with HIP events on the calling stream.  One JSON line per scene and
@@ -193,75 +186,13 @@ def run_nets(names, batch, layout, reps, emit):
     return recs
 
 
-def _time_call(torch, f, reps):
-    t_end = time.perf_counter() + 0.1
-    while time.perf_counter() < t_end:
-        f()
-        torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        f()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) * 1e3 / reps
-
-
-def run_vendor(workload_names, reps, emit):
-    """Per layer: microseconds of the vendor convolution and of the C-ABI
-    call in both layouts, on the same seeded tensors."""
-    import torch
-    import torch.nn.functional as F
-
-    import workloads
-    from paper_2307_04941_amd import mg3m
-
-    mg3m.load_library()
-    torch.cuda.set_device(0)
-    torch.backends.cudnn.allow_tf32 = False
-    tot = collections.defaultdict(lambda: collections.defaultdict(float))
-    for wl in workload_names:
-        for i, L in enumerate(workloads.workload(wl)):
-            Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
-            flops = 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo
-            args = (L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad)
-            rec = {"workload": wl, "layer": L.name, "gflop": round(flops / 1e9, 3)}
-            _, x, w = workloads.layer_tensors(wl, i, "NCHW")
-            xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
-            y = torch.empty((L.N, L.K, Ho, Wo), dtype=torch.float32, device="cuda")
-            ref = F.conv2d(xd, wd, stride=L.stride, padding=L.pad)
-            mg3m.conv2d_fwd_f32(xd, wd, y, *args, "NCHW")
-            torch.cuda.synchronize()
-            rec["max_rel_diff"] = float((y - ref).abs().max() / ref.abs().max().clamp_min(1e-30))
-            del ref
-            times = {"vendor_nchw": _time_call(torch, lambda: F.conv2d(xd, wd, stride=L.stride,
-                                                                       padding=L.pad), reps),
-                     "mg3m_nchw": _time_call(torch, lambda: mg3m.conv2d_fwd_f32(xd, wd, y, *args, "NCHW"),
-                                             reps)}
-            del xd, wd, y
-            _, x, w = workloads.layer_tensors(wl, i, "HWCN")
-            xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
-            y = torch.empty((Ho, Wo, L.K, L.N), dtype=torch.float32, device="cuda")
-            times["mg3m_hwcn"] = _time_call(torch, lambda: mg3m.conv2d_fwd_f32(xd, wd, y, *args, "HWCN"), reps)
-            del xd, wd, y
-            torch.cuda.empty_cache()
-            for k, us in times.items():
-                rec[k] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 2)}
-                tot[wl][k] += us
-            tot[wl]["flop"] += flops
-            emit(rec)
-    emit({"summary": "vendor", "metric": "whole-workload fp32 TFLOPS",
-          "workloads": {w: {k: round(d["flop"] / us / 1e6, 2) for k, us in d.items() if k != "flop"}
-                        for w, d in tot.items()}})
-
-
 def _mean(v):
     return round(sum(v) / len(v), 2) if v else None
 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64", "net", "vendor"])
+    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64", "net"])
     ap.add_argument("--nets", default="vgg16,alexnet,resnet50")
     ap.add_argument("--batch", default="vgg16=64,alexnet=128,resnet50=64",
                     help="net: batch per network, name=N,...")
@@ -286,8 +217,6 @@ def main():
     if a.mode == "net":
         batch = {k: int(v) for k, v in (kv.split("=") for kv in a.batch.split(","))}
         run_nets(a.nets.split(","), batch, a.layout, a.reps, emit)
-    elif a.mode == "vendor":
-        run_vendor(a.workloads.split(",") if a.workloads else ["vgg16_n64", "resnet50_n32"], a.reps, emit)
     elif a.mode == "adaptability":
         names = (a.workloads.split(",") if a.workloads else
                  ["channel_scenes_n128", "batch_sweep", "filter_sweep_n128", "padstride_sweep_n128"])

@@ -142,7 +142,7 @@ int workspace_pool(void* stream, hipMemPool_t* pool, std::string* err) {
   uint64_t keep = UINT64_MAX;
   e = hipMemPoolSetAttribute(p, hipMemPoolAttrReleaseThreshold, &keep);
   if (e != hipSuccess) {
-    hipMemPoolDestroy(p);
+    (void)hipMemPoolDestroy(p);
     *err = std::string("hipMemPoolSetAttribute: ") + hipGetErrorString(e);
     return MG3M_ERR_HIP;
   }
