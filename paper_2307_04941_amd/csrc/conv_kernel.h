@@ -378,6 +378,153 @@ struct BVecNTap {
   }
 };
 
+// ------------------------------------- direct global->LDS loaders (one tap)
+// The one-tap HWCN loaders in a form that loads straight into LDS
+// (buffer_load_dwordx4 ... lds): a wave's 16-byte load puts lane l's data at
+// the wave's LDS address + 16*l, so thread t's slot in a stage is float
+// 4*t, its row and physical column follow from t as in the register-staged
+// loaders, and the thread loads the logical column that the XOR swizzle
+// places in that slot (the swizzle is its own inverse).  No VGPRs hold the
+// staged data and no LDS stores are issued; the loaded rows are visible to
+// the work-group after the loads complete and a barrier.
+typedef __attribute__((address_space(3))) void* lds_addr_t;
+
+__device__ __forceinline__ void bload_lds16(__amdgpu_buffer_rsrc_t r, float* lds, unsigned off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_addr_t)lds, 16, off, 0, 0, 0);
+}
+
+template <class C, int MT, int KT>
+struct AVecMTapDma {
+  static constexpr int MC4 = MT / 4;
+  static constexpr int RSTEP = C::T / MC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % MC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::A_ELEMS, "A vec-M split");
+  static_assert(C::AS == MT, "unpadded rows: thread t's slot is float 4*t");
+  static_assert(RSTEP % 2 == 0, "a thread's rows share their swizzle");
+  int base, wslot;          // element offset at tap (0, 0) and channel 0; the wave's first slot
+  bool m_ok;
+  int r, s, c0;
+
+  __device__ void init(const KArgs& a, int t, int m0, int kbeg) {
+    const int kr0 = t / MC4;
+    const int col = C::LA::col(kr0, (t % MC4) * 4);   // logical column of the thread's slot
+    const int m = m0 + col;
+    m_ok = m < a.Mg;
+    base = kr0 * a.K + m;
+    wslot = __builtin_amdgcn_readfirstlane((t >> 6) * 256);
+    const int t0 = kbeg / KT, rs = a.R * a.S;
+    const int slab = t0 / rs, tap = t0 - slab * rs;
+    c0 = slab * KT;
+    r = tap / a.S;
+    s = tap - r * a.S;
+  }
+  __device__ void advance(const KArgs& a) {
+    if (++s == a.S) {
+      s = 0;
+      if (++r == a.R) { r = 0; c0 += KT; }
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t wr, float* As) {
+    const int o = base + ((r * a.S + s) * a.C + c0) * a.K;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const unsigned off = (unsigned)(o + i * RSTEP * a.K) * 4u;
+      bload_lds16(wr, As + wslot + i * RSTEP * MT, m_ok ? off : kOOB);
+    }
+  }
+};
+
+template <class C, int NT, int KT>
+struct BVecNTapDma {
+  static constexpr int NC4 = NT / 4;
+  static constexpr int RSTEP = C::T / NC4;
+  static constexpr int NV = KT / RSTEP;
+  static_assert(C::T % NC4 == 0 && KT % RSTEP == 0 && NV * 4 == C::B_ELEMS, "B vec-N split");
+  static_assert(C::BS == NT, "unpadded rows: thread t's slot is float 4*t");
+  static_assert(RSTEP % 2 == 0, "a thread's rows share their swizzle");
+  int ih0, iw0, base, wslot;
+  bool col_ok;
+  int r, s, c0;
+
+  __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
+    const int kr0 = t / NC4;
+    const int n = n0 + C::LB::col(kr0, (t % NC4) * 4);   // first of the four logical columns
+    col_ok = n < a.Ng;
+    const int pix = n / a.N;
+    const int b = n - pix * a.N;
+    const int ho = pix / a.Wo, wo = pix - ho * a.Wo;
+    ih0 = ho * a.sh - a.ph;
+    iw0 = wo * a.sw - a.pw;
+    base = ((ih0 * a.W + iw0) * a.C + kr0) * a.N + b;
+    wslot = __builtin_amdgcn_readfirstlane((t >> 6) * 256);
+    const int t0 = kbeg / KT, rs = a.R * a.S;
+    const int slab = t0 / rs, tap = t0 - slab * rs;
+    c0 = slab * KT;
+    r = tap / a.S;
+    s = tap - r * a.S;
+  }
+  __device__ void advance(const KArgs& a) {
+    if (++s == a.S) {
+      s = 0;
+      if (++r == a.R) { r = 0; c0 += KT; }
+    }
+  }
+  __device__ void load(const KArgs& a, __amdgpu_buffer_rsrc_t xr, float* Bs) {
+    const bool ok = col_ok & ((unsigned)(ih0 + r) < (unsigned)a.H) & ((unsigned)(iw0 + s) < (unsigned)a.W);
+    const int o = base + ((r * a.W + s) * a.C + c0) * a.N;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const unsigned off = (unsigned)(o + i * RSTEP * a.N) * 4u;
+      bload_lds16(xr, Bs + wslot + i * RSTEP * NT, ok ? off : kOOB);
+    }
+  }
+};
+
+// s_waitcnt with only the vector-memory count at zero (gfx9 encoding:
+// vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14 = 0, expcnt bits 6:4
+// and lgkmcnt bits 11:8 at their maxima, i.e. not waited on).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// The stage pipeline of run_stages with direct-to-LDS loaders: stage it+1's
+// loads go straight into the other buffer (last read in iteration it-1, which
+// every wave finished before that iteration's barrier) while stage it's MFMAs
+// run; each iteration ends by waiting for this wave's loads and a barrier.
+template <class C, class AL, class BL, class F>
+__device__ __forceinline__ void run_stages_dma(const KArgs& a, AL& al, BL& bl, float* As0, float* Bs0, int nk,
+                                               __amdgpu_buffer_rsrc_t xr, __amdgpu_buffer_rsrc_t wr,
+                                               F&& compute) {
+  if (nk <= 0) return;
+  al.load(a, wr, As0);
+  bl.load(a, xr, Bs0);
+  wait_vmem();
+  __syncthreads();
+  auto step = [&](auto cur_c) {
+    constexpr int CUR = decltype(cur_c)::value;
+    al.advance(a);
+    bl.advance(a);
+    al.load(a, wr, As0 + (CUR ^ 1) * C::A_STAGE);
+    bl.load(a, xr, Bs0 + (CUR ^ 1) * C::B_STAGE);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(As0 + CUR * C::A_STAGE, Bs0 + CUR * C::B_STAGE);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmem();
+    __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  int it = 0;
+  for (; it + 2 <= nk - 1; it += 2) {
+    step(B0{});
+    step(B1{});
+  }
+  if (it < nk - 1) {
+    step(B0{});
+    ++it;
+  }
+  const int last = it & 1;
+  compute(As0 + last * C::A_STAGE, Bs0 + last * C::B_STAGE);
+}
+
 // NCHW input x[N][C][H][W] (Eq. 1's order), reduction order k = (c*R + r)*S + s.
 // Each thread owns four consecutive output columns n..n+3 (consecutive output
 // pixels of one image) and NV consecutive rows of the KT x NT tile.  With
@@ -727,6 +874,8 @@ struct ASel<kHWCN, kAVecM, C, MT, KT, BM> { using type = AVecM<C, MT, KT>; };
 template <class C, int MT, int KT>
 struct ASel<kHWCN, kAVecM, C, MT, KT, kBVecNTap> { using type = AVecMTap<C, MT, KT>; };
 template <class C, int MT, int KT>
+struct ASel<kHWCN, kAVecM, C, MT, KT, kBVecNTapDma> { using type = AVecMTapDma<C, MT, KT>; };
+template <class C, int MT, int KT>
 struct ASel<kNCHW, kAVecM, C, MT, KT, kBVecWTap> { using type = AVecMTap<C, MT, KT>; };
 template <class C, int MT, int KT, int BM>
 struct ASel<kNCHW, kAVecK, C, MT, KT, BM> { using type = AVecK<C, MT, KT>; };
@@ -739,6 +888,8 @@ template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecN, C, NT, KT> { using type = BVecN<C, NT, KT>; };
 template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecNTap, C, NT, KT> { using type = BVecNTap<C, NT, KT>; };
+template <class C, int NT, int KT>
+struct BSel<kHWCN, kBVecNTapDma, C, NT, KT> { using type = BVecNTapDma<C, NT, KT>; };
 template <class C, int NT, int KT>
 struct BSel<kHWCN, kBVecC, C, NT, KT> { using type = BVecC<C, NT, KT>; };
 template <class C, int NT, int KT>
@@ -1005,9 +1156,9 @@ __device__ __forceinline__ void tile_product_f32(const KArgs& a, float* lds, int
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, [&](const float* As, const float* Bs) {
-    mma_stage<C, KT>(acc, As, Bs, wm, wn, hh, q);
-  });
+  auto mma = [&](const float* As, const float* Bs) { mma_stage<C, KT>(acc, As, Bs, wm, wn, hh, q); };
+  if constexpr (BM == kBVecNTapDma) run_stages_dma<C>(a, al, bl, As0, Bs0, nk, xr, wr, mma);
+  else run_stages<C>(a, al, bl, As0, Bs0, nk, xr, wr, mma);
   store(acc, m0, n0, wm, wn, hh, q);
 }
 
@@ -1109,62 +1260,6 @@ __device__ __forceinline__ void store_tile_f32(const KArgs& a, floatx16 (&acc)[C
   }
 }
 
-// Work-groups [0, dp_tiles) compute whole tiles (tile xcd_group(i)) over
-// the full reduction and store them to y; the work-groups after them run the
-// tail (tail_runs_f32) in the same launch, starting as the last round of
-// whole tiles drains.  Stream-K runs (a loop over pieces) only with the
-// one-tap HWCN loader (tail_runs_multi): for the other loaders the loop would
-// cost the whole tiles registers and occupancy.  FUSE: the output stage
-// applies y = act(conv + add) (KArgs::add, relu).  A separate instantiation:
-// the fused stage works on the accumulators in VGPRs, and the compiler copies
-// all of them out of the AGPRs at once, which in a shared kernel would cost
-// the plain convolution a wave per SIMD.
-template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
-__global__ __launch_bounds__(WM * WN * 64)
-void conv_igemm_f32(KArgs a) {
-  using C = Cfg<MT, NT, KT, WM, WN>;
-  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
-
-  if ((int)blockIdx.x >= a.dp_tiles) {
-    tail_runs_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN, tail_runs_multi(BM)>(a, lds, blockIdx.x - a.dp_tiles);
-    return;
-  }
-  const int tile = xcd_group(blockIdx.x, a.dp_tiles);
-  tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
-      a, lds, threadIdx.x, tile, 0, a.k_tiles,
-      [&](floatx16 (&acc)[C::TM][C::TN], int m0, int n0, int wm, int wn, int hh, int q) {
-        store_tile_f32<LAYOUT, C, FUSE>(a, acc, m0, n0, wm, wn, hh, q);
-      });
-}
-
-// ------------------------------------------------- persistent whole tiles
-// mma_stage over the first nkk k-pairs of a stage only (rows 2*nkk and up are
-// past Kg: their zero-filled products are skipped, not computed).
-template <class C, int KT>
-__device__ __forceinline__ void mma_stage_upto(floatx16 (&acc)[C::TM][C::TN], const float* As,
-                                               const float* Bs, int wm, int wn, int hh, int q, int nkk) {
-  int ca[C::TM], cb[C::TN];
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i) ca[i] = hh * C::AS + C::LA::col(hh, wm * C::WTM + i * 32) + q;
-#pragma unroll
-  for (int j = 0; j < C::TN; ++j) cb[j] = hh * C::BS + C::LB::col(hh, wn * C::WTN + j * 32) + q;
-#pragma unroll
-  for (int kk = 0; kk < KT / 2; ++kk) {
-    if (kk < nkk) {   // uniform: a scalar branch per k-pair
-      float av[C::TM], bv[C::TN];
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i) av[i] = As[ca[i] + 2 * kk * C::AS];
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) bv[j] = Bs[cb[j] + 2 * kk * C::BS];
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-  }
-}
-
 // Epilogue of a whole tile through a buffer resource on y, element stores
 // (the layouts where output channel m and m+1 are mstride apart, any
 // mstride): a per-lane base offset per 32-column block plus the row's part,
@@ -1198,6 +1293,65 @@ __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&ac
           bstore1(yr, (col_ok & (r < rows_left)) ? o + (unsigned)e * rs4 : kOOB, 0u, acc[i][j][4 * g + e]);
         }
       }
+  }
+}
+
+// Work-groups [0, dp_tiles) compute whole tiles (tile xcd_group(i)) over
+// the full reduction and store them to y; the work-groups after them run the
+// tail (tail_runs_f32) in the same launch, starting as the last round of
+// whole tiles drains.  Stream-K runs (a loop over pieces) only with the
+// one-tap HWCN loader (tail_runs_multi): for the other loaders the loop would
+// cost the whole tiles registers and occupancy.  FUSE: the output stage
+// applies y = act(conv + add) (KArgs::add, relu).  A separate instantiation:
+// the fused stage works on the accumulators in VGPRs, and the compiler copies
+// all of them out of the AGPRs at once, which in a shared kernel would cost
+// the plain convolution a wave per SIMD.
+template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
+__global__ __launch_bounds__(WM * WN * 64)
+void conv_igemm_f32(KArgs a) {
+  using C = Cfg<MT, NT, KT, WM, WN>;
+  __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+
+  if ((int)blockIdx.x >= a.dp_tiles) {
+    tail_runs_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN, tail_runs_multi(BM)>(a, lds, blockIdx.x - a.dp_tiles);
+    return;
+  }
+  const int tile = xcd_group(blockIdx.x, a.dp_tiles);
+  tile_product_f32<LAYOUT, AM, BM, MT, NT, KT, WM, WN>(
+      a, lds, threadIdx.x, tile, 0, a.k_tiles,
+      [&](floatx16 (&acc)[C::TM][C::TN], int m0, int n0, int wm, int wn, int hh, int q) {
+        // the direct-to-LDS path (HWCN, N % 4 == 0: element stores) stores
+        // through a buffer resource: branch-free, 2.4% faster on VGG-16 conv3
+        if constexpr (BM == kBVecNTapDma && !FUSE) store_tile_f32_buf<LAYOUT, C>(a, acc, m0, n0, wm, wn, hh, q);
+        else store_tile_f32<LAYOUT, C, FUSE>(a, acc, m0, n0, wm, wn, hh, q);
+      });
+}
+
+// ------------------------------------------------- persistent whole tiles
+// mma_stage over the first nkk k-pairs of a stage only (rows 2*nkk and up are
+// past Kg: their zero-filled products are skipped, not computed).
+template <class C, int KT>
+__device__ __forceinline__ void mma_stage_upto(floatx16 (&acc)[C::TM][C::TN], const float* As,
+                                               const float* Bs, int wm, int wn, int hh, int q, int nkk) {
+  int ca[C::TM], cb[C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i) ca[i] = hh * C::AS + C::LA::col(hh, wm * C::WTM + i * 32) + q;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) cb[j] = hh * C::BS + C::LB::col(hh, wn * C::WTN + j * 32) + q;
+#pragma unroll
+  for (int kk = 0; kk < KT / 2; ++kk) {
+    if (kk < nkk) {   // uniform: a scalar branch per k-pair
+      float av[C::TM], bv[C::TN];
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i) av[i] = As[ca[i] + 2 * kk * C::AS];
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j) bv[j] = Bs[cb[j] + 2 * kk * C::BS];
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
   }
 }
 
@@ -1450,7 +1604,8 @@ void conv_igemm_f32_m16(KArgs a) {
 template <int LAYOUT, int AM, int BM, bool FUSE, int TI>
 constexpr KernelFn kernel_at() {
   constexpr TileDesc d = kTiles[TI];
-  if constexpr (d.m16 != 0) return &conv_igemm_f32_m16<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
+  if constexpr (d.m16 != 0 && BM == kBVecNTapDma) return nullptr;   // not built: 16-row tiles stage through VGPRs
+  else if constexpr (d.m16 != 0) return &conv_igemm_f32_m16<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
   else return &conv_igemm_f32<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
 }
 

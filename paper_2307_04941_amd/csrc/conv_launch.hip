@@ -97,6 +97,7 @@ static KernelFn kernel_for(int variant, int tile) {
   switch (variant) {
     case kVarHwcnVecN: return conv_kernel_hwcn_vecn(tile);
     case kVarHwcnVecNTap: return conv_kernel_hwcn_vecn_tap(tile);
+    case kVarHwcnVecNTapDma: return conv_kernel_hwcn_vecn_tap_dma(tile);
     case kVarHwcnVecC: return conv_kernel_hwcn_vecc(tile);
     case kVarHwcnVecA: return conv_kernel_hwcn_veca(tile);
     case kVarHwcnScalar: return conv_kernel_hwcn_scalar(tile);
@@ -107,9 +108,13 @@ static KernelFn kernel_for(int variant, int tile) {
   }
 }
 
+// The direct-to-LDS variant has no fused instantiation: its plans (tile,
+// schedule, workspace) are exactly those of the register-staged one-tap
+// loaders, whose fused kernel runs them.
 static KernelFn kernel_fused_for(int variant, int tile) {
   switch (variant) {
-    case kVarHwcnVecNTap: return conv_kernel_hwcn_vecn_tap_fused(tile);
+    case kVarHwcnVecNTap:
+    case kVarHwcnVecNTapDma: return conv_kernel_hwcn_vecn_tap_fused(tile);
     case kVarHwcnVecN: return conv_kernel_hwcn_vecn_fused(tile);
     case kVarHwcnVecC:
     case kVarHwcnVecA:

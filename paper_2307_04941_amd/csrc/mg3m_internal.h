@@ -26,7 +26,8 @@ enum Layout : int { kHWCN = 0, kNCHW = 1 };
 //                               channels (NCHW, C % kt == 0; the filter is first
 //                               copied to [R][S][C][K] and read by kAVecM)
 enum AMode : int { kAVecM = 0, kAVecK = 1, kAScalar = 2 };
-enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3, kBVecW = 4, kBVecWTap = 5 };
+enum BMode : int { kBVecN = 0, kBVecC = 1, kBScalar = 2, kBVecNTap = 3, kBVecW = 4, kBVecWTap = 5,
+                   kBVecNTapDma = 6 };
 // The loader pairs that are instantiated.
 enum Variant : int {
   kVarHwcnVecN = 0,     // HWCN, A vec-M, B vec-N
@@ -37,7 +38,8 @@ enum Variant : int {
   kVarNchwScalar = 5,   // NCHW, A scalar, B vec-W
   kVarHwcnVecNTap = 6,  // HWCN, A vec-M, B vec-N with one tap per slab (the tuned path)
   kVarNchwTap = 7,      // NCHW, A vec-M on the [R][S][C][K] filter copy, B vec-W one tap per slab
-  kNumVariants = 8
+  kVarHwcnVecNTapDma = 8,  // kVarHwcnVecNTap with both operands loaded straight into LDS
+  kNumVariants = 9
 };
 // Epilogue store: single elements, or 16-byte vectors of four consecutive
 // output channels (HWCN with N == 1 and K % 4 == 0, where they are contiguous).
@@ -253,12 +255,13 @@ std::string plan_to_string(const ConvShape& s, const Plan& p);
 // spanning two tiles, taken in a loop).  Only the one-tap HWCN loader does
 // so without losing occupancy on its whole tiles; the others, and the
 // fp64-accumulating kernel, take split tail plans (one piece per run).
-constexpr bool tail_runs_multi(int b_mode) { return b_mode == kBVecNTap; }
+constexpr bool tail_runs_multi(int b_mode) { return b_mode == kBVecNTap || b_mode == kBVecNTapDma; }
 
 // Kernel entry points by (variant, tile): conv_hwcn_*.hip, conv_nchw.hip.
 using KernelFn = void (*)(KArgs);
 KernelFn conv_kernel_hwcn_vecn(int tile);
 KernelFn conv_kernel_hwcn_vecn_tap(int tile);
+KernelFn conv_kernel_hwcn_vecn_tap_dma(int tile);   // conv_hwcn_vecn_tap_dma.hip
 KernelFn conv_kernel_hwcn_vecc(int tile);
 KernelFn conv_kernel_hwcn_veca(int tile);
 KernelFn conv_kernel_hwcn_scalar(int tile);

@@ -77,7 +77,7 @@ int resident_wgs(const TileDesc& t, bool acc64, int persist_variant = -1) {
 // over the fastest plan per layer 9.2% -> 3.3%; its 7x7 stem 231 -> 146 us).
 double variant_factor(int variant) {
   switch (variant) {
-    case kVarHwcnVecNTap: return 1.0;
+    case kVarHwcnVecNTap: case kVarHwcnVecNTapDma: return 1.0;
     case kVarNchwTap: return 0.9;
     case kVarNchwVecA: return 1.0;
     case kVarHwcnVecN: return 0.85;
@@ -87,7 +87,7 @@ double variant_factor(int variant) {
 }
 
 struct Override {
-  int mt = 0, nt = 0, kt = 0, split = 0, tail = 0, persist = 0;
+  int mt = 0, nt = 0, kt = 0, split = 0, tail = 0, persist = 0, dma = -1;   // dma: -1 = the default
   long long sk = 0;
 };
 
@@ -153,6 +153,13 @@ int parse_override(const char* text, Override* o, std::string* err) {
         return MG3M_ERR_PLAN;
       }
       o->tail = (int)v;
+    } else if (key == "dma") {
+      long v = std::strtol(val.c_str(), &tail, 10);
+      if (tail == val.c_str() || *tail != 0 || (v != 0 && v != 1)) {
+        *err = "plan override: dma must be 0 or 1";
+        return MG3M_ERR_PLAN;
+      }
+      o->dma = (int)v;
     } else if (key == "persist") {
       long v = std::strtol(val.c_str(), &tail, 10);
       if (tail == val.c_str() || *tail != 0 || v < 1 || v > 16) {
@@ -353,11 +360,13 @@ int make_shape(int N, int C, int H, int W, int K, int R, int S, int stride_h, in
 }
 
 // Loader variant and epilogue mode for a plan whose tile is already set.
-void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p) {
+// dma: the one-tap HWCN loaders in their direct-to-LDS form.
+void choose_modes(const ConvShape& s, bool x16, bool w16, bool y16, Plan* p, bool dma = false) {
   if (s.layout == kHWCN) {
     if (s.K % 4 == 0 && w16) {
       p->a_mode = kAVecM;
-      if (s.N % 4 == 0 && x16 && s.C % p->t.kt == 0) p->b_mode = kBVecNTap, p->variant = kVarHwcnVecNTap;
+      if (s.N % 4 == 0 && x16 && s.C % p->t.kt == 0)
+        p->b_mode = dma ? kBVecNTapDma : kBVecNTap, p->variant = dma ? kVarHwcnVecNTapDma : kVarHwcnVecNTap;
       else if (s.N % 4 == 0 && x16) p->b_mode = kBVecN, p->variant = kVarHwcnVecN;
       else if (s.N == 1 && s.C % 4 == 0 && x16) p->b_mode = kBVecC, p->variant = kVarHwcnVecC;
       else p->b_mode = kBScalar, p->variant = kVarHwcnVecA;
@@ -410,7 +419,12 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   auto consider = [&](int ti, int sched, long long sp) {
     Plan c{};
     if (!shape_plan(s, acc64, ti, sched, sp, &c)) return;
-    choose_modes(s, x16, w16, y16, &c);
+    // the one-tap HWCN loaders load straight into LDS unless the override says
+    // otherwise, except in the persistent and fp64-accumulating kernels and
+    // the 16-row tile, which stage through VGPRs
+    const bool dma_ok = !c.acc64 && !c.t.m16 && !c.persist;
+    choose_modes(s, x16, w16, y16, &c, dma_ok && o.dma != 0);
+    if (o.dma == 1 && c.variant != kVarHwcnVecNTapDma) return;
     // runs spanning two tiles need the kernel's loop over pieces (only the
     // 32x32x2 fp32 kernel with the one-tap HWCN loader has it)
     if (c.tail_wgs > 0 && c.sk_s == 0 && (c.acc64 || c.t.m16 || !tail_runs_multi(c.b_mode))) return;
@@ -475,6 +489,9 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   }
   if (best < 0) {
     *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
+           (o.dma == 1 ? std::string(" dma=1 (the direct-to-LDS loaders serve the fp32 kernel's one-tap HWCN path"
+                                     " with 32x32x2-MFMA tiles, not persistent plans)")
+                       : std::string()) +
            (o.persist ? " persist=" + std::to_string(o.persist) +
                             " (persistent tiles need the fp32 kernel's batch-vector HWCN loaders: HWCN, N and K"
                             " multiples of 4, aligned buffers; not the 16-row tile)"
@@ -493,7 +510,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
 
 std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* an[] = {"vec_m", "vec_k", "scalar"};
-  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap", "vec_w", "vec_w_tap"};
+  static const char* bn[] = {"vec_n", "vec_c", "scalar", "vec_n_tap", "vec_w", "vec_w_tap", "vec_n_tap_dma"};
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,

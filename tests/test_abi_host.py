@@ -165,6 +165,9 @@ def _check_plan(shape, layout, plan=None):
     # partials (slots up to wgs + tail - 2), plus the [R][S][C][K] filter copy
     # of a tap-major NCHW plan (b_mode 5)
     copy = -(-4 * Mg * Kg // 256) * 256 if p["b_mode"] == 5 else 0
+    # the direct-to-LDS one-tap loaders: HWCN, 32x32x2-MFMA tiles, not persistent
+    assert p["b_mode"] != 6 or (layout == "HWCN" and p["mt"] != 16 and not p["persistent"]
+                                and N % 4 == 0 and K % 4 == 0 and C % p["kt"] == 0)
     assert p["b_mode"] != 5 or (layout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
                                 and (st if isinstance(st, int) else st[1]) == 1)
     slots = wgs + tail - 1 if tail else 0
@@ -534,6 +537,25 @@ def test_noalloc_validation_before_any_device_call():
     assert lib.conv2d_fwd_f32_noalloc(X, Wp, Y, *shape, 1, None) == 6
     msg = mg3m.mg3m_last_error()
     assert "134217728" in msg and "150994944" in msg, msg
+
+
+def test_one_tap_loaders_default_to_direct_lds():
+    """Where the one-tap HWCN loaders apply, the selector's plans load straight
+    into LDS (b_mode 6) unless they are persistent or on the 16-row tile;
+    dma=0 keeps the same plan with the loaders staging through VGPRs (b_mode 3),
+    and dma=1 is refused where the direct-to-LDS form does not apply."""
+    shape = (64, 256, 56, 56, 256, 3, 3, 1, 1)
+    p = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN")
+    q = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "dma=0")
+    assert p["b_mode"] == 6 and q["b_mode"] == 3
+    same = ("mt", "nt", "kt", "split", "dp_tiles", "tail_tiles", "tail_wgs", "grid", "workspace_bytes")
+    assert all(p[k] == q[k] for k in same), (p, q)
+    for bad in ("tile=16x64,dma=1", "tile=128x128,persist=2,dma=1"):
+        with pytest.raises(mg3m.Mg3mError):
+            mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", bad)
+    assert mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW")["b_mode"] == 5
+    with pytest.raises(mg3m.Mg3mError):
+        mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "dma=1")
 
 
 def test_selector_picks_persistent_and_deep_64x64_tiles():

@@ -109,6 +109,28 @@ def test_persistent_register_table_matches_build(resources):
     assert not drift, "persistent register table drifted from the build:\n" + "\n".join(drift)
 
 
+def _resident(regs, waves, lds):
+    """Work-groups per CU as the planner counts them (512 registers per lane
+    per SIMD in granules of 8, at most 8 waves per SIMD, 160 KB of LDS)."""
+    per_simd = min(8, 512 // ((regs + 7) // 8 * 8))
+    return min(max(1, 4 * per_simd // waves), max(1, 160 * 1024 // lds))
+
+
+def test_direct_lds_kernels_keep_the_modelled_occupancy(resources):
+    """The selector counts resident work-groups from the register-staged
+    kernel's registers; the direct-to-LDS kernel of the same tile (the
+    default one-tap path) needs no more registers and must give the same
+    count once LDS caps it."""
+    for i, t in enumerate(tile_tables()["f32"]):
+        mt, nt, kt, wm, wn, regs, m16, lds = t[:8]
+        if m16:
+            continue
+        name = f"void mg3m::conv_igemm_f32<0, 0, 6, {mt}, {nt}, {kt}, {wm}, {wn}, false>(mg3m::KArgs)"
+        got = resources[name]
+        assert got["vgpr_count"] <= regs and got["lds_bytes"] == lds, (i, got)
+        assert _resident(got["vgpr_count"], wm * wn, lds) == _resident(regs, wm * wn, lds), (i, got)
+
+
 def test_no_kernel_spills_to_scratch(resources):
     """Every kernel keeps its state in registers (no private segment)."""
     spills = [k for k, r in resources.items() if r.get("scratch_bytes", 0) != 0]

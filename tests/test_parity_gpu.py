@@ -88,21 +88,30 @@ def _int_case(shape, seed):
     return _oracle_cache[key]
 
 
+@pytest.mark.parametrize("dma", [0, 1], ids=["lds_via_vgprs", "direct_to_lds"])
 @pytest.mark.parametrize("tile", TILES)
-def test_every_tile_vec_n_tap(tile):
+def test_every_tile_vec_n_tap(tile, dma):
+    """dma=0: the loaders staging through VGPRs (b_mode 3); dma=1: the same
+    loaders in their direct-to-LDS form (b_mode 6, the default where it
+    applies; not built for the 16-row tile)."""
+    if dma and tile == "16x64":
+        with pytest.raises(mg3m.Mg3mError):
+            mg3m.conv2d_fwd_f32_plan_info(*TAP_SHAPES[0], "HWCN", f"tile={tile},dma=1")
+        return
+    suffix = ",dma=1" if dma else ",dma=0"
     for si, shape in enumerate(TAP_SHAPES):
         x, w, st, pd, exact = _int_case(shape, 90 + si)
         for split in (1, 2, 5):
-            plan = f"tile={tile},split={split}"
+            plan = f"tile={tile},split={split}{suffix}"
             info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
-            assert info["b_mode"] == 3, info
+            assert info["b_mode"] == (6 if dma else 3), info
             say(f"forced vec_n_tap {plan} shape={shape}")
             y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
             assert np.array_equal(y, exact), f"{shape} {plan}: not bit-exact"
     x, w, st, pd, exact = _int_case(TAP_HYBRID, 95)
-    plan = f"tile={tile},tail=3"
+    plan = f"tile={tile},tail=3{suffix}"
     info = mg3m.conv2d_fwd_f32_plan_info(*TAP_HYBRID, "HWCN", plan)
-    assert info["b_mode"] == 3 and info["dp_tiles"] > 0 and info["tail_tiles"] > 0, info
+    assert info["b_mode"] == (6 if dma else 3) and info["dp_tiles"] > 0 and info["tail_tiles"] > 0, info
     say(f"forced vec_n_tap hybrid {plan}: dp_tiles {info['dp_tiles']} tail_tiles {info['tail_tiles']}")
     y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
     assert np.array_equal(y, exact), f"{TAP_HYBRID} {plan}: not bit-exact"
