@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libmg3m.so")
 SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn_tap_dma.hip", "conv_hwcn_vecn.hip", "conv_hwcn_vecc.hip", "conv_hwcn_veca.hip", "conv_hwcn_scalar.hip",
            "conv_nchw.hip", "conv_acc64_hwcn_tap.hip", "conv_acc64_hwcn.hip", "conv_acc64_nchw.hip",
            "conv_hwcn_vecn_tap_fused.hip", "conv_hwcn_vecn_fused.hip", "conv_hwcn_other_fused.hip",
-           "conv_nchw_fused.hip", "conv_nchw_tap.hip", "conv_nchw_tap_fused.hip", "conv_hwcn_persist.hip",
+           "conv_nchw_fused.hip", "conv_nchw_tap.hip", "conv_nchw_tap_fused.hip", "conv_hwcn_persist.hip", "conv_hwcn_persist_fused.hip",
            "conv_launch.hip", "pool.hip", "plan.cpp", "abi.cpp", "net.cpp", "noalloc.hip", "measure.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,7 +40,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # the loop over tiles, and in AGPRs the compiler copied all of them to VGPRs
 # and back around every stage (180-216 registers instead of 117-155).
 PER_SOURCE = {s: ["-mllvm", "-amdgpu-mfma-vgpr-form=1"] for s in SOURCES
-              if s.startswith("conv_acc64_") or s == "conv_hwcn_persist.hip"}
+              if s.startswith("conv_acc64_") or s.startswith("conv_hwcn_persist")}
 
 
 def _compile(src: str, obj: str, extra=()):

@@ -1266,7 +1266,7 @@ __device__ __forceinline__ void store_tile_f32(const KArgs& a, floatx16 (&acc)[C
 // and elements outside the output sent to the out-of-range offset (with a
 // zero scalar offset, as the loaders do), which the buffer hardware drops --
 // no branches and no 64-bit address per store.
-template <int LAYOUT, class C>
+template <int LAYOUT, class C, bool FUSE = false>
 __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&acc)[C::TM][C::TN], int m0, int n0,
                                                    int wm, int wn, int hh, int q) {
   const __amdgpu_buffer_rsrc_t yr = make_rsrc(a.y, a.y_bytes);
@@ -1290,7 +1290,13 @@ __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&ac
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = i * 32 + 8 * g + e;         // row offset from the lane's first row
-          bstore1(yr, (col_ok & (r < rows_left)) ? o + (unsigned)e * rs4 : kOOB, 0u, acc[i][j][4 * g + e]);
+          const bool ok = col_ok & (r < rows_left);
+          float v = acc[i][j][4 * g + e];
+          // fused output stage (add read only where the output element exists)
+          if constexpr (FUSE) {
+            if (ok) v = finish1(a, v, (int)((o + (unsigned)e * rs4) / 4u));
+          }
+          bstore1(yr, ok ? o + (unsigned)e * rs4 : kOOB, 0u, v);
         }
       }
   }
@@ -1425,7 +1431,7 @@ void conv_igemm_f32_pt(KArgs a) {
       bl.advance(a);
       al.load(a, wr);
       bl.load(a, xr);
-      if (pending) store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+      if (pending) store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, pm0, pn0, wm, wn, hh, q);
       // the stores read acc before it is cleared (else both stay live)
       __builtin_amdgcn_sched_barrier(0);
       clear();
@@ -1460,7 +1466,7 @@ void conv_igemm_f32_pt(KArgs a) {
       bl.load(a, xr);
     }
     if (nk == 1) {
-      if (pending) store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+      if (pending) store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, pm0, pn0, wm, wn, hh, q);
       __builtin_amdgcn_sched_barrier(0);
       clear();
     }
@@ -1481,27 +1487,27 @@ void conv_igemm_f32_pt(KArgs a) {
     m0 = (tile % a.tiles_m) * MT;
     n0 = (tile / a.tiles_m) * NT;
   }
-  store_tile_f32_buf<LAYOUT, C>(a, acc, pm0, pn0, wm, wn, hh, q);
+  store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, pm0, pn0, wm, wn, hh, q);
 }
 
-template <int LAYOUT, int AM, int BM, int TI>
+template <int LAYOUT, int AM, int BM, bool FUSE, int TI>
 constexpr KernelFn kernel_pt_at() {
   constexpr TileDesc d = kTiles[TI];
   if constexpr (d.m16 != 0) return nullptr;     // 16-row tiles: not built persistent
-  else return &conv_igemm_f32_pt<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, false>;
+  else return &conv_igemm_f32_pt<LAYOUT, AM, BM, d.mt, d.nt, d.kt, d.wm, d.wn, FUSE>;
 }
 
-template <int LAYOUT, int AM, int BM, int... TI>
+template <int LAYOUT, int AM, int BM, bool FUSE, int... TI>
 KernelFn pick_tile_pt(int tile, std::integer_sequence<int, TI...>) {
   KernelFn fn = nullptr;
-  ((fn = (tile == TI ? kernel_pt_at<LAYOUT, AM, BM, TI>() : fn)), ...);
+  ((fn = (tile == TI ? kernel_pt_at<LAYOUT, AM, BM, FUSE, TI>() : fn)), ...);
   return fn;
 }
 
-template <int LAYOUT, int AM, int BM>
+template <int LAYOUT, int AM, int BM, bool FUSE = false>
 KernelFn kernel_pt_for_tile(int tile) {
   if (tile < 0 || tile >= kNumTiles) return nullptr;
-  return pick_tile_pt<LAYOUT, AM, BM>(tile, std::make_integer_sequence<int, kNumTiles>{});
+  return pick_tile_pt<LAYOUT, AM, BM, FUSE>(tile, std::make_integer_sequence<int, kNumTiles>{});
 }
 
 // ------------------------------------------------------ 16-row tiles

@@ -166,8 +166,8 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
     *err = "internal: stream-K tail plan for a kernel without multi-piece runs";
     return MG3M_ERR_PLAN;
   }
-  if (p.persist && (p.acc64 || fused || p.tail_wgs != 0 || p.grid > p.dp_tiles)) {
-    *err = "internal: persistent plans take whole tiles of the plain fp32 kernel only";
+  if (p.persist && (p.acc64 || p.tail_wgs != 0 || p.grid > p.dp_tiles)) {
+    *err = "internal: persistent plans take whole tiles of the fp32 kernel only";
     return MG3M_ERR_PLAN;
   }
   if (p.dp_tiles < 0 || p.tail_wgs < 0 || (!p.persist && p.grid != (long long)p.dp_tiles + p.tail_wgs) ||
@@ -175,7 +175,7 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
     *err = "internal: grid out of range or inconsistent";
     return MG3M_ERR_PLAN;
   }
-  KernelFn fn = p.persist ? conv_kernel_pt(p.variant, p.tile)
+  KernelFn fn = p.persist ? (fused ? conv_kernel_pt_fused(p.variant, p.tile) : conv_kernel_pt(p.variant, p.tile))
                 : p.acc64 ? kernel64_for(p.variant, p.tile)
                           : (fused ? kernel_fused_for(p.variant, p.tile) : kernel_for(p.variant, p.tile));
   if (fn == nullptr) {

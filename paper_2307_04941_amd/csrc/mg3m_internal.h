@@ -275,6 +275,7 @@ KernelFn conv_kernel_nchw_tap(int tile);            // conv_nchw_tap.hip
 // Persistent whole-tile kernels by (variant, tile): conv_hwcn_persist.hip;
 // null where not built (other variants, 16-row tiles).
 KernelFn conv_kernel_pt(int variant, int tile);
+KernelFn conv_kernel_pt_fused(int variant, int tile);   // conv_hwcn_persist_fused.hip
 constexpr bool persist_built(int variant, const TileDesc& t) {
   return (variant == kVarHwcnVecN || variant == kVarHwcnVecNTap) && t.m16 == 0;
 }

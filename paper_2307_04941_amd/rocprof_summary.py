@@ -85,6 +85,15 @@ FAMILIES = [("conv_igemm_f32<", ", false>", "convolution (fp32, plain output)"),
             ("filter_kcrs_to_rsck", "", "NCHW filter copy")]
 
 
+def kernel_tag(kernel: str) -> str:
+    """Short file-name tag of a kernel: its function name (persistent and
+    16-row kernels keep their suffix) and its integer template arguments."""
+    fn = kernel[:kernel.index("<")].split("::")[-1]
+    args = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").split(",")
+    base = fn.replace("conv_igemm_f32", "conv_igemm")
+    return base + "_" + "_".join(v for v in args if v.lstrip("-").isdigit())
+
+
 def family(name: str) -> str:
     for head, tail, label in FAMILIES:
         if head in name and tail in name:
@@ -137,14 +146,14 @@ def mfma_summary(a):
     if not acc:
         raise ValueError(f"no dispatch of {kernel} in {a.mfma}")
     traffic = None
-    tpath = os.path.join(a.out, f"traffic_{a.workload}.json")
+    tpath = os.path.join(a.out, f"traffic_{a.label or a.workload}.json")
     if os.path.exists(tpath):
         with open(tpath) as f:
             t = json.load(f)
         if t.get("kernel") == kernel:
             traffic = t["hbm_bytes_per_launch"]
     args = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").split(",")
-    tag = "conv_igemm_" + "_".join(v for v in args if v.lstrip("-").isdigit())
+    tag = kernel_tag(kernel)
     lines = [f"MFMA utilisation of {kernel}, workload {a.workload}",
              f"command: {a.command_mfma}", "",
              f"GPU: {xcc} XCDs, {simds} SIMDs, {clk_max / 1e9:.2f} GHz maximum engine clock",
@@ -168,7 +177,7 @@ def mfma_summary(a):
         lines.append(f"HBM traffic {traffic / 1e6:.1f} MB per launch (traffic_{a.workload}.json) over the "
                      f"mean launch time here: {gbs:.0f} GB/s = {100 * gbs / 8000:.1f}% of the 8.0 TB/s HBM peak "
                      f"(counter runs serialise dispatches; the benchmark's own launches run faster)")
-    with open(os.path.join(a.out, f"{tag}_{a.workload}_mfma.txt"), "w") as f:
+    with open(os.path.join(a.out, f"{tag}_{a.label or a.workload}_mfma.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines[-3:]))
     return 0
@@ -178,6 +187,9 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--stats-only", default=None, metavar="NAME")
     ap.add_argument("--workload")
+    ap.add_argument("--label", default=None,
+                    help="workload part of the output file names (default: --workload), e.g. for a run "
+                         "of selected layers")
     ap.add_argument("--trace")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
@@ -206,7 +218,7 @@ def main(argv=None):
         bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
     kernel = bench["roofline"]["kernel"]
     args = kernel[kernel.index("<") + 1:kernel.index(">")].replace(" ", "").split(",")
-    tag = "conv_igemm_" + "_".join(v for v in args if v.lstrip("-").isdigit())
+    tag = kernel_tag(kernel)
     os.makedirs(a.out, exist_ok=True)
 
     # ---- kernel statistics
@@ -230,7 +242,7 @@ def main(argv=None):
     lines += [f"  achieved {roof['achieved']} TFLOP/s of {roof['peak']} ({100 * roof['frac']:.1f}%)",
               f"bench.py value: {bench['value']} {bench['unit']} ({bench.get('pct_peak')}% of peak), "
               f"{bench['ms_per_step']} ms per step, kernel digest {bench['kernel_digest']}"]
-    with open(os.path.join(a.out, f"{tag}_{a.workload}_kernel_stats.txt"), "w") as f:
+    with open(os.path.join(a.out, f"{tag}_{a.label or a.workload}_kernel_stats.txt"), "w") as f:
         f.write("\n".join(lines) + "\n")
 
     # ---- HBM traffic of the dominant kernel
@@ -258,7 +270,7 @@ def main(argv=None):
         "alg_flops_per_launch": alg_flops,
         "command_fetch": a.command_fetch, "command_write": a.command_write,
     }
-    with open(os.path.join(a.out, f"traffic_{a.workload}.json"), "w") as f:
+    with open(os.path.join(a.out, f"traffic_{a.label or a.workload}.json"), "w") as f:
         json.dump(out, f, indent=1)
     txt = [f"HBM traffic of {kernel}, workload {a.workload}",
            f"FETCH_SIZE run: {a.command_fetch}", f"WRITE_SIZE run: {a.command_write}", "",
@@ -271,7 +283,7 @@ def main(argv=None):
            "", "per dispatch (KiB, unscaled): FETCH_SIZE / WRITE_SIZE"]
     for (d, _, fv), (_, _, wv) in zip([x for x in fetch if x[1] == kernel], [x for x in write if x[1] == kernel]):
         txt.append(f"  dispatch {d}: {fv:.0f} / {wv:.0f}")
-    with open(os.path.join(a.out, f"{tag}_{a.workload}_traffic.txt"), "w") as f:
+    with open(os.path.join(a.out, f"{tag}_{a.label or a.workload}_traffic.txt"), "w") as f:
         f.write("\n".join(txt) + "\n")
     print(json.dumps(out))
 

@@ -97,6 +97,40 @@ def test_fused_add_relu(layout, plan, shape):
     assert np.all(np.abs(y.cpu().numpy() - ref) <= tol)
 
 
+@pytest.mark.parametrize("plan,shape", [
+    (None, (32, 3, 64, 64, 64, 3, 3, 1, 1)),                        # first-layer shape: the selector's pick
+    ("tile=128x128,persist=1", (4, 64, 13, 11, 68, 3, 3, 1, 1)),    # ragged rows and columns, 1-tap loaders
+    ("tile=64x256,persist=1", (32, 3, 56, 56, 64, 3, 3, 1, 1)),     # several tiles per work-group
+])
+def test_fused_add_relu_persistent(plan, shape):
+    """The persistent whole-tile kernel's fused output stage: add read and
+    ReLU applied in its buffer-store epilogue (HWCN only)."""
+    import torch
+    info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
+    assert info["persistent"] == 1, info
+    say(f"fused persistent {plan} {shape}: grid {info['grid']} tiles {info['dp_tiles']}")
+    x, w, st, pd = make(shape, 962, "HWCN")
+    acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+    rng = np.random.Generator(np.random.PCG64(963))
+    add = rng.standard_normal(acc.shape).astype(np.float32)
+    N, C, H, W, K, R, S = mg3m.dims_of(x, w, "HWCN")
+    ws = torch.empty(1, dtype=torch.float32, device="cuda")
+    xd, wd = to_dev(x), to_dev(w)
+    for relu in (0, 1):
+        for inplace in (False, True):
+            addd = to_dev(add)
+            y = addd if inplace else torch.empty(acc.shape, dtype=torch.float32, device="cuda")
+            mg3m.conv2d_fwd_f32_fused(xd, wd, y, addd, relu, N, C, H, W, K, R, S, 1, 1, 1, 1, "HWCN",
+                                      ws, 4, plan)
+            got = y.cpu().numpy().astype(np.float64)
+            ref, tol = _fused_ref(acc, mag, add, relu)
+            assert np.all(np.abs(got - ref) <= tol), f"relu={relu} inplace={inplace}"
+    y = torch.empty(acc.shape, dtype=torch.float32, device="cuda")
+    mg3m.conv2d_fwd_f32_fused(xd, wd, y, None, 1, N, C, H, W, K, R, S, 1, 1, 1, 1, "HWCN", ws, 4, plan)
+    ref, tol = _fused_ref(acc, mag, None, 1)
+    assert np.all(np.abs(y.cpu().numpy() - ref) <= tol)
+
+
 MINI = [
     {"op": "conv", "input": 0, "K": 16, "R": 3, "stride": 1, "pad": 1, "relu": 1},     # 1
     {"op": "conv", "input": 1, "K": 16, "R": 3, "stride": 1, "pad": 1, "relu": 0},     # 2
