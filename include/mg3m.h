@@ -80,9 +80,12 @@ int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, in
  * the plan shares the Kg reduction of some output tiles out among several
  * work-groups (all tiles, or only those left over after whole rounds of
  * work-groups; each work-group takes an equal run of their k-tiles, stream-K
- * fashion), the pieces' partial sums go to a workspace that this call takes
- * from the library's stream-ordered pool for the stream's device (taken and
- * given back on `stream`; see mg3m_trim_workspace_pool) and a second kernel
+ * fashion), the pieces' partial sums go to a workspace that the library keeps
+ * for `stream` (one buffer per stream, reused by every later call there and
+ * replaced by a larger one, stream-ordered, when a plan needs more; taken
+ * from the library's stream-ordered pool for the stream's device; a call
+ * being captured into a graph takes a pool block inside the graph instead;
+ * see mg3m_trim_workspace_pool) and a second kernel
  * sums them in a fixed order, so results are
  * deterministic run to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
  * a filter of more than one tap and stride_w 1 take the reduction tap-major: a
@@ -170,8 +173,8 @@ int conv2d_fwd_f32_hw_workspace_bytes(int N, int C, int H, int W, int K, int R, 
  * rounding of its fp64 sum.  On fp64 MFMA (half the fp32 peak).  Separate
  * vertical and horizontal stride and padding as in conv2d_fwd_f32_hw.  When
  * the plan shares out the reduction of some tiles, their pieces' fp64 partial
- * sums go to a workspace taken from the library's stream-ordered pool (as
- * for conv2d_fwd_f32) and a second kernel adds them
+ * sums go to the workspace the library keeps for `stream` (as for
+ * conv2d_fwd_f32) and a second kernel adds them
  * in a fixed order in fp64 before the one rounding, so results are
  * deterministic run to run.  plan: NULL, or an override with the keys of
  * conv2d_fwd_f32_ex: tile=<MT>x<NT> (one of 128x128, 64x256, 256x64,
@@ -361,13 +364,18 @@ int conv2d_fwd_f32_noalloc(const float *x, const float *w, float *y,
                            int stride, int pad, int layout, void *stream);
 
 /* The workspaces that conv2d_fwd_f32 and conv2d_fwd_f32_acc64 take for
- * themselves come from one stream-ordered memory pool per device, which the library creates at the first such call
- * on that device.  Freed blocks stay in the pool for the next call (mapping
- * tens of MB afresh per call costs microseconds), so a pool holds the most
- * that calls on its device had in use at once.  This call returns to the
- * system every block of every pool that no call is using, and keeps the pools
- * for later calls.  Host call; work already queued is unaffected.  Returns
- * MG3M_OK, or MG3M_ERR_HIP with the HIP error text in mg3m_last_error(). */
+ * themselves come from one stream-ordered memory pool per device, which the
+ * library creates at the first such call on that device.  Each stream that is
+ * not being captured keeps one buffer from it (the largest its calls needed)
+ * for its later calls, up to 32 streams per device; calls on further streams,
+ * and captured calls, take a block per call and give it back on the stream.
+ * Freed blocks stay in the pool for the next call (mapping tens of MB afresh
+ * per call costs microseconds).  This call waits for the last call that used
+ * each such buffer, gives the buffers back to their pools (the next call on
+ * each stream takes a new one), then returns to the system every
+ * block of every pool that no call is using, and keeps the pools for later
+ * calls.  Blocking host call.  Returns MG3M_OK, or MG3M_ERR_HIP with the HIP
+ * error text in mg3m_last_error(). */
 int mg3m_trim_workspace_pool(void);
 
 #ifdef __cplusplus

@@ -4,6 +4,7 @@
 // rejected call writes nothing.  No exception crosses the interface.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
@@ -13,6 +14,7 @@
 #include <string>
 #include <unordered_map>
 #include <utility>
+#include <vector>
 
 #include "mg3m.h"
 #include "mg3m_internal.h"
@@ -151,6 +153,120 @@ int workspace_pool(void* stream, hipMemPool_t* pool, std::string* err) {
   return MG3M_OK;
 }
 
+// Above the pool sits one grow-only workspace per (device, stream handle) for
+// streams that are not being captured: each call on a stream reuses the
+// buffer the last call there left, so the steady state neither allocates nor
+// frees.  (Taking and giving back a pool block per call made
+// hipMallocFromPoolAsync wait for the stream's queued work whenever the last
+// block was freed by a call not yet run, which kept the host from running
+// ahead: 300-600 us per call on the ResNet-50 layers.)  Each buffer carries
+// the event recorded after the last call that used it, and a call first makes
+// its stream wait for that event: on the same stream this orders nothing new,
+// and if a destroyed stream's handle comes back for a new stream, the new
+// stream's calls still start after the old ones.  A larger plan frees the old
+// buffer on the stream (after that wait) and takes a larger one.  The lock is
+// held from the lookup until the call's launches and its event are queued.
+// At most kWsStreamsPerDevice streams per device get a buffer, later ones
+// use the pool per call; captured calls use the pool too, whose blocks the
+// graph then owns.
+constexpr int kWsStreamsPerDevice = 32;
+struct WsCache {
+  struct Entry {
+    int dev;
+    void* stream;
+    void* ptr;
+    size_t bytes;
+    hipEvent_t last;      // recorded after the last call that used ptr
+  };
+  std::mutex mu;
+  std::vector<Entry> entries;
+};
+WsCache& ws_cache() {
+  static WsCache* c = new WsCache();   // never destroyed, like the pools
+  return *c;
+}
+
+// The workspace of one call.  Either the stream's cached buffer: *lock then
+// holds the cache and *done is the event the caller records on the stream
+// after its last launch; or (the stream is being captured, or the device
+// already has kWsStreamsPerDevice cached streams) a pool block that the
+// caller gives back with hipFreeAsync (*done = nullptr).
+int own_workspace_for(void* stream, size_t bytes, float** ws, hipEvent_t* done,
+                      std::unique_lock<std::mutex>* lock, std::string* err) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  *done = nullptr;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(st, &cap);
+  if (e != hipSuccess) {
+    *err = std::string("hipStreamIsCapturing: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  int dev = 0;
+  e = st != nullptr ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    *err = std::string("device of the stream: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  hipMemPool_t pool = nullptr;
+  if (int rc = workspace_pool(stream, &pool, err)) return rc;
+  if (cap == hipStreamCaptureStatusNone) {
+    WsCache& c = ws_cache();
+    std::unique_lock<std::mutex> lk(c.mu);
+    WsCache::Entry* hit = nullptr;
+    int on_dev = 0;
+    for (auto& en : c.entries) {
+      if (en.dev == dev && en.stream == stream) hit = &en;
+      on_dev += en.dev == dev;
+    }
+    if (hit == nullptr && on_dev < kWsStreamsPerDevice) {
+      hipEvent_t ev = nullptr;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) {
+        *err = std::string("hipEventCreateWithFlags: ") + hipGetErrorString(e);
+        return MG3M_ERR_HIP;
+      }
+      c.entries.push_back({dev, stream, nullptr, 0, ev});
+      hit = &c.entries.back();
+    } else if (hit != nullptr) {
+      e = hipStreamWaitEvent(st, hit->last, 0);
+      if (e != hipSuccess) {
+        *err = std::string("hipStreamWaitEvent: ") + hipGetErrorString(e);
+        return MG3M_ERR_HIP;
+      }
+    }
+    if (hit != nullptr) {
+      if (hit->bytes < bytes) {
+        if (hit->ptr != nullptr) {
+          e = hipFreeAsync(hit->ptr, st);      // after every call that used it
+          if (e != hipSuccess) {
+            *err = std::string("hipFreeAsync: ") + hipGetErrorString(e);
+            return MG3M_ERR_HIP;
+          }
+          hit->ptr = nullptr;
+          hit->bytes = 0;
+        }
+        e = hipMallocFromPoolAsync(&hit->ptr, bytes, pool, st);
+        if (e != hipSuccess) {
+          hit->ptr = nullptr;
+          *err = std::string("hipMallocFromPoolAsync: ") + hipGetErrorString(e);
+          return MG3M_ERR_HIP;
+        }
+        hit->bytes = bytes;
+      }
+      *ws = static_cast<float*>(hit->ptr);
+      *done = hit->last;
+      *lock = std::move(lk);
+      return MG3M_OK;
+    }
+  }
+  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(ws), bytes, pool, st);
+  if (e != hipSuccess) {
+    *err = std::string("hipMallocFromPoolAsync: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  return MG3M_OK;
+}
+
 int run(const float* x, const float* w, float* y, const Geom& g, void* workspace,
         size_t workspace_bytes, bool own_workspace, const char* plan, void* stream,
         const float* add = nullptr, int relu = 0) {
@@ -173,14 +289,14 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     return fail(MG3M_ERR_ALIAS, "add partly overlaps y");
 
   float* ws = nullptr;
+  bool pooled = false;                       // ws is a pool block to give back after the launches
+  hipEvent_t ws_done = nullptr;              // else, with own_workspace: recorded after the launches
+  std::unique_lock<std::mutex> ws_lock;      // holds the per-stream workspace until then
   if (p.ws_bytes > 0) {
     if (own_workspace) {
-      hipMemPool_t pool = nullptr;
       std::string perr;
-      if (int prc = workspace_pool(stream, &pool, &perr)) return fail(prc, perr);
-      hipError_t e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), p.ws_bytes, pool,
-                                            static_cast<hipStream_t>(stream));
-      if (e != hipSuccess) return fail(MG3M_ERR_HIP, std::string("hipMallocFromPoolAsync: ") + hipGetErrorString(e));
+      if (int prc = own_workspace_for(stream, p.ws_bytes, &ws, &ws_done, &ws_lock, &perr)) return fail(prc, perr);
+      pooled = ws_done == nullptr;
     } else {
       if (workspace == nullptr || workspace_bytes < p.ws_bytes)
         return fail(MG3M_ERR_WORKSPACE, "plan needs " + std::to_string(p.ws_bytes) + " workspace bytes");
@@ -235,7 +351,15 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     r.relu = relu;
     rc = mg3m::launch_tail_reduce(r, stream, &err);
   }
-  if (own_workspace && ws != nullptr) {
+  if (ws_done != nullptr) {
+    // recorded even after a failed launch: a later call waits for what was queued
+    hipError_t e = hipEventRecord(ws_done, static_cast<hipStream_t>(stream));
+    if (rc == MG3M_OK && e != hipSuccess) {
+      rc = MG3M_ERR_HIP;
+      err = std::string("hipEventRecord: ") + hipGetErrorString(e);
+    }
+  }
+  if (pooled) {
     hipError_t e = hipFreeAsync(ws, static_cast<hipStream_t>(stream));
     if (rc == MG3M_OK && e != hipSuccess) {
       rc = MG3M_ERR_HIP;
@@ -538,6 +662,29 @@ const char* mg3m_last_error(void) { return g_last_error.c_str(); }
 
 int mg3m_trim_workspace_pool(void) {
   g_last_error.clear();
+  {
+    // per-stream buffers: wait for the last call that used each, then give
+    // it back (its stream may be gone, so not stream-ordered)
+    WsCache& c = ws_cache();
+    std::lock_guard<std::mutex> lock(c.mu);
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    for (auto& en : c.entries) {
+      if (e == hipSuccess) e = hipEventSynchronize(en.last);
+      if (e == hipSuccess) e = hipSetDevice(en.dev);
+      if (e == hipSuccess && en.ptr != nullptr) e = hipFreeAsync(en.ptr, nullptr);
+      if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+      if (e == hipSuccess) e = hipEventDestroy(en.last);
+      if (e != hipSuccess) break;
+      en.last = nullptr;
+    }
+    if (e == hipSuccess) e = hipSetDevice(cur);
+    c.entries.erase(std::remove_if(c.entries.begin(), c.entries.end(),
+                                   [](const WsCache::Entry& en) { return en.last == nullptr; }),
+                    c.entries.end());
+    if (e != hipSuccess) return fail(MG3M_ERR_HIP, std::string("freeing the per-stream workspaces: ") +
+                                                       hipGetErrorString(e));
+  }
   WsPools& wp = ws_pools();
   std::lock_guard<std::mutex> lock(wp.mu);
   for (auto& kv : wp.pools) {

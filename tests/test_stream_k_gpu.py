@@ -155,3 +155,87 @@ def test_workspace_pool_reuse_and_trim():
     Kg = SK_SMALL[1] * SK_SMALL[5] * SK_SMALL[6]
     assert_parity_acc64(run_gpu(x, w, st, pd, "HWCN", acc64=True), acc, mag, Kg, "acc64 after trim")
     mg3m.mg3m_trim_workspace_pool()
+
+
+def _launch_plain(case, stream):
+    """conv2d_fwd_f32 of one prepared case on `stream`, into a fresh output
+    made on that stream."""
+    import torch
+    (N, C, H, W, K, R, S, st, pd), xd, wd = case[0], case[1], case[2]
+    Ho, Wo = mg3m.conv2d_out_dims(H, W, R, S, st, pd)
+    with torch.cuda.stream(stream):
+        y = torch.full((Ho, Wo, K, N), float("nan"), dtype=torch.float32, device="cuda")
+    mg3m.conv2d_fwd_f32(xd, wd, y, N, C, H, W, K, R, S, st, pd, "HWCN", stream=stream)
+    return y
+
+
+def _plain_cases(seed):
+    shapes = [SK_SMALL, (8, 256, 14, 14, 256, 3, 3, 1, 1), SK_SMALL, SK_SCALAR]
+    cases = []
+    for i, shape in enumerate(shapes):
+        info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN")
+        assert info["workspace_bytes"] > 0, info
+        x, w, st, pd = make(shape, seed + i, "HWCN")
+        acc, mag = oracle.conv2d(x, w, st, pd, "HWCN")
+        cases.append((shape, to_dev(x), to_dev(w), acc, mag))
+    return cases
+
+
+def test_workspace_per_stream():
+    """conv2d_fwd_f32 keeps one workspace per stream and reuses it: calls
+    queued on two streams at once, each stream's buffer grown while earlier
+    calls that use it are still queued, more streams than get a buffer of
+    their own (those take a pool block per call), and new buffers after the
+    trim call has given the old ones back."""
+    import torch
+    cases = _plain_cases(800)
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    extra = [torch.cuda.Stream() for _ in range(34)]
+    torch.cuda.synchronize()
+    jobs = []
+    for rep in range(2):
+        for k, s in enumerate(streams):
+            for i in range(len(cases)):
+                c = cases[(i + k) % len(cases)]
+                jobs.append((c, _launch_plain(c, s)))
+    for j, s in enumerate(extra):
+        c = cases[j % len(cases)]
+        jobs.append((c, _launch_plain(c, s)))
+    say(f"{len(jobs)} calls queued on {len(streams) + len(extra)} streams")
+    torch.cuda.synchronize()
+    for (shape, _, _, acc, mag), y in jobs:
+        assert_parity(y.cpu().numpy(), acc, mag, f"{shape}")
+    mg3m.mg3m_trim_workspace_pool()
+    for c in cases[:2]:
+        y = _launch_plain(c, streams[0])
+        torch.cuda.synchronize()
+        assert_parity(y.cpu().numpy(), c[3], c[4], f"after trim {c[0]}")
+
+
+def test_workspace_under_graph_capture():
+    """A captured conv2d_fwd_f32 takes its workspace from the pool inside the
+    graph, not from the stream's buffer; every replay, with eager calls on
+    the same stream between them, equals the eager result bit for bit."""
+    import torch
+    cases = _plain_cases(820)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    c = cases[1]
+    (N, C, H, W, K, R, S, st, pd), xd, wd = c[0], c[1], c[2]
+    y = _launch_plain(c, s)                    # the stream's buffer, sized for this shape
+    torch.cuda.synchronize()
+    assert_parity(y.cpu().numpy(), c[3], c[4], "eager")
+    ref = y.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        mg3m.conv2d_fwd_f32(xd, wd, y, N, C, H, W, K, R, S, st, pd, "HWCN", stream=s)
+    for rep in range(3):
+        other = _launch_plain(cases[3], s)     # eager work on the stream's own buffer
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), f"replay {rep}"
+        assert_parity(other.cpu().numpy(), cases[3][3], cases[3][4], f"eager call between replays {rep}")
+    del g
+    mg3m.mg3m_trim_workspace_pool()
