@@ -19,7 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmg3m.so")
-SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn_tap_dma.hip", "conv_hwcn_vecn.hip", "conv_hwcn_vecc.hip", "conv_hwcn_veca.hip", "conv_hwcn_scalar.hip",
+SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn_tap_dma.hip", "conv_hwcn_vecn_tap_dma_fused.hip", "conv_hwcn_vecn.hip", "conv_hwcn_vecc.hip", "conv_hwcn_veca.hip", "conv_hwcn_scalar.hip",
            "conv_nchw.hip", "conv_acc64_hwcn_tap.hip", "conv_acc64_hwcn.hip", "conv_acc64_nchw.hip",
            "conv_hwcn_vecn_tap_fused.hip", "conv_hwcn_vecn_fused.hip", "conv_hwcn_other_fused.hip",
            "conv_nchw_fused.hip", "conv_nchw_tap.hip", "conv_nchw_tap_fused.hip", "conv_hwcn_persist.hip", "conv_hwcn_persist_fused.hip",

@@ -1270,6 +1270,8 @@ template <int LAYOUT, class C, bool FUSE = false>
 __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&acc)[C::TM][C::TN], int m0, int n0,
                                                    int wm, int wn, int hh, int q) {
   const __amdgpu_buffer_rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+  const bool has_add = FUSE && a.add != nullptr;
+  const __amdgpu_buffer_rsrc_t ar = make_rsrc(has_add ? a.add : a.y, a.y_bytes);
   // opaque here, so that the row offsets below are formed where the stores
   // use them (hoisted out of the persistent kernel's loop over tiles, their
   // products spilled scalar registers)
@@ -1291,12 +1293,15 @@ __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&ac
         for (int e = 0; e < 4; ++e) {
           const int r = i * 32 + 8 * g + e;         // row offset from the lane's first row
           const bool ok = col_ok & (r < rows_left);
+          const unsigned off = ok ? o + (unsigned)e * rs4 : kOOB;
           float v = acc[i][j][4 * g + e];
-          // fused output stage (add read only where the output element exists)
           if constexpr (FUSE) {
-            if (ok) v = finish1(a, v, (int)((o + (unsigned)e * rs4) / 4u));
+            // fused output stage: add (same layout as y) read through its own
+            // buffer resource at the store's offset; ReLU keeps NaN
+            if (has_add) v += bload1(ar, off);
+            if (a.relu != 0 && v < 0.f) v = 0.f;
           }
-          bstore1(yr, ok ? o + (unsigned)e * rs4 : kOOB, 0u, v);
+          bstore1(yr, off, 0u, v);
         }
       }
   }
@@ -1312,8 +1317,27 @@ __device__ __forceinline__ void store_tile_f32_buf(const KArgs& a, floatx16 (&ac
 // the fused stage works on the accumulators in VGPRs, and the compiler copies
 // all of them out of the AGPRs at once, which in a shared kernel would cost
 // the plain convolution a wave per SIMD.
+// Waves per SIMD that the tile's plain kernel reaches with its registers and
+// LDS (the planner's occupancy model).  The fused direct-to-LDS kernels are
+// held to the same (left alone, the add loads of their epilogue took them to
+// 140 registers, a wave per SIMD fewer); they need no staging registers, so
+// the bound costs no spills.
+constexpr int plain_waves_per_simd(int mt, int nt, int kt, int wm, int wn) {
+  for (int i = 0; i < kNumTiles; ++i) {
+    const TileDesc& d = kTiles[i];
+    if (d.mt == mt && d.nt == nt && d.kt == kt && d.wm == wm && d.wn == wn && d.m16 == 0) {
+      const int by_regs = 512 / ((d.regs + 7) / 8 * 8);
+      const int by_lds = 160 * 1024 / lds_bytes_for(d) * d.wm * d.wn / 4;
+      const int w = by_regs < by_lds ? by_regs : by_lds;
+      return w < 1 ? 1 : (w < 8 ? w : 8);
+    }
+  }
+  return 1;
+}
+
 template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
 __global__ __launch_bounds__(WM * WN * 64)
+__attribute__((amdgpu_waves_per_eu(FUSE && BM == kBVecNTapDma ? plain_waves_per_simd(MT, NT, KT, WM, WN) : 1)))
 void conv_igemm_f32(KArgs a) {
   using C = Cfg<MT, NT, KT, WM, WN>;
   __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
@@ -1328,7 +1352,7 @@ void conv_igemm_f32(KArgs a) {
       [&](floatx16 (&acc)[C::TM][C::TN], int m0, int n0, int wm, int wn, int hh, int q) {
         // the direct-to-LDS path (HWCN, N % 4 == 0: element stores) stores
         // through a buffer resource: branch-free, 2.4% faster on VGG-16 conv3
-        if constexpr (BM == kBVecNTapDma && !FUSE) store_tile_f32_buf<LAYOUT, C>(a, acc, m0, n0, wm, wn, hh, q);
+        if constexpr (BM == kBVecNTapDma) store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, m0, n0, wm, wn, hh, q);
         else store_tile_f32<LAYOUT, C, FUSE>(a, acc, m0, n0, wm, wn, hh, q);
       });
 }

@@ -113,8 +113,8 @@ static KernelFn kernel_for(int variant, int tile) {
 // loaders, whose fused kernel runs them.
 static KernelFn kernel_fused_for(int variant, int tile) {
   switch (variant) {
-    case kVarHwcnVecNTap:
-    case kVarHwcnVecNTapDma: return conv_kernel_hwcn_vecn_tap_fused(tile);
+    case kVarHwcnVecNTap: return conv_kernel_hwcn_vecn_tap_fused(tile);
+    case kVarHwcnVecNTapDma: return conv_kernel_hwcn_vecn_tap_dma_fused(tile);
     case kVarHwcnVecN: return conv_kernel_hwcn_vecn_fused(tile);
     case kVarHwcnVecC:
     case kVarHwcnVecA:

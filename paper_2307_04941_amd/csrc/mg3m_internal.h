@@ -262,6 +262,7 @@ using KernelFn = void (*)(KArgs);
 KernelFn conv_kernel_hwcn_vecn(int tile);
 KernelFn conv_kernel_hwcn_vecn_tap(int tile);
 KernelFn conv_kernel_hwcn_vecn_tap_dma(int tile);   // conv_hwcn_vecn_tap_dma.hip
+KernelFn conv_kernel_hwcn_vecn_tap_dma_fused(int tile);   // conv_hwcn_vecn_tap_dma_fused.hip
 KernelFn conv_kernel_hwcn_vecc(int tile);
 KernelFn conv_kernel_hwcn_veca(int tile);
 KernelFn conv_kernel_hwcn_scalar(int tile);

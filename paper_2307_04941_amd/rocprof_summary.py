@@ -77,6 +77,8 @@ def copy_scale(rows, known_kib: float):
 
 FAMILIES = [("conv_igemm_f32<", ", false>", "convolution (fp32, plain output)"),
             ("conv_igemm_f32<", ", true>", "convolution (fp32, fused add/ReLU)"),
+            ("conv_igemm_f32_pt<", ", false>", "convolution (fp32, persistent, plain output)"),
+            ("conv_igemm_f32_pt<", ", true>", "convolution (fp32, persistent, fused add/ReLU)"),
             ("conv_igemm_f32_m16<", ", false>", "convolution (fp32, 16-row tile, plain output)"),
             ("conv_igemm_f32_m16<", ", true>", "convolution (fp32, 16-row tile, fused add/ReLU)"),
             ("conv_igemm_acc64<", "", "convolution (fp64 accumulation)"),
