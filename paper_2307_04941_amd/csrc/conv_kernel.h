@@ -1390,9 +1390,8 @@ __device__ __forceinline__ void mma_stage_upto(floatx16 (&acc)[C::TM][C::TN], co
 // work-group's life is a stage or two of MFMAs and then a burst of output
 // stores, and work-groups that start together compute together and store
 // together, so the chip alternates between the two instead of overlapping
-// them.  Here gridDim.x work-groups each take tiles slot, slot + G, slot +
-// 2G, ... (G = gridDim.x, slot = xcd_group(blockIdx.x, G): every XCD takes a
-// contiguous block of each G consecutive tiles), and the stages of all of a
+// them.  Here gridDim.x work-groups each take every cnt-th tile of their
+// XCD's contiguous run of tiles (below), and the stages of all of a
 // work-group's tiles form one pipeline, one stage's loads in flight while
 // the previous stage's MFMAs run; the last stage of a tile loads the first
 // stage of the next one.  A tile's output stores are issued one stage later,
@@ -1407,9 +1406,19 @@ __global__ __launch_bounds__(WM * WN * 64)
 void conv_igemm_f32_pt(KArgs a) {
   using C = Cfg<MT, NT, KT, WM, WN>;
   __shared__ __attribute__((aligned(16))) float lds[C::LDS_FLOATS];
+  // Work-group i runs on XCD i % 8.  Each XCD takes one contiguous run of the
+  // tiles, in proportion to its work-groups, and its work-groups walk that
+  // run together: tiles lo + loc, lo + loc + cnt, ...  A band of cnt
+  // consecutive tiles is in flight per XCD at a time, and the next band
+  // starts where it ends, so the input rows the two share (a filter's halo)
+  // are still in that XCD's L2.
   const int G = (int)gridDim.x;
-  int tile = xcd_group(blockIdx.x, G);
-  if (tile >= a.dp_tiles) return;
+  const int q8 = G >> 3, r8 = G & 7, xcd = (int)(blockIdx.x & 7), loc = (int)(blockIdx.x >> 3);
+  const int cnt = q8 + (xcd < r8 ? 1 : 0);                               // work-groups on this XCD
+  const int rank0 = xcd < r8 ? xcd * (q8 + 1) : r8 * (q8 + 1) + (xcd - r8) * q8;
+  const int hi = (int)((long long)a.dp_tiles * (rank0 + cnt) / G);
+  int tile = (int)((long long)a.dp_tiles * rank0 / G) + loc;
+  if (tile >= hi) return;
 
   const int t = threadIdx.x;
   float* const As0 = lds;
@@ -1447,7 +1456,7 @@ void conv_igemm_f32_pt(KArgs a) {
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   };
   for (;;) {
-    const int next = tile + G;
+    const int next = tile + cnt;
     if (nk > 1) {
       // stage 0 (staged in buffer cur), stage 1's loads in flight; then the
       // previous tile's stores
@@ -1482,7 +1491,7 @@ void conv_igemm_f32_pt(KArgs a) {
     }
     // the last stage: its loads are the next tile's first stage; with one
     // stage per tile, the previous tile's stores go out after them
-    const bool fetch = next < a.dp_tiles;
+    const bool fetch = next < hi;
     if (fetch) {
       al.init(a, t, (next % a.tiles_m) * MT, 0);
       bl.init(a, t, (next / a.tiles_m) * NT, 0);
