@@ -43,6 +43,14 @@
  * launch fail that way (nothing is launched), for testing callers' error
  * paths.  No C++ exception crosses this interface.  Calls on different streams may run
  * concurrently from different host threads.
+ *
+ * Environment (read at each call that plans a shape):
+ *   MG3M_FORCE_PLAN=<override>  applied wherever a call passes no override
+ *       (plan NULL, and the plain entry points): the override syntax of
+ *       conv2d_fwd_f32_ex.  A forced plan that does not apply to a shape
+ *       fails that call with MG3M_ERR_PLAN, naming the variable.
+ *   MG3M_LOG=1  prints each plan once to stderr, when the library first
+ *       makes it for a shape, alignment and override.
  */
 #ifndef MG3M_H
 #define MG3M_H
@@ -112,8 +120,7 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    64x128, 128x64, 64x64, 32x128, 32x64, 128x32, 64x32,
  *                    256x128, 128x256, 128x128 with kt=32, 16x64 (16x16x4
  *                    MFMAs; the selector takes it only when K mod 32 is 1..16),
- *                    and 64x64 with kt=32 (four 32x32 waves; reached only
- *                    through this override, never by the selector)
+ *                    and 64x64 with kt=32 (four 32x32 waves)
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
  *   split=<n>        share every tile's reduction out over n work-groups per tile
  *                    (1..64, clamped to the tile's k-tiles; 1 = no split)

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <exception>
 #include <functional>
@@ -72,8 +73,21 @@ PlanCache& plan_cache() {
 }
 constexpr size_t kPlanCacheMax = 4096;
 
+// MG3M_FORCE_PLAN stands in for a missing override; MG3M_LOG=1 reports each
+// new plan on stderr.
+const char* forced_plan() {
+  const char* e = std::getenv("MG3M_FORCE_PLAN");
+  return (e != nullptr && *e != 0) ? e : nullptr;
+}
+bool log_plans() {
+  const char* e = std::getenv("MG3M_LOG");
+  return e != nullptr && *e != 0 && std::strcmp(e, "0") != 0;
+}
+
 int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16,
                    mg3m::ConvShape* s, mg3m::Plan* p) {
+  const char* forced = plan == nullptr ? forced_plan() : nullptr;
+  if (forced != nullptr) plan = forced;
   PlanKey key{{g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout,
                (g.acc64 ? 1 : 0), (x16 ? 4 : 0) | (w16 ? 2 : 0) | (y16 ? 1 : 0),
                (int)(uint32_t)((uint64_t)g.ws_cap >> 32), (int)(uint32_t)g.ws_cap},
@@ -92,7 +106,12 @@ int shape_and_plan(const Geom& g, const char* plan, bool x16, bool w16, bool y16
   int rc = mg3m::make_shape(g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw, g.layout, s, &err);
   if (rc) return fail(rc, err);
   rc = mg3m::make_plan(*s, plan, g.acc64, x16, w16, y16, p, &err, g.ws_cap);
-  if (rc) return fail(rc, err);
+  if (rc) return fail(rc, forced != nullptr ? err + " (plan forced by MG3M_FORCE_PLAN)" : err);
+  if (log_plans())
+    std::fprintf(stderr, "mg3m plan: N=%d C=%d H=%d W=%d K=%d R=%d S=%d stride=%dx%d pad=%dx%d %s%s%s: %s\n",
+                 g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.sh, g.sw, g.ph, g.pw,
+                 g.layout == mg3m::kHWCN ? "HWCN" : "NCHW", g.acc64 ? " acc64" : "",
+                 forced != nullptr ? " (MG3M_FORCE_PLAN)" : "", mg3m::plan_to_string(*s, *p).c_str());
   std::lock_guard<std::mutex> lock(cache.mu);
   if (cache.map.size() >= kPlanCacheMax) cache.map.clear();
   cache.map.emplace(std::move(key), std::make_pair(*s, *p));

@@ -578,3 +578,45 @@ def test_selector_picks_persistent_and_deep_64x64_tiles():
     for L in workloads.workload("vgg16_n64")[1:]:
         p = mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
         assert p["persistent"] == 0 and (p["mt"], p["kt"]) != (64, 32), (L.name, p)
+
+
+def test_force_plan_environment(monkeypatch):
+    """MG3M_FORCE_PLAN stands in for a missing override (plain calls and
+    plan queries), an explicit override still wins, and a forced plan that
+    does not apply fails with MG3M_ERR_PLAN naming the variable."""
+    shape = (8, 64, 28, 28, 128, 3, 3, 1, 1)
+    chosen = mg3m.conv2d_fwd_f32_plan_string(*shape, "HWCN")
+    assert not chosen.startswith("tile=32x64,"), chosen
+    monkeypatch.setenv("MG3M_FORCE_PLAN", "tile=32x64,split=3")
+    forced = mg3m.conv2d_fwd_f32_plan_string(*shape, "HWCN")
+    assert forced.startswith("tile=32x64,") and ",split=3," in forced, forced
+    explicit = mg3m.conv2d_fwd_f32_plan_string(*shape, "HWCN", "tile=128x128")
+    assert explicit.startswith("tile=128x128,"), explicit
+    monkeypatch.setenv("MG3M_FORCE_PLAN", "tile=48x48")
+    with pytest.raises(mg3m.Mg3mError) as e:
+        mg3m.conv2d_fwd_f32_plan_string(*shape, "HWCN")
+    assert e.value.status == 7 and "MG3M_FORCE_PLAN" in str(e.value)
+    monkeypatch.delenv("MG3M_FORCE_PLAN")
+    assert mg3m.conv2d_fwd_f32_plan_string(*shape, "HWCN") == chosen
+
+
+def test_log_prints_each_new_plan_once():
+    """MG3M_LOG=1: one stderr line per plan the library makes, none for a
+    plan it already holds."""
+    import subprocess
+    code = ("from paper_2307_04941_amd import mg3m\n"
+            "for _ in range(3):\n"
+            "    mg3m.conv2d_fwd_f32_plan_string(4, 16, 12, 12, 32, 3, 3, 1, 1, 'HWCN')\n"
+            "mg3m.conv2d_fwd_f32_plan_string(4, 16, 12, 12, 32, 3, 3, 1, 1, 'NCHW')\n")
+    env = dict(os.environ, MG3M_LOG="1")
+    env.pop("MG3M_FORCE_PLAN", None)
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                         timeout=120)
+    assert out.returncode == 0, out.stderr
+    lines = [ln for ln in out.stderr.splitlines() if ln.startswith("mg3m plan:")]
+    assert len(lines) == 2, out.stderr
+    assert "HWCN" in lines[0] and "NCHW" in lines[1] and "tile=" in lines[0], lines
+    env["MG3M_LOG"] = "0"
+    quiet = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                           timeout=120)
+    assert quiet.returncode == 0 and "mg3m plan:" not in quiet.stderr
