@@ -1,6 +1,7 @@
 """Build libmg3m.so (the HIP kernels, the planner and the C ABI) for gfx950.
 
-    python -m paper_2307_04941_amd.build
+    python -m paper_2307_04941_amd.build                 # libmg3m.so
+    python -m paper_2307_04941_amd.build --lds-poison    # debug/libmg3m_lds_poison.so
 
 Compiles in-tree with hipcc; the shared library lands next to this file.
 """
@@ -141,23 +142,36 @@ def write_kernel_digests(objs, tmp) -> dict:
     return table
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    """Compile every source and link libmg3m.so; returns its path."""
+# Debug build with every LDS stage poisoned with NaN once consumed (see
+# poison_stage in csrc/conv_kernel.h); tests/test_lds_poison_gpu.py runs
+# parity cases on it when it is built.
+LIB_LDS_POISON = os.path.join(PKG, "debug", "libmg3m_lds_poison.so")
+
+
+def build(verbose: bool = False, extra=(), lds_poison: bool = False) -> str:
+    """Compile every source and link libmg3m.so (or, lds_poison, the debug
+    library LIB_LDS_POISON); returns its path."""
+    lib = LIB_LDS_POISON if lds_poison else LIB
+    if lds_poison:
+        extra = (*extra, "-DMG3M_LDS_POISON=1")
+        os.makedirs(os.path.dirname(lib), exist_ok=True)
     with tempfile.TemporaryDirectory(prefix="mg3m_build_") as tmp:
         objs = [os.path.join(tmp, s + ".o") for s in SOURCES]
         with concurrent.futures.ThreadPoolExecutor(len(SOURCES)) as ex:
             list(ex.map(lambda so: _compile(so[0], so[1], extra), zip(SOURCES, objs)))
-        write_kernel_digests(objs, tmp)
-        out_tmp = LIB + ".tmp"
+        if not lds_poison:
+            write_kernel_digests(objs, tmp)
+        out_tmp = lib + ".tmp"
         cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out_tmp, *objs]
         p = subprocess.run(cmd, capture_output=True, text=True)
         if p.returncode != 0:
             raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{p.stdout}\n{p.stderr}")
-        os.replace(out_tmp, LIB)
+        os.replace(out_tmp, lib)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {lib}")
+    return lib
 
 
 if __name__ == "__main__":
-    build(verbose=True, extra=sys.argv[1:])
+    args = sys.argv[1:]
+    build(verbose=True, extra=[a for a in args if a != "--lds-poison"], lds_poison="--lds-poison" in args)

@@ -480,6 +480,24 @@ struct BVecNTapDma {
   }
 };
 
+// Debug build (-DMG3M_LDS_POISON=1, `build --lds-poison`): at the start of
+// every stage the LDS buffer that the previous stage consumed is filled with
+// NaN, behind a barrier, before it is staged again.  A read that some missing
+// barrier lets through then returns NaN (and the output shows it) instead of
+// a stale stage's values.  Off in the product build.
+#ifndef MG3M_LDS_POISON
+#define MG3M_LDS_POISON 0
+#endif
+template <class C>
+__device__ __forceinline__ void poison_stage(float* As, float* Bs) {
+  if constexpr (MG3M_LDS_POISON != 0) {
+    const float nan = __builtin_nanf("");
+    for (int i = (int)threadIdx.x; i < C::A_STAGE; i += C::T) As[i] = nan;
+    for (int i = (int)threadIdx.x; i < C::B_STAGE; i += C::T) Bs[i] = nan;
+    __syncthreads();
+  }
+}
+
 // s_waitcnt with only the vector-memory count at zero (gfx9 encoding:
 // vmcnt[3:0] in bits 3:0 and vmcnt[5:4] in bits 15:14 = 0, expcnt bits 6:4
 // and lgkmcnt bits 11:8 at their maxima, i.e. not waited on).
@@ -500,6 +518,7 @@ __device__ __forceinline__ void run_stages_dma(const KArgs& a, AL& al, BL& bl, f
   __syncthreads();
   auto step = [&](auto cur_c) {
     constexpr int CUR = decltype(cur_c)::value;
+    poison_stage<C>(As0 + (CUR ^ 1) * C::A_STAGE, Bs0 + (CUR ^ 1) * C::B_STAGE);
     al.advance(a);
     bl.advance(a);
     al.load(a, wr, As0 + (CUR ^ 1) * C::A_STAGE);
@@ -1006,6 +1025,7 @@ __device__ __forceinline__ void run_stages(const KArgs& a, AL& al, BL& bl, float
   __syncthreads();
   auto step = [&](auto cur_c) {
     constexpr int CUR = decltype(cur_c)::value;
+    poison_stage<C>(As0 + (CUR ^ 1) * C::A_STAGE, Bs0 + (CUR ^ 1) * C::B_STAGE);
     al.advance(a);
     bl.advance(a);
     al.load(a, wr);
@@ -1460,6 +1480,7 @@ void conv_igemm_f32_pt(KArgs a) {
     if (nk > 1) {
       // stage 0 (staged in buffer cur), stage 1's loads in flight; then the
       // previous tile's stores
+      poison_stage<C>(As0 + (cur ^ 1) * C::A_STAGE, Bs0 + (cur ^ 1) * C::B_STAGE);
       al.advance(a);
       bl.advance(a);
       al.load(a, wr);
@@ -1476,6 +1497,7 @@ void conv_igemm_f32_pt(KArgs a) {
       cur ^= 1;
       // stages 1 .. nk-2
       for (int it = 1; it + 1 < nk; ++it) {
+        poison_stage<C>(As0 + (cur ^ 1) * C::A_STAGE, Bs0 + (cur ^ 1) * C::B_STAGE);
         al.advance(a);
         bl.advance(a);
         al.load(a, wr);
@@ -1492,6 +1514,7 @@ void conv_igemm_f32_pt(KArgs a) {
     // the last stage: its loads are the next tile's first stage; with one
     // stage per tile, the previous tile's stores go out after them
     const bool fetch = next < hi;
+    poison_stage<C>(As0 + (cur ^ 1) * C::A_STAGE, Bs0 + (cur ^ 1) * C::B_STAGE);
     if (fetch) {
       al.init(a, t, (next % a.tiles_m) * MT, 0);
       bl.init(a, t, (next / a.tiles_m) * NT, 0);

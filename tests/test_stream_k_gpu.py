@@ -239,3 +239,35 @@ def test_workspace_under_graph_capture():
         assert_parity(other.cpu().numpy(), cases[3][3], cases[3][4], f"eager call between replays {rep}")
     del g
     mg3m.mg3m_trim_workspace_pool()
+
+
+def test_workspace_per_stream_from_host_threads():
+    """Host threads calling conv2d_fwd_f32 at once, each on its own stream
+    (and two of them sharing one): every result equals the oracle's."""
+    import threading
+    import torch
+    cases = _plain_cases(840)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    torch.cuda.synchronize()
+    results, errors = [], []
+
+    def worker(k):
+        try:
+            s = streams[min(k, 2)]          # threads 2 and 3 share a stream
+            for i in range(6):
+                c = cases[(i + k) % len(cases)]
+                results.append((c, _launch_plain(c, s)))
+        except Exception as e:               # reported below, on the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not errors, errors
+    torch.cuda.synchronize()
+    say(f"{len(results)} calls from 4 host threads")
+    assert len(results) == 24
+    for (shape, _, _, acc, mag), y in results:
+        assert_parity(y.cpu().numpy(), acc, mag, f"{shape}")
