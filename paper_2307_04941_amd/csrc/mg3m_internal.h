@@ -93,8 +93,8 @@ constexpr int kNumTiles = 15;
 inline constexpr TileDesc kTiles[kNumTiles] = {
     // mt,  nt, kt, wm, wn, regs, eff,  m16, forced, eff_multitap, regs_pt {vec_n, vec_n_tap}
     {128, 128, 16, 2, 2, 116, 0.913, 0, 0, 1.0, {136, 121}},  // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 116, 0.865, 0, 0, 1.0, {157, 125}},   // 1: four waves sharing one filter tile (TB(1,8)-like)
-    {256, 64, 16, 4, 1, 120, 0.891, 0, 0, 1.0, {133, 125}},   // 2: four waves sharing one patch tile
+    {64, 256, 16, 1, 4, 116, 0.865, 0, 0, 1.0, {158, 125}},   // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {256, 64, 16, 4, 1, 120, 0.891, 0, 0, 1.0, {134, 125}},   // 2: four waves sharing one patch tile
     {64, 128, 16, 1, 2, 120, 0.890, 0, 0, 1.0, {161, 129}},   // 3
     {128, 64, 16, 2, 1, 128, 0.823, 0, 0, 1.0, {145, 129}},   // 4
     {64, 64, 16, 1, 1, 128, 0.740, 0, 0, 1.0, {163, 132}},    // 5: one wave per work-group (TB(1,1)-like)
