@@ -121,6 +121,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    256x128, 128x256, 128x128 with kt=32, 16x64 (16x16x4
  *                    MFMAs; the selector takes it only when K mod 32 is 1..16),
  *                    and 64x64 with kt=32 (four 32x32 waves)
+ *   waves=<WM>x<WN>  the work-group's wave grid (1..8 each), to pick among tiles
+ *                    of one shape (64x64 comes as 1x1 with kt=16 and 2x2 with
+ *                    kt=32), so the tile, waves and kt of a plan string read back
+ *                    as an override for the same tile
  *   kt=16|32         reduction depth staged per step (default 16 with a tile)
  *   split=<n>        share every tile's reduction out over n work-groups per tile
  *                    (1..64, clamped to the tile's k-tiles; 1 = no split)

@@ -88,6 +88,7 @@ double variant_factor(int variant) {
 
 struct Override {
   int mt = 0, nt = 0, kt = 0, split = 0, tail = 0, persist = 0, dma = -1;   // dma: -1 = the default
+  int wm = 0, wn = 0;                                                     // waves (0: any)
   long long sk = 0;
 };
 
@@ -132,6 +133,19 @@ int parse_override(const char* text, Override* o, std::string* err) {
         *err = "plan override: bad tile '" + val + "'";
         return MG3M_ERR_PLAN;
       }
+    } else if (key == "waves") {
+      size_t x = val.find('x');
+      char* e1 = nullptr;
+      char* e2 = nullptr;
+      const std::string a = x == std::string::npos ? std::string() : val.substr(0, x);
+      const std::string b = x == std::string::npos ? std::string() : val.substr(x + 1);
+      const long wm = std::strtol(a.c_str(), &e1, 10), wn = std::strtol(b.c_str(), &e2, 10);
+      if (a.empty() || b.empty() || *e1 != 0 || *e2 != 0 || wm < 1 || wm > 8 || wn < 1 || wn > 8) {
+        *err = "plan override: waves must be <WM>x<WN> (1..8 each)";
+        return MG3M_ERR_PLAN;
+      }
+      o->wm = (int)wm;
+      o->wn = (int)wn;
     } else if (key == "split") {
       long v = std::strtol(val.c_str(), &tail, 10);
       if (tail == val.c_str() || *tail != 0 || v < 1 || v > 64) {
@@ -455,11 +469,13 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   for (int ti = 0; ti < (acc64 ? kNumTiles64 : kNumTiles); ++ti) {
     const TileDesc& td = tile_desc(acc64, ti);
     if (o.mt && !(td.mt == o.mt && td.nt == o.nt)) continue;
+    if (o.wm && !(td.wm == o.wm && td.wn == o.wn)) continue;
     // The selector takes a 16-row tile only where it saves padding, i.e. a
     // 32-row block would be at most half full (the case it was timed on).
     if (!o.mt && td.m16 && !(s.Mg % 32 != 0 && s.Mg % 32 <= 16)) continue;
-    // A tile the cost model does not yet rank correctly is left to overrides.
-    if (!o.mt && td.forced_only) continue;
+    // A tile the cost model does not yet rank correctly is left to overrides
+    // that name its shape and its waves.
+    if (td.forced_only && !(o.mt && o.wm)) continue;
     // a forced tile without a depth means the default depth of 16
     if ((o.kt || o.mt) && td.kt != (o.kt ? o.kt : 16)) continue;
     if (o.split) {

@@ -620,3 +620,27 @@ def test_log_prints_each_new_plan_once():
     quiet = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
                            timeout=120)
     assert quiet.returncode == 0 and "mg3m plan:" not in quiet.stderr
+
+
+@pytest.mark.parametrize("bad", ["waves=2", "waves=2x", "waves=x2", "waves=0x2", "waves=9x1", "waves=2x2x2",
+                                 "waves=2 x2"])
+def test_override_waves_key(bad):
+    """waves=<WM>x<WN> picks among tiles of one shape by their wave grid, so
+    the tile part of a plan string (tile, waves, kt) reads back as an
+    override naming the same kernel tile; malformed values are rejected."""
+    shape = (32, 64, 56, 56, 256, 1, 1, 1, 0)
+    p = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "tile=64x64,waves=2x2,kt=32")
+    assert (p["mt"], p["nt"], p["kt"], p["waves_m"], p["waves_n"]) == (64, 64, 32, 2, 2), p
+    p = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "tile=64x64,waves=1x1")
+    assert (p["mt"], p["nt"], p["kt"], p["waves_m"], p["waves_n"]) == (64, 64, 16, 1, 1), p
+    for layer_shape in [(64, 256, 56, 56, 256, 3, 3, 1, 1), (32, 1024, 14, 14, 256, 1, 1, 1, 0), shape]:
+        text = mg3m.conv2d_fwd_f32_plan_string(*layer_shape, "HWCN")
+        head = ",".join(f for f in text.split(",") if f.split("=")[0] in ("tile", "waves", "kt"))
+        again = mg3m.conv2d_fwd_f32_plan_info(*layer_shape, "HWCN", head)
+        first = mg3m.conv2d_fwd_f32_plan_info(*layer_shape, "HWCN")
+        assert all(again[k] == first[k] for k in ("mt", "nt", "kt", "waves_m", "waves_n")), (head, again)
+    with pytest.raises(mg3m.Mg3mError) as ei:
+        mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", bad)
+    assert ei.value.status == 7, bad
+    with pytest.raises(mg3m.Mg3mError):
+        mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "tile=64x64,waves=3x1")
