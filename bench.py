@@ -318,7 +318,8 @@ def main():
 
     per_layer = []
     for j, (L, Ho, Wo) in enumerate(layers):
-        us = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j + 1][0]) for k in range(args.steps)])) * 1e3
+        us_steps = np.array([evs[k][j][0].elapsed_time(evs[k][j + 1][0]) for k in range(args.steps)]) * 1e3
+        us = float(np.mean(us_steps))
         kus = float(np.mean([evs[k][j][0].elapsed_time(evs[k][j][1]) for k in range(args.steps)])) * 1e3
         fl = layer_flops(L, Ho, Wo)
         by = layer_alg_bytes(L, Ho, Wo)
@@ -328,7 +329,8 @@ def main():
         attainable = min(PEAK_TFLOPS, ai * HBM_GBS / 1e3)
         per_layer.append({
             "layer": L.name, "N": L.N, "C": L.C, "H": L.H, "K": L.K, "R": L.R, "stride": L.stride,
-            "pad": L.pad, "us": round(us, 2), "kernel_us": round(kus, 2),
+            "pad": L.pad, "us": round(us, 2), "us_min": round(float(us_steps.min()), 2),
+            "us_p90": round(float(np.percentile(us_steps, 90)), 2), "kernel_us": round(kus, 2),
             "tflops": round(fl / us / 1e6, 2),
             "pct_peak": round(100 * fl / us / 1e6 / PEAK_TFLOPS, 1),
             "pct_roofline": round(100 * fl / us / 1e6 / attainable, 1),
@@ -339,7 +341,11 @@ def main():
             "flops": fl, "alg_bytes": by,
         })
         if cold is not None:
-            per_layer[-1]["cold_us"] = round(float(cold_layer[j]), 2)
+            cu = float(cold_layer[j])
+            per_layer[-1].update({
+                "cold_us": round(cu, 2), "cold_us_min": round(float(cold_us[:, j].min()), 2),
+                "cold_us_p90": round(float(np.percentile(cold_us[:, j], 90)), 2),
+                "cold_tflops": round(fl / cu / 1e6, 2), "cold_pct_peak": round(100 * fl / cu / 1e6 / PEAK_TFLOPS, 1)})
 
     # dominant kernel: the instantiation with the largest share of kernel time
     groups = {}
