@@ -238,8 +238,16 @@ int own_workspace_for(void* stream, size_t bytes, float** ws, hipEvent_t* done,
       on_dev += en.dev == dev;
     }
     if (hit == nullptr && on_dev < kWsStreamsPerDevice) {
+      // the event belongs to the stream's device, whichever device is current
       hipEvent_t ev = nullptr;
-      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      int cur = dev;
+      e = hipGetDevice(&cur);
+      if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (cur != dev) {
+        const hipError_t e2 = hipSetDevice(cur);
+        if (e == hipSuccess) e = e2;
+      }
       if (e != hipSuccess) {
         *err = std::string("hipEventCreateWithFlags: ") + hipGetErrorString(e);
         return MG3M_ERR_HIP;
