@@ -172,6 +172,28 @@ def build(verbose: bool = False, extra=(), lds_poison: bool = False) -> str:
     return lib
 
 
+# tests/c_abi_gpu.c: the C ABI called from plain C (no Python, no torch),
+# linked against the built library; tests/test_c_abi_gpu.py runs it.
+C_ABI_TEST = os.path.join(PKG, "debug", "c_abi_gpu")
+
+
+def build_c_abi_test(verbose: bool = False) -> str:
+    """Compile tests/c_abi_gpu.c with gcc against include/mg3m.h and link it
+    with the built libmg3m.so and ROCm's HIP runtime."""
+    os.makedirs(os.path.dirname(C_ABI_TEST), exist_ok=True)
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+           f"-I{INCLUDE}", "-I/opt/rocm/include", os.path.join(ROOT, "tests", "c_abi_gpu.c"),
+           "-o", C_ABI_TEST + ".tmp", f"-L{PKG}", "-lmg3m", "-L/opt/rocm/lib", "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath,/opt/rocm/lib"]
+    p = subprocess.run(cmd, capture_output=True, text=True)
+    if p.returncode != 0:
+        raise RuntimeError(f"gcc failed:\n{' '.join(cmd)}\n{p.stdout}\n{p.stderr}")
+    os.replace(C_ABI_TEST + ".tmp", C_ABI_TEST)
+    if verbose:
+        print(f"built {C_ABI_TEST}")
+    return C_ABI_TEST
+
+
 if __name__ == "__main__":
     args = sys.argv[1:]
     build(verbose=True, extra=[a for a in args if a != "--lds-poison"], lds_poison="--lds-poison" in args)
