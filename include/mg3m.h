@@ -273,10 +273,15 @@ int mg3m_net_create(const mg3m_layer *layers, int n_layers, int N, int C, int H,
 
 /* Shape of activation id (0 .. n_layers) and, for 1 .. n_layers-1, its device
  * pointer in the arena (NULL for the input and the output, which the caller
- * owns).  Host only.  ptr may be NULL. */
+ * owns).  Stored activations are HWCN ([H][W][C][N]) in every network: an
+ * NCHW network runs its layers in HWCN and changes layout only for x, y and
+ * its filters (copied once per forward pass).  Host only.  ptr may be NULL. */
 int mg3m_net_activation(const mg3m_net *net, int id, int *C, int *H, int *W, const float **ptr);
 
-/* Bytes of the activation arena and of the split-K workspace (host only). */
+/* Bytes of the activation arena (for an NCHW network including the HWCN
+ * copies of its input and output) and of the workspace (the split-K partials
+ * and, for an NCHW network, the [R][S][C][K] copies of its filters).  Host
+ * only. */
 int mg3m_net_memory(const mg3m_net *net, size_t *arena_bytes, size_t *workspace_bytes);
 
 /* Run the whole chain: x (activation 0) -> y (the last activation), both

@@ -24,7 +24,7 @@ SOURCES = ["conv_hwcn_vecn_tap.hip", "conv_hwcn_vecn_tap_dma.hip", "conv_hwcn_ve
            "conv_nchw.hip", "conv_acc64_hwcn_tap.hip", "conv_acc64_hwcn.hip", "conv_acc64_nchw.hip",
            "conv_hwcn_vecn_tap_fused.hip", "conv_hwcn_vecn_fused.hip", "conv_hwcn_other_fused.hip",
            "conv_nchw_fused.hip", "conv_nchw_tap.hip", "conv_nchw_tap_fused.hip", "conv_hwcn_persist.hip", "conv_hwcn_persist_fused.hip",
-           "conv_launch.hip", "pool.hip", "plan.cpp", "abi.cpp", "net.cpp", "noalloc.hip", "measure.hip"]
+           "conv_launch.hip", "pool.hip", "layout.hip", "plan.cpp", "abi.cpp", "net.cpp", "noalloc.hip", "measure.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -291,6 +291,10 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
 int launch_tail_reduce(const RArgs& r, void* stream, std::string* err);
 int launch_maxpool(const PArgs& p, void* stream, std::string* err);
 // wt[R][S][C][K] = w[K][C][R][S] (conv_launch.hip).
+// out[b][c][a] = in[a][c][b] (layout.hip): NCHW -> HWCN with (A, Cm, B) =
+// (N, C, H*W), HWCN -> NCHW with (H*W, C, N).  A and Cm at most 65535 tiles
+// of 64 and 65535, else MG3M_ERR_TOO_LARGE.
+int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void* stream, std::string* err);
 int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
                           std::string* err);
 

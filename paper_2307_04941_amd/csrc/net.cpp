@@ -9,6 +9,12 @@
 // mg3m_net_forward_graph captures those launches into a HIP graph once and
 // replays it, which removes the per-launch host cost for networks of many
 // small layers.
+//
+// Every layer runs in HWCN, the tuned layout, whatever the network's layout.
+// An NCHW network changes layout only at its edges: its input is copied to
+// HWCN in the arena, its filters to [R][S][C][K] in a buffer of the network's
+// own, and its last layer's HWCN output to the caller's NCHW y, each by one
+// kernel per forward pass.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -21,7 +27,7 @@
 #include "mg3m_internal.h"
 
 struct mg3m_net {
-  int layout = 0, N = 0, device = 0;
+  int layout = 0, N = 0, device = 0;   // layout: of x, y and the filters; the layers run in HWCN
   std::vector<mg3m_layer> layers;
   std::vector<int> C, H, W;            // per activation 0 .. n
   std::vector<long long> offset;       // byte offset in the arena; -1 for the input and the output
@@ -29,6 +35,10 @@ struct mg3m_net {
   size_t arena_bytes = 0;
   void* ws = nullptr;
   size_t ws_bytes = 0;
+  // NCHW networks: HWCN filter copies, one block per convolution (offset per layer, -1 for pooling)
+  float* wt = nullptr;
+  size_t wt_bytes = 0;
+  std::vector<long long> wt_off;
   // captured forward pass
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
@@ -89,16 +99,20 @@ struct Arena {
   }
 };
 
+bool nchw(const mg3m_net& n) { return n.layout == MG3M_LAYOUT_NCHW; }
+
 mg3m::ConvGeom conv_geom(const mg3m_net& n, int i) {
   const mg3m_layer& L = n.layers[i];
   const int in = L.input;
   return mg3m::ConvGeom{n.N, n.C[in], n.H[in], n.W[in], L.K, L.R, L.S, L.stride, L.stride,
-                        L.pad, L.pad, n.layout, false};
+                        L.pad, L.pad, MG3M_LAYOUT_HWCN, false};
 }
 
+// The HWCN tensor layer code reads or writes for activation id: the caller's
+// x and y in an HWCN network, arena blocks otherwise.
 const float* act_ptr(const mg3m_net& n, int id, const float* x, float* y) {
-  if (id == 0) return x;
-  if (id == (int)n.layers.size()) return y;
+  if (!nchw(n) && id == 0) return x;
+  if (!nchw(n) && id == (int)n.layers.size()) return y;
   return reinterpret_cast<const float*>(n.arena + n.offset[id]);
 }
 
@@ -113,6 +127,8 @@ int build(mg3m_net& n, int C0, int H0, int W0) {
   n.H[0] = H0;
   n.W[0] = W0;
   n.ws_bytes = 0;
+  n.wt_bytes = 0;
+  n.wt_off.assign(L, -1);
   for (int i = 0; i < L; ++i) {
     const mg3m_layer& ly = n.layers[i];
     if (ly.input < 0 || ly.input > i) return mg3m::set_error(MG3M_ERR_ARG, at(i) + "input must be an earlier activation");
@@ -128,6 +144,10 @@ int build(mg3m_net& n, int C0, int H0, int W0) {
       n.H[i + 1] = s.Ho;
       n.W[i + 1] = s.Wo;
       n.ws_bytes = std::max(n.ws_bytes, p.ws_bytes);
+      if (nchw(n)) {
+        n.wt_off[i] = (long long)n.wt_bytes;
+        n.wt_bytes += round_up(4 * (size_t)ly.K * n.C[in] * ly.R * ly.S);
+      }
       if (ly.add != -1) {
         if (ly.add < 0 || ly.add > i) return mg3m::set_error(MG3M_ERR_ARG, at(i) + "add must be an earlier activation or -1");
         if (n.C[ly.add] != ly.K || n.H[ly.add] != s.Ho || n.W[ly.add] != s.Wo)
@@ -154,10 +174,11 @@ int build(mg3m_net& n, int C0, int H0, int W0) {
   return MG3M_OK;
 }
 
-// Offsets of activations 1 .. L-1.  keep_all: one block each.  Otherwise the
-// block of activation j is released after layer last_use[j] has run, so it is
-// never handed to a layer that still reads j (a layer's output never shares
-// space with its own inputs).
+// Offsets of activations 1 .. L-1 (and, in an NCHW network, of the HWCN
+// copies of the input, 0, and of the output, L).  keep_all: one block each.
+// Otherwise the block of activation j is released after layer last_use[j]
+// has run, so it is never handed to a layer that still reads j (a layer's
+// output never shares space with its own inputs).
 void place(mg3m_net& n, bool keep_all) {
   const int L = (int)n.layers.size();
   std::vector<int> last_use(L + 1, -1);
@@ -167,14 +188,15 @@ void place(mg3m_net& n, bool keep_all) {
   }
   n.offset.assign(L + 1, -1);
   Arena arena;
+  auto bytes_of = [&](int id) { return round_up(4 * (size_t)n.N * n.C[id] * n.H[id] * n.W[id]); };
+  if (nchw(n)) n.offset[0] = (long long)arena.take(bytes_of(0));
+  const int first = nchw(n) ? 0 : 1;        // activations whose block the arena owns
+  const int last = nchw(n) ? L : L - 1;
   for (int i = 0; i < L; ++i) {
     const int out = i + 1;
-    if (out < L) {
-      const size_t bytes = round_up(4 * (size_t)n.N * n.C[out] * n.H[out] * n.W[out]);
-      n.offset[out] = (long long)arena.take(bytes);
-    }
+    if (out <= last) n.offset[out] = (long long)arena.take(bytes_of(out));
     if (!keep_all) {
-      for (int j = 1; j < L; ++j)
+      for (int j = first; j < L; ++j)
         if (last_use[j] == i && n.offset[j] >= 0) arena.give((size_t)n.offset[j]);
     }
   }
@@ -184,6 +206,19 @@ void place(mg3m_net& n, bool keep_all) {
 
 int run_layers(mg3m_net& n, const float* x, float* y, hipStream_t stream) {
   const int L = (int)n.layers.size();
+  std::string err;
+  if (nchw(n)) {
+    // the input and every filter to HWCN ([N][C][H][W] -> [H][W][C][N], [K][C][R][S] -> [R][S][C][K])
+    int rc = mg3m::launch_swap_outer_inner(x, const_cast<float*>(act_ptr(n, 0, x, y)), n.N, n.C[0],
+                                           n.H[0] * n.W[0], stream, &err);
+    for (int i = 0; rc == MG3M_OK && i < L; ++i) {
+      const mg3m_layer& ly = n.layers[i];
+      if (ly.op == MG3M_OP_CONV)
+        rc = mg3m::launch_filter_to_rsck(ly.w, n.wt + n.wt_off[i] / 4, ly.K, n.C[ly.input], ly.R, ly.S, stream,
+                                         &err);
+    }
+    if (rc) return mg3m::set_error(rc, err);
+  }
   for (int i = 0; i < L; ++i) {
     const mg3m_layer& ly = n.layers[i];
     const float* src = act_ptr(n, ly.input, x, y);
@@ -192,13 +227,19 @@ int run_layers(mg3m_net& n, const float* x, float* y, hipStream_t stream) {
     int rc;
     if (ly.op == MG3M_OP_CONV) {
       const float* add = ly.add >= 0 ? act_ptr(n, ly.add, x, y) : nullptr;
-      rc = mg3m::conv_run(src, ly.w, dst, conv_geom(n, i), n.ws, n.ws_bytes, false, nullptr, add, ly.relu,
+      const float* w = nchw(n) ? n.wt + n.wt_off[i] / 4 : ly.w;
+      rc = mg3m::conv_run(src, w, dst, conv_geom(n, i), n.ws, n.ws_bytes, false, nullptr, add, ly.relu,
                           stream);
     } else {
       rc = mg3m::maxpool_run(src, dst, n.N, n.C[in], n.H[in], n.W[in], ly.R, ly.S, ly.stride, ly.stride,
-                             ly.pad, ly.pad, n.layout, stream);
+                             ly.pad, ly.pad, MG3M_LAYOUT_HWCN, stream);
     }
     if (rc) return mg3m::set_error(rc, at(i) + mg3m_last_error());
+  }
+  if (nchw(n)) {
+    // the output back to NCHW: [H][W][C][N] -> [N][C][H][W]
+    int rc = mg3m::launch_swap_outer_inner(act_ptr(n, L, x, y), y, n.H[L] * n.W[L], n.C[L], n.N, stream, &err);
+    if (rc) return mg3m::set_error(rc, err);
   }
   return MG3M_OK;
 }
@@ -212,6 +253,9 @@ int check_io(const mg3m_net* net, const float* x, float* y) {
   const uintptr_t a0 = reinterpret_cast<uintptr_t>(net->arena), a1 = a0 + net->arena_bytes;
   if ((ax >= a0 && ax < a1) || (ay >= a0 && ay < a1))
     return mg3m::set_error(MG3M_ERR_ALIAS, "x or y lies inside the network's arena");
+  const uintptr_t f0 = reinterpret_cast<uintptr_t>(net->wt), f1 = f0 + net->wt_bytes;
+  if (net->wt != nullptr && ((ax >= f0 && ax < f1) || (ay >= f0 && ay < f1)))
+    return mg3m::set_error(MG3M_ERR_ALIAS, "x or y lies inside the network's filter copies");
   return MG3M_OK;
 }
 
@@ -229,8 +273,10 @@ void release(mg3m_net* n) {
   drop_graph(n);
   if (n->arena) (void)hipFree(n->arena);
   if (n->ws) (void)hipFree(n->ws);
+  if (n->wt) (void)hipFree(n->wt);
   n->arena = nullptr;
   n->ws = nullptr;
+  n->wt = nullptr;
 }
 
 }  // namespace
@@ -261,6 +307,7 @@ int mg3m_net_create(const mg3m_layer* layers, int n_layers, int N, int C, int H,
     hipError_t e = hipGetDevice(&n->device);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&n->arena), n->arena_bytes);
     if (e == hipSuccess && n->ws_bytes > 0) e = hipMalloc(&n->ws, n->ws_bytes);
+    if (e == hipSuccess && n->wt_bytes > 0) e = hipMalloc(reinterpret_cast<void**>(&n->wt), n->wt_bytes);
     if (e != hipSuccess) {
       release(n);
       delete n;
@@ -285,6 +332,7 @@ int mg3m_net_activation(const mg3m_net* net, int id, int* C, int* H, int* W, con
   *H = net->H[id];
   *W = net->W[id];
   if (ptr) *ptr = (id == 0 || id == L) ? nullptr : reinterpret_cast<const float*>(net->arena + net->offset[id]);
+  // (stored activations are HWCN in every network)
   return MG3M_OK;
 }
 
@@ -293,7 +341,7 @@ int mg3m_net_memory(const mg3m_net* net, size_t* arena_bytes, size_t* workspace_
   if (net == nullptr || arena_bytes == nullptr || workspace_bytes == nullptr)
     return mg3m::set_error(MG3M_ERR_NULL, "net and out-parameters must be non-NULL");
   *arena_bytes = net->arena_bytes;
-  *workspace_bytes = net->ws_bytes;
+  *workspace_bytes = net->ws_bytes + net->wt_bytes;
   return MG3M_OK;
 }
 

@@ -305,7 +305,9 @@ class Net:
 
     def activation(self, i):
         """A torch view of stored activation i (1 .. n_layers-1), valid after a
-        forward pass (every one of them only with keep_all)."""
+        forward pass (every one of them only with keep_all).  Stored
+        activations are HWCN, shape (H, W, C, N), in every network: an NCHW
+        network runs its layers in HWCN and changes layout only for x and y."""
         import torch
         c, h, w, p = ctypes.c_int(), ctypes.c_int(), ctypes.c_int(), ctypes.c_void_p()
         _check(load_library().mg3m_net_activation(self._h, i, ctypes.byref(c), ctypes.byref(h),
@@ -313,7 +315,7 @@ class Net:
         if not p.value:
             raise ValueError("activation 0 and the last one are the caller's tensors")
         n = self.input_shape[0] * c.value * h.value * w.value
-        return _device_view(p.value, n, torch).view(self.shape(i))
+        return _device_view(p.value, n, torch).view(h.value, w.value, c.value, self.input_shape[0])
 
     def memory(self):
         a, b = ctypes.c_size_t(), ctypes.c_size_t()

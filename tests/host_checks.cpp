@@ -3,7 +3,7 @@
 // planner, the C ABI's validation and dispatch path and the network
 // executor's validation, on a seeded grid of shapes, plan overrides and
 // malformed arguments; and the CPU oracle against its pins.  Nothing here
-// touches a GPU: the four kernel launchers are replaced by stubs that check
+// touches a GPU: the five kernel launchers are replaced by stubs that check
 // each launch's arguments against the plan and the buffers instead of
 // launching, and the device pointers passed in are never dereferenced.  HIP
 // runtime calls (workspace pool, events, allocations) fail on a host without
@@ -43,7 +43,7 @@ static int g_failures = 0;
 // ------------------------------------------------------------ launch stubs
 // What the last stubbed launches saw, for the checks after each call.
 struct Seen {
-  int convs = 0, reduces = 0, copies = 0, pools = 0;
+  int convs = 0, reduces = 0, copies = 0, pools = 0, swaps = 0;
   mg3m::Plan plan{};
   mg3m::KArgs args{};
   mg3m::RArgs rargs{};
@@ -103,6 +103,12 @@ int launch_maxpool(const PArgs& p, void*, std::string*) {
 int launch_filter_to_rsck(const float*, float* wt, int K, int C, int R, int S, void*, std::string*) {
   ++g_seen.copies;
   CHECK(wt != nullptr && (long long)K * C * R * S > 0, "filter copy");
+  return MG3M_OK;
+}
+
+int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void*, std::string*) {
+  ++g_seen.swaps;
+  CHECK(in != nullptr && out != nullptr && A >= 1 && Cm >= 1 && B >= 1, "layout change");
   return MG3M_OK;
 }
 

@@ -167,7 +167,8 @@ def _check_chain(net, layers, x_host, y_host, layout, sample=None, seed=0):
     """Every layer against the oracle applied to its own GPU inputs."""
     acts = {0: x_host, len(layers): y_host}
     for i in range(1, len(layers)):
-        acts[i] = _host(net.activation(i))
+        a = _host(net.activation(i))          # stored activations are HWCN in every network
+        acts[i] = a if layout == "HWCN" else np.ascontiguousarray(np.transpose(a, (3, 2, 0, 1)))
     rng = np.random.Generator(np.random.PCG64(seed))
     worst = 0.0
     for i, d in enumerate(layers):
