@@ -97,7 +97,11 @@ int conv2d_out_dims(int H, int W, int R, int S, int stride, int pad, int *Ho, in
  * sums them in a fixed order, so results are
  * deterministic run to run.  NCHW plans with C a multiple of the plan's kt, K a multiple of 4,
  * a filter of more than one tap and stride_w 1 take the reduction tap-major: a
- * first kernel copies the filter to [R][S][C][K] in that workspace. */
+ * first kernel copies the filter to [R][S][C][K] in that workspace.  An NCHW
+ * call may instead run as HWCN (the selector weighs both; see via= below):
+ * x and the filter are copied to HWCN and [R][S][C][K] in the workspace, the
+ * HWCN kernels write an HWCN copy of y there, and a last kernel writes y in
+ * NCHW (applying the fused output stage, for conv2d_fwd_f32_fused). */
 int conv2d_fwd_f32(const float *x, const float *w, float *y,
                    int N, int C, int H, int W, int K, int R, int S,
                    int stride, int pad, int layout, void *stream);
@@ -121,6 +125,10 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *                    256x128, 128x256, 128x128 with kt=32, 16x64 (16x16x4
  *                    MFMAs; the selector takes it only when K mod 32 is 1..16),
  *                    and 64x64 with kt=32 (four 32x32 waves)
+ *   via=hwcn|none    NCHW calls of the fp32 kernel: run as HWCN on copies of x, w and
+ *                    y in the workspace (hwcn), or in NCHW (none); by default the
+ *                    selector weighs both.  via=hwcn on HWCN or fp64 calls ->
+ *                    MG3M_ERR_PLAN
  *   waves=<WM>x<WN>  the work-group's wave grid (1..8 each), to pick among tiles
  *                    of one shape (64x64 comes as 1x1 with kt=16 and 2x2 with
  *                    kt=32), so the tile, waves and kt of a plan string read back
@@ -326,6 +334,8 @@ typedef struct mg3m_plan_info {
     int a_mode, b_mode;       /* operand loader variant of the main kernel (its template arguments) */
     int e_mode;               /* epilogue store mode */
     int persistent;           /* 1: grid work-groups loop over the dp_tiles whole tiles */
+    int via_hwcn;             /* 1: an NCHW call run as HWCN on copies in the workspace (layout, a_mode,
+                                 b_mode and e_mode are then the HWCN kernels') */
 } mg3m_plan_info;
 
 int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,

@@ -335,11 +335,19 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
     }
   }
 
-  // workspace: [R][S][C][K] filter copy (tap-major NCHW plans), then the partials
+  // workspace: [R][S][C][K] filter copy (tap-major NCHW plans) or the HWCN
+  // copies of x, w and y (NCHW calls run as HWCN), then the partials
+  const bool via = p.via_hwcn != 0;
+  auto at_byte = [&](size_t off) { return reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + off); };
+  const size_t xr = (xb + 255) / 256 * 256, wr = (wb + 255) / 256 * 256;
   float* const wt = p.wt_bytes > 0 ? ws : nullptr;
-  float* const part = ws != nullptr ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + p.wt_bytes) : nullptr;
+  float* const xh = via ? at_byte(0) : nullptr;
+  float* const wh = via ? at_byte(xr) : nullptr;
+  float* const yh = via ? at_byte(xr + wr) : nullptr;
+  float* const part = ws != nullptr ? at_byte(p.wt_bytes + p.via_bytes) : nullptr;
+  float* const yk = via ? yh : y;                  // the output the kernels write
   mg3m::KArgs a{};
-  a.x = x; a.w = wt != nullptr ? wt : w; a.y = y; a.ws = part;
+  a.x = via ? xh : x; a.w = via ? wh : (wt != nullptr ? wt : w); a.y = yk; a.ws = part;
   a.x_bytes = (unsigned)xb; a.w_bytes = (unsigned)wb; a.y_bytes = (unsigned)yb;
   a.N = s.N; a.C = s.C; a.H = s.H; a.W = s.W; a.K = s.K; a.R = s.R; a.S = s.S;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw; a.Ho = s.Ho; a.Wo = s.Wo;
@@ -347,12 +355,18 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   a.tiles_m = p.tiles_m; a.k_tiles = p.k_tiles;
   a.dp_tiles = p.dp_tiles; a.tail_tiles = p.tail_tiles; a.sk_q = p.sk_q; a.sk_r = p.sk_r; a.sk_s = p.sk_s;
   a.e_mode = p.e_mode;
-  a.mstride = s.layout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
-  a.add = add;
-  a.relu = relu;
+  const int klayout = via ? mg3m::kHWCN : s.layout;   // the layout the kernels run in
+  a.mstride = klayout == mg3m::kHWCN ? s.N : s.Ho * s.Wo;
+  // an NCHW call run as HWCN applies its output stage on the way back to NCHW
+  a.add = via ? nullptr : add;
+  a.relu = via ? 0 : relu;
 
   std::string err;
   if (wt != nullptr) rc = mg3m::launch_filter_to_rsck(w, wt, s.K, s.C, s.R, s.S, stream, &err);
+  if (via) {
+    rc = mg3m::launch_swap_outer_inner(x, xh, s.N, s.C, s.H * s.W, stream, &err);   // [N][C][H][W] -> [H][W][C][N]
+    if (rc == MG3M_OK) rc = mg3m::launch_filter_to_rsck(w, wh, s.K, s.C, s.R, s.S, stream, &err);
+  }
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
   g_ev_start = g_ev_stop = nullptr;
   if (ev0 != nullptr) {
@@ -366,18 +380,20 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   }
   if (rc == MG3M_OK && p.tail_tiles > 0) {
     mg3m::RArgs r{};
-    r.ws = part; r.y = y; r.mt = p.t.mt; r.nt = p.t.nt;
+    r.ws = part; r.y = yk; r.mt = p.t.mt; r.nt = p.t.nt;
     r.tiles_m = p.tiles_m; r.dp_tiles = p.dp_tiles; r.tail_tiles = p.tail_tiles;
     r.k_tiles = p.k_tiles; r.sk_q = p.sk_q; r.sk_r = p.sk_r; r.sk_s = p.sk_s;
-    r.layout = s.layout; r.N = s.N; r.K = s.K; r.HoWo = s.Ho * s.Wo;
+    r.layout = klayout; r.N = s.N; r.K = s.K; r.HoWo = s.Ho * s.Wo;
     r.Mg = (int)s.Mg; r.Ng = (int)s.Ng;
-    const bool contiguous4 = s.layout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
-    r.vec4 = contiguous4 && aligned(y, 16);
+    const bool contiguous4 = klayout == mg3m::kHWCN ? s.N % 4 == 0 : (s.Ho * s.Wo) % 4 == 0;
+    r.vec4 = contiguous4 && aligned(yk, 16);
     r.f64 = p.acc64;
-    r.add = add;
-    r.relu = relu;
+    r.add = a.add;
+    r.relu = a.relu;
     rc = mg3m::launch_tail_reduce(r, stream, &err);
   }
+  // [Ho][Wo][K][N] -> [N][K][Ho][Wo], with the output stage
+  if (rc == MG3M_OK && via) rc = mg3m::launch_swap_outer_inner(yh, y, s.Ho * s.Wo, s.K, s.N, stream, &err, add, relu);
   if (ws_done != nullptr) {
     // recorded even after a failed launch: a later call waits for what was queued
     hipError_t e = hipEventRecord(ws_done, static_cast<hipStream_t>(stream));
@@ -641,6 +657,7 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S, in
     info->layout = p.layout; info->a_mode = p.a_mode; info->b_mode = p.b_mode;
     info->e_mode = p.e_mode;
     info->persistent = p.persist;
+    info->via_hwcn = p.via_hwcn;
     return MG3M_OK;
   } catch (...) {
     return fail(MG3M_ERR_HIP, "unknown exception");

@@ -181,6 +181,8 @@ struct Plan {
   int variant;
   size_t ws_bytes;          // workspace: the filter copy (wt_bytes), then the partials
   size_t wt_bytes;          // [R][S][C][K] copy of an NCHW filter (kVarNchwTap), 256-byte rounded; else 0
+  int via_hwcn;             // 1: an NCHW call run as HWCN on copies of x, w and y in the workspace
+  size_t via_bytes;         // those copies (x, then w, then y, each 256-byte rounded) at the workspace's front
   int lds_bytes;
   double pad_eff;
   double est_us;
@@ -294,7 +296,10 @@ int launch_maxpool(const PArgs& p, void* stream, std::string* err);
 // out[b][c][a] = in[a][c][b] (layout.hip): NCHW -> HWCN with (A, Cm, B) =
 // (N, C, H*W), HWCN -> NCHW with (H*W, C, N).  A and Cm at most 65535 tiles
 // of 64 and 65535, else MG3M_ERR_TOO_LARGE.
-int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void* stream, std::string* err);
+// With add (same layout and size as out) and relu: out = act(in' + add), the
+// fused output stage of an NCHW call run as HWCN.
+int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void* stream, std::string* err,
+                            const float* add = nullptr, int relu = 0);
 int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
                           std::string* err);
 

@@ -89,6 +89,7 @@ double variant_factor(int variant) {
 struct Override {
   int mt = 0, nt = 0, kt = 0, split = 0, tail = 0, persist = 0, dma = -1;   // dma: -1 = the default
   int wm = 0, wn = 0;                                                     // waves (0: any)
+  int via = -1;                                                           // NCHW run as HWCN: 1, 0, -1 = either
   long long sk = 0;
 };
 
@@ -146,6 +147,15 @@ int parse_override(const char* text, Override* o, std::string* err) {
       }
       o->wm = (int)wm;
       o->wn = (int)wn;
+    } else if (key == "via") {
+      if (val == "hwcn") {
+        o->via = 1;
+      } else if (val == "none") {
+        o->via = 0;
+      } else {
+        *err = "plan override: via must be hwcn or none";
+        return MG3M_ERR_PLAN;
+      }
     } else if (key == "split") {
       long v = std::strtol(val.c_str(), &tail, 10);
       if (tail == val.c_str() || *tail != 0 || v < 1 || v > 64) {
@@ -430,14 +440,25 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   size_t least_over_cap = SIZE_MAX;     // smallest workspace among the candidates over ws_cap
   // the split factors the cost model was calibrated on
   const int splits[] = {2, 3, 4, 6, 8, 16};
-  auto consider = [&](int ti, int sched, long long sp) {
+  // via: an NCHW call run as HWCN on 16-byte aligned copies of x, w and y in
+  // the workspace, the layout changed on the way in and out (layout.hip)
+  auto consider_one = [&](int ti, int sched, long long sp, bool via) {
     Plan c{};
-    if (!shape_plan(s, acc64, ti, sched, sp, &c)) return;
+    ConvShape sv = s;
+    if (via) sv.layout = kHWCN;
+    if (!shape_plan(sv, acc64, ti, sched, sp, &c)) return;
     // the one-tap HWCN loaders load straight into LDS unless the override says
     // otherwise, except in the persistent and fp64-accumulating kernels and
     // the 16-row tile, which stage through VGPRs
     const bool dma_ok = !c.acc64 && !c.t.m16 && !c.persist;
-    choose_modes(s, x16, w16, y16, &c, dma_ok && o.dma != 0);
+    choose_modes(sv, via || x16, via || w16, via || y16, &c, dma_ok && o.dma != 0);
+    if (via) {
+      auto r256 = [](size_t b) { return (b + 255) / 256 * 256; };
+      c.via_hwcn = 1;
+      c.via_bytes = r256(4 * (size_t)s.N * s.C * s.H * s.W) + r256(4 * (size_t)s.Mg * (size_t)s.Kg) +
+                    r256(4 * (size_t)s.Mg * (size_t)s.Ng);
+      c.ws_bytes += c.via_bytes;
+    }
     if (o.dma == 1 && c.variant != kVarHwcnVecNTapDma) return;
     // runs spanning two tiles need the kernel's loop over pieces (only the
     // 32x32x2 fp32 kernel with the one-tap HWCN loader has it)
@@ -455,7 +476,9 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       least_over_cap = std::min(least_over_cap, c.ws_bytes);
       return;
     }
-    c.est_us = predict_us(s, c);
+    c.est_us = predict_us(sv, c);
+    // the layout changes: x and w in, y out, each read and written once
+    if (via) c.est_us += 2.0 * (double)c.via_bytes / kStreamBytesPerS * 1e6 + 3 * kLaunchUs;
     // ties: less workspace traffic, then the larger tile
     const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
                         (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
@@ -465,6 +488,15 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
       best = ti;
       best_plan = c;
     }
+  };
+  const bool via_ok = s.layout == kNCHW && !acc64;
+  if (o.via == 1 && !via_ok) {
+    *err = "plan override: via=hwcn applies to NCHW calls of the fp32 kernel";
+    return MG3M_ERR_PLAN;
+  }
+  auto consider = [&](int ti, int sched, long long sp) {
+    if (o.via != 1) consider_one(ti, sched, sp, false);
+    if (via_ok && o.via != 0) consider_one(ti, sched, sp, true);
   };
   for (int ti = 0; ti < (acc64 ? kNumTiles64 : kNumTiles); ++ti) {
     const TileDesc& td = tile_desc(acc64, ti);
@@ -530,10 +562,11 @@ std::string plan_to_string(const ConvShape& s, const Plan& p) {
   static const char* en[] = {"elem", "vec_m"};
   char buf[512];
   std::snprintf(buf, sizeof buf,
-                "%s%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,tail_wgs=%d,grid=%lld,"
+                "%s%s%stile=%dx%d,waves=%dx%d,kt=%d,split=%d,dp_tiles=%d,tail_tiles=%d,tail_wgs=%d,grid=%lld,"
                 "tiles=%dx%d,k_tiles=%d,a=%s,b=%s,e=%s,lds=%d,ws=%zu,pad_eff=%.4f,est_us=%.2f,"
                 "Mg=%lld,Ng=%lld,Kg=%lld",
-                p.acc64 ? "acc=f64," : "", p.persist ? "persist," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.tail_wgs, p.grid,
+                p.acc64 ? "acc=f64," : "", p.via_hwcn ? "via=hwcn," : "",
+                p.persist ? "persist," : "", p.t.mt, p.t.nt, p.t.wm, p.t.wn, p.t.kt, p.split, p.dp_tiles, p.tail_tiles, p.tail_wgs, p.grid,
                 p.tiles_m, p.tiles_n, p.k_tiles, an[p.a_mode], bn[p.b_mode], en[p.e_mode],
                 p.lds_bytes, p.ws_bytes, p.pad_eff, p.est_us, s.Mg, s.Ng, s.Kg);
   return buf;

@@ -44,7 +44,7 @@ class PlanInfo(ctypes.Structure):
         ("pad_efficiency", ctypes.c_double), ("est_us", ctypes.c_double),
         ("layout", ctypes.c_int), ("a_mode", ctypes.c_int), ("b_mode", ctypes.c_int),
         ("e_mode", ctypes.c_int),
-        ("persistent", ctypes.c_int),
+        ("persistent", ctypes.c_int), ("via_hwcn", ctypes.c_int),
     ]
 
     def as_dict(self):

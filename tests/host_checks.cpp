@@ -76,7 +76,8 @@ int launch_conv(const Plan& p, const KArgs& a, void*, std::string* err) {
     CHECK(covered == steps, "tail runs cover %lld of %lld steps", covered, steps);
     CHECK(p.sk_q >= 1 && p.sk_q <= p.k_tiles, "run length");
     const long long slots = (long long)p.tail_wgs + p.tail_tiles - 1;
-    CHECK((size_t)slots * p.t.mt * p.t.nt * (p.acc64 ? 8 : 4) + p.wt_bytes <= p.ws_bytes, "partial slots");
+    CHECK((size_t)slots * p.t.mt * p.t.nt * (p.acc64 ? 8 : 4) + p.wt_bytes + p.via_bytes <= p.ws_bytes,
+          "partial slots");
   }
   // tensor sizes the kernel addresses through its buffer resources
   CHECK((long long)a.x_bytes == 4LL * a.N * a.C * a.H * a.W, "x_bytes");
@@ -106,9 +107,11 @@ int launch_filter_to_rsck(const float*, float* wt, int K, int C, int R, int S, v
   return MG3M_OK;
 }
 
-int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void*, std::string*) {
+int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, void*, std::string*,
+                            const float*, int relu) {
   ++g_seen.swaps;
-  CHECK(in != nullptr && out != nullptr && A >= 1 && Cm >= 1 && B >= 1, "layout change");
+  CHECK(in != nullptr && out != nullptr && in != out && A >= 1 && Cm >= 1 && B >= 1, "layout change");
+  CHECK(relu == 0 || relu == 1, "layout change relu");
   return MG3M_OK;
 }
 

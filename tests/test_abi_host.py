@@ -155,20 +155,29 @@ def _check_plan(shape, layout, plan=None):
         assert p["split"] == -(-wgs // tail) >= 2
     else:
         assert wgs == 0 and p["split"] == 1 and p["k_tiles_per_wg"] == kt
+    # an NCHW call may run as HWCN on copies of x, w and y (via_hwcn): its
+    # kernels are then the HWCN ones
+    via = p["via_hwcn"] == 1
+    assert not via or layout == "NCHW"
+    klayout = "HWCN" if via else layout
+    assert p["layout"] == (0 if klayout == "HWCN" else 1)
     if p["persistent"]:
         # persistent: every tile whole, fewer work-groups than tiles, each
         # looping over them
         assert tail == 0 and 1 <= p["grid"] < p["dp_tiles"] and p["grid"] % 256 == 0 or p["grid"] == p["dp_tiles"]
-        assert p["b_mode"] in (0, 3) and layout == "HWCN" and p["mt"] != 16
+        assert p["b_mode"] in (0, 3) and klayout == "HWCN" and p["mt"] != 16
     else:
         assert p["grid"] == p["dp_tiles"] + wgs <= 2**31 - 1
     # partials (slots up to wgs + tail - 2), plus the [R][S][C][K] filter copy
-    # of a tap-major NCHW plan (b_mode 5)
-    copy = -(-4 * Mg * Kg // 256) * 256 if p["b_mode"] == 5 else 0
+    # of a tap-major NCHW plan (b_mode 5), or the HWCN copies of x, w and y
+    r256 = lambda b: -(-b // 256) * 256
+    copy = r256(4 * Mg * Kg) if p["b_mode"] == 5 else 0
+    if via:
+        copy = r256(4 * N * C * H * W) + r256(4 * Mg * Kg) + r256(4 * Mg * Ng)
     # the direct-to-LDS one-tap loaders: HWCN, 32x32x2-MFMA tiles, not persistent
-    assert p["b_mode"] != 6 or (layout == "HWCN" and p["mt"] != 16 and not p["persistent"]
+    assert p["b_mode"] != 6 or (klayout == "HWCN" and p["mt"] != 16 and not p["persistent"]
                                 and N % 4 == 0 and K % 4 == 0 and C % p["kt"] == 0)
-    assert p["b_mode"] != 5 or (layout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
+    assert p["b_mode"] != 5 or (klayout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
                                 and (st if isinstance(st, int) else st[1]) == 1)
     slots = wgs + tail - 1 if tail else 0
     assert p["workspace_bytes"] == 4 * slots * p["mt"] * p["nt"] + copy
@@ -241,11 +250,14 @@ def test_stream_k_override():
     assert (p["dp_tiles"], p["tail_tiles"], p["tail_wgs"]) == (r["dp_tiles"], r["tail_tiles"], r["tail_tiles"] + 100)
     # runs spanning two tiles only with the one-tap HWCN loader (b_mode 3) of
     # the fp32 kernel; runs that fall on tile boundaries are a split anywhere
-    for layout, shape in (("NCHW", small), ("HWCN", (3, 64, 14, 14, 256, 3, 3, 1, 1))):
+    for layout, shape, via in (("NCHW", small, ",via=none"), ("HWCN", (3, 64, 14, 14, 256, 3, 3, 1, 1), "")):
         with pytest.raises(mg3m.Mg3mError) as ei:
-            mg3m.conv2d_fwd_f32_plan_info(*shape, layout, f"tile=256x64,sk={tail + 1}")
+            mg3m.conv2d_fwd_f32_plan_info(*shape, layout, f"tile=256x64,sk={tail + 1}{via}")
         assert ei.value.status == 7 and "one-tap HWCN" in mg3m.mg3m_last_error()
-    p = _check_plan(small, "NCHW", f"tile=256x64,sk={4 * tail}")
+    # an NCHW call takes such runs when it runs as HWCN
+    p = _check_plan(small, "NCHW", f"tile=256x64,sk={tail + 1}")
+    assert p["via_hwcn"] == 1 and p["tail_wgs"] == tail + 1
+    p = _check_plan(small, "NCHW", f"tile=256x64,sk={4 * tail},via=none")
     assert (p["tail_wgs"], p["split"], p["k_tiles_per_wg"]) == (4 * tail, 4, 9)
     for bad in (f"tile=256x64,sk={tail - 1}", f"tile=256x64,sk={tail * kt + 1}", "sk=0", "sk=x",
                 "split=2,sk=20", "tail=2,sk=20", "split=2,tail=3"):
@@ -553,9 +565,11 @@ def test_one_tap_loaders_default_to_direct_lds():
     for bad in ("tile=16x64,dma=1", "tile=128x128,persist=2,dma=1"):
         with pytest.raises(mg3m.Mg3mError):
             mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", bad)
-    assert mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW")["b_mode"] == 5
+    assert mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "via=none")["b_mode"] == 5
     with pytest.raises(mg3m.Mg3mError):
-        mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "dma=1")
+        mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "dma=1,via=none")
+    v = mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "dma=1")
+    assert v["via_hwcn"] == 1 and v["b_mode"] == 6
 
 
 def test_selector_picks_persistent_and_deep_64x64_tiles():

@@ -24,8 +24,9 @@ CASES = [
     ((32, 3, 64, 64, 64, 3, 3, 1, 1), "HWCN", "tile=64x256,persist=1", False),   # persistent, vec-N
     ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,persist=1", False),  # persistent, one-tap
     ((8, 16, 14, 14, 16, 3, 3, 1, 1), "HWCN", "tile=16x64", False),              # 16x16x4 MFMAs
-    ((3, 32, 10, 9, 40, 3, 3, 1, 1), "NCHW", "tile=64x64,split=3", False),       # NCHW tap-major
-    ((2, 6, 11, 9, 37, 3, 3, 1, 1), "NCHW", "tile=128x128", False),              # NCHW element-wise
+    ((3, 32, 10, 9, 40, 3, 3, 1, 1), "NCHW", "tile=64x64,split=3,via=none", False),   # NCHW tap-major
+    ((2, 6, 11, 9, 37, 3, 3, 1, 1), "NCHW", "tile=128x128,via=none", False),          # NCHW element-wise
+    ((4, 64, 13, 11, 68, 3, 3, 1, 1), "NCHW", "tile=128x128,sk=7,via=hwcn", False),   # NCHW run as HWCN
     ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,split=3", True),     # fp64 accumulation
 ]
 

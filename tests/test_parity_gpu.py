@@ -150,7 +150,7 @@ def test_every_tile_nchw_tap_major(tile):
     x, w, st, pd = make(shape, 81, "NCHW", dist="int")
     acc, _ = oracle.conv2d(x, w, st, pd, "NCHW")
     for split in (1, 3):
-        plan = f"tile={tile},split={split}"
+        plan = f"tile={tile},split={split},via=none"
         info = mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", plan)
         assert info["b_mode"] == 5, info
         say(f"forced NCHW tap-major {plan}: workspace {info['workspace_bytes']}")
@@ -164,7 +164,7 @@ def test_every_tile_nchw(tile):
     x, w, st, pd = make(shape, 78, "NCHW")
     acc, mag = oracle.conv2d(x, w, st, pd, "NCHW")
     for split in (1, 3):
-        plan = f"tile={tile},split={split}"
+        plan = f"tile={tile},split={split},via=none"
         say(f"forced NCHW {plan}")
         y = run_gpu(x, w, st, pd, "NCHW", plan=plan)
         assert_parity(y, acc, mag, f"{shape} {plan}")
@@ -200,7 +200,7 @@ def test_nchw_row_vector_loader(case):
     say(f"NCHW loader edge {case} shape={shape}")
     x, w, st, pd = make(shape, 700 + case, "NCHW", dist="int")
     acc, _ = oracle.conv2d(x, w, st, pd, "NCHW")
-    for plan in (None, "tile=32x64,split=1", "tile=128x128,split=2"):
+    for plan in (None, "tile=32x64,split=1,via=none", "tile=128x128,split=2,via=none"):
         y = run_gpu(x, w, st, pd, "NCHW", plan=plan)
         assert np.array_equal(y, acc.astype(np.float32)), f"{shape} {plan}"
 
@@ -324,10 +324,12 @@ def test_guard_bands_and_determinism():
     assert_parity(outs[0].reshape(Ho, Wo, 96, 4), acc, mag, "guard")
 
 
-@pytest.mark.parametrize("layout,plan", [("HWCN", "split=4"), ("NCHW", "tile=128x128,split=3")])
+@pytest.mark.parametrize("layout,plan", [("HWCN", "split=4"), ("NCHW", "tile=128x128,split=3,via=none"),
+                                         ("NCHW", "tile=128x128,split=3,via=hwcn")])
 def test_workspace_guard_bands(layout, plan):
     """A caller workspace is written only inside the bytes the plan asks for
-    (NCHW: the filter copy, then the partials)."""
+    (NCHW: the filter copy, then the partials; run as HWCN: the copies of x,
+    w and y, then the partials)."""
     import torch
     shape = (4, 32, 14, 14, 96, 3, 3, 1, 1)
     x, w, st, pd = make(shape, 83, layout)

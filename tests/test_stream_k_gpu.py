@@ -56,7 +56,7 @@ def test_stream_k_runs(case):
 
 # Split runs of unequal length (k-tiles not a multiple of the runs per tile)
 # for every kind of kernel: one-tap HWCN, element-wise HWCN, NCHW.
-SPLIT_CASES = [(shape, layout, plan)
+SPLIT_CASES = [(shape, layout, plan + (",via=none" if layout == "NCHW" else ""))
                for shape, layout in ((SK_SMALL, "HWCN"), (SK_SCALAR, "HWCN"), (SK_SMALL, "NCHW"),
                                      (SK_ROUNDS, "NCHW"))
                for plan in ("tile=256x64,tail=5", "tile=128x32,tail=7", "tile=64x64,split=8")]
@@ -97,13 +97,16 @@ def test_split_runs_bit_exact(layout):
     x, w, st, pd = make(SK_SMALL, 762, layout, dist="int")
     acc, _ = oracle.conv2d(x, w, st, pd, layout)
     for plan in ("tile=256x64,tail=5", "tile=256x64,split=36", "tile=128x32,tail=7"):
+        plan += ",via=none" if layout == "NCHW" else ""
         y = run_gpu(x, w, st, pd, layout, plan=plan)
         assert np.array_equal(y.astype(np.float64), acc), f"{plan}: not bit-exact"
 
 
-@pytest.mark.parametrize("layout,plan", [("HWCN", "sk"), ("NCHW", "tile=256x64,tail=5")])
+@pytest.mark.parametrize("layout,plan", [("HWCN", "sk"), ("NCHW", "tile=256x64,tail=5,via=none"),
+                                         ("NCHW", "tile=256x64,tail=5,via=hwcn")])
 def test_tail_fused_add_relu(layout, plan):
-    """The fused output stage is applied by the tail reduction."""
+    """The fused output stage is applied by the tail reduction (an NCHW call
+    run as HWCN: by the layout change back to NCHW)."""
     import torch
     x, w, st, pd = make(SK_SMALL, 770, layout)
     acc, mag = oracle.conv2d(x, w, st, pd, layout)
