@@ -191,36 +191,13 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
   return MG3M_OK;
 }
 
-// wt[((r*S + s)*C + c)*K + k] = w[((k*C + c)*R + r)*S + s]: one thread per
-// element of wt, so the writes are coalesced along K; the reads gather from a
-// filter that is small next to the convolution's traffic.
-__global__ __launch_bounds__(256) void filter_kcrs_to_rsck(const float* w, float* wt, int K, int C,
-                                                           int R, int S) {
-  const long long total = (long long)K * C * R * S;
-  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  const int k = (int)(i % K);
-  const long long rsc = i / K;
-  const int c = (int)(rsc % C);
-  const int rs = (int)(rsc / C);
-  wt[i] = w[((long long)k * C + c) * (R * S) + rs];
-}
-
+// wt[((r*S + s)*C + c)*K + k] = w[((k*C + c)*R + r)*S + s] is the layout
+// change out[b][c][a] = in[a][c][b] with (A, Cm, B) = (K, C, R*S): its tiles
+// read each filter row's C*R*S floats in order and write each (tap, c)'s K
+// contiguous floats.
 int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
                           std::string* err) {
-  const long long blocks = ((long long)K * C * R * S + 255) / 256;
-  if (blocks < 1 || blocks > 0x7fffffffLL) {
-    *err = "internal: filter copy out of range";
-    return MG3M_ERR_PLAN;
-  }
-  hipLaunchKernelGGL(filter_kcrs_to_rsck, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
-                     w, wt, K, C, R, S);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) {
-    *err = std::string("filter copy launch: ") + hipGetErrorString(e);
-    return MG3M_ERR_HIP;
-  }
-  return MG3M_OK;
+  return launch_swap_outer_inner(w, wt, K, C, R * S, stream, err);
 }
 
 int launch_tail_reduce(const RArgs& r, void* stream, std::string* err) {

@@ -6,6 +6,7 @@
 // the fused output stage applied on the way back).
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <string>
 
 #include "mg3m.h"
@@ -13,28 +14,91 @@
 
 namespace {
 
-// One work-group moves a 64 x 64 block of (a, b) for one c through LDS, so
-// the reads run along b and the writes along a, both 256 contiguous bytes
-// per row.  The extra column keeps the transposed reads off one bank.
+// The input is read as in[a][j] with j = c * B + b (J = Cm * B), and one
+// work-group moves a 64 x 64 block of (a, j) through LDS: the reads run along
+// j, 256 contiguous bytes per a; the writes run along a, 256 contiguous bytes
+// per j at out[b][c][a0 .. a0 + 64).  Flattening (c, b) keeps both sides whole
+// when B is small (a filter's R*S taps, a batch of one).  VL (J a multiple of
+// 4, in 16-byte aligned): 16-byte loads; VS (A a multiple of 4, out and add
+// 16-byte aligned): 16-byte stores.  The extra column keeps the transposed
+// reads off one bank.  Tiles run j-fastest over a 1-D grid.
+template <bool VL, bool VS>
 __global__ __launch_bounds__(256) void swap_outer_inner(const float* __restrict__ in, float* out, int A, int Cm,
-                                                        int B, const float* add, int relu) {
+                                                        int B, const float* add, int relu, unsigned tiles_j) {
   __shared__ float t[64][65];
-  const int b0 = (int)blockIdx.x * 64, a0 = (int)blockIdx.y * 64, c = (int)blockIdx.z;
-  const int tx = (int)(threadIdx.x & 63), ty = (int)(threadIdx.x >> 6);
-  for (int i = ty; i < 64; i += 4) {
-    const int a = a0 + i, b = b0 + tx;
-    if (a < A && b < B) t[i][tx] = in[((size_t)a * Cm + c) * B + b];
-  }
-  __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int b = b0 + i, a = a0 + tx;
-    if (a < A && b < B) {
-      const size_t o = ((size_t)b * Cm + c) * A + a;
-      float v = t[tx][i];
-      if (add != nullptr) v += add[o];          // add may be out itself: read before the write
-      out[o] = (relu != 0 && v < 0.f) ? 0.f : v;  // ReLU keeps NaN
+  const unsigned J = (unsigned)Cm * (unsigned)B;
+  const unsigned tj = blockIdx.x % tiles_j, ta = blockIdx.x / tiles_j;
+  const int a0 = (int)ta * 64;
+  const unsigned j0 = tj * 64;
+  const int tid = (int)threadIdx.x;
+  if constexpr (VL) {
+    const int q = tid & 15, r = tid >> 4;           // float4 q of a row, rows r, r + 16, ...
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int a = a0 + r + 16 * i;
+      const unsigned j = j0 + 4 * q;
+      if (a < A && j < J) {                         // J % 4 == 0: the whole float4 is inside
+        const float4 v = *reinterpret_cast<const float4*>(in + (size_t)a * J + j);
+        t[r + 16 * i][4 * q] = v.x;
+        t[r + 16 * i][4 * q + 1] = v.y;
+        t[r + 16 * i][4 * q + 2] = v.z;
+        t[r + 16 * i][4 * q + 3] = v.w;
+      }
+    }
+  } else {
+    const int tx = tid & 63, ty = tid >> 6;
+    for (int i = ty; i < 64; i += 4) {
+      const int a = a0 + i;
+      const unsigned j = j0 + tx;
+      if (a < A && j < J) t[i][tx] = in[(size_t)a * J + j];
     }
   }
+  __syncthreads();
+  if constexpr (VS) {
+    const int q = tid & 15, r = tid >> 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const unsigned j = j0 + r + 16 * i;
+      const int a = a0 + 4 * q;
+      if (a < A && j < J) {                         // A % 4 == 0: the whole float4 is inside
+        const unsigned c = j / (unsigned)B, b = j - c * (unsigned)B;
+        const size_t o = ((size_t)b * Cm + c) * A + a;
+        const int row = r + 16 * i;
+        float4 v = make_float4(t[4 * q][row], t[4 * q + 1][row], t[4 * q + 2][row], t[4 * q + 3][row]);
+        if (add != nullptr) {                       // add may be out itself: read before the write
+          const float4 d = *reinterpret_cast<const float4*>(add + o);
+          v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+        }
+        if (relu != 0) {                            // ReLU keeps NaN
+          v.x = v.x < 0.f ? 0.f : v.x; v.y = v.y < 0.f ? 0.f : v.y;
+          v.z = v.z < 0.f ? 0.f : v.z; v.w = v.w < 0.f ? 0.f : v.w;
+        }
+        *reinterpret_cast<float4*>(out + o) = v;
+      }
+    }
+  } else {
+    const int tx = tid & 63, ty = tid >> 6;
+    for (int i = ty; i < 64; i += 4) {
+      const unsigned j = j0 + i;
+      const int a = a0 + tx;
+      if (a < A && j < J) {
+        const unsigned c = j / (unsigned)B, b = j - c * (unsigned)B;
+        const size_t o = ((size_t)b * Cm + c) * A + a;
+        float v = t[tx][i];
+        if (add != nullptr) v += add[o];            // add may be out itself: read before the write
+        out[o] = (relu != 0 && v < 0.f) ? 0.f : v;  // ReLU keeps NaN
+      }
+    }
+  }
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <bool VL, bool VS>
+void launch(unsigned blocks, unsigned tiles_j, const float* in, float* out, int A, int Cm, int B, const float* add,
+            int relu, hipStream_t stream) {
+  hipLaunchKernelGGL((swap_outer_inner<VL, VS>), dim3(blocks), dim3(256), 0, stream, in, out, A, Cm, B, add, relu,
+                     tiles_j);
 }
 
 }  // namespace
@@ -47,13 +111,22 @@ int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, v
     *err = "internal: empty layout change";
     return MG3M_ERR_SHAPE;
   }
-  const long long ta = (A + 63) / 64, tb = (B + 63) / 64;
-  if (ta > 65535 || Cm > 65535 || tb > 0x7fffffffLL) {
+  const long long J = (long long)Cm * B;
+  const long long tj = (J + 63) / 64, ta = (A + 63) / 64;
+  // j and the block index are 32-bit in the kernel; a block count times 256
+  // threads stays within the 32-bit launch size
+  if (J > 0x7fffffffLL || tj * ta > (1LL << 24) - 1) {
     *err = "layout change: a dimension exceeds the launch grid";
     return MG3M_ERR_TOO_LARGE;
   }
-  hipLaunchKernelGGL(swap_outer_inner, dim3((unsigned)tb, (unsigned)ta, (unsigned)Cm), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), in, out, A, Cm, B, add, relu);
+  const bool vl = J % 4 == 0 && aligned16(in);
+  const bool vs = A % 4 == 0 && aligned16(out) && (add == nullptr || aligned16(add));
+  const unsigned blocks = (unsigned)(tj * ta), tiles_j = (unsigned)tj;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (vl && vs) launch<true, true>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
+  else if (vl) launch<true, false>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
+  else if (vs) launch<false, true>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
+  else launch<false, false>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("layout change launch: ") + hipGetErrorString(e);

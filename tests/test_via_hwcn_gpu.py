@@ -93,3 +93,20 @@ def test_selector_runs_small_spatial_nchw_layers_as_hwcn():
     x, w, st, pd, exact = _exact(shape, 895)
     y = run_gpu(x, w, st, pd, "NCHW")
     assert np.array_equal(y, exact)
+
+
+@pytest.mark.parametrize("shape", [
+    (2, 70, 9, 9, 130, 1, 1, 1, 0),          # filter copy: 4-byte loads and stores; 1x1 taps (B = 1)
+    (8, 64, 8, 8, 64, 3, 3, 1, 1),           # every copy with 16-byte loads and stores
+    (4, 67, 6, 6, 128, 3, 3, 1, 1),          # filter copy: 4-byte loads, 16-byte stores
+    (5, 36, 20, 20, 72, 1, 1, 2, 0),         # x copy: 16-byte loads, 4-byte stores (N = 5)
+    (3, 130, 5, 7, 66, 3, 3, 1, 1),          # tiles across c with ragged a and j edges
+])
+def test_layout_change_paths(shape):
+    """The layout-change kernel reads in[a][c*B + b] in 64 x 64 tiles, so a
+    tile spans several c when B is small; each mix of 16-byte and 4-byte loads
+    and stores, ragged edges in a and j, and B = 1 (1x1 filters), exactly."""
+    x, w, st, pd, exact = _exact(shape, 900 + shape[1])
+    say(f"layout change {shape}")
+    y = run_gpu(x, w, st, pd, "NCHW", plan="via=hwcn")
+    assert np.array_equal(y, exact), shape
