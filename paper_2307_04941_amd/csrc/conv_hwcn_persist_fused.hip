@@ -9,6 +9,7 @@ KernelFn conv_kernel_pt_fused(int variant, int tile) {
   switch (variant) {
     case kVarHwcnVecN: return kernel_pt_for_tile<kHWCN, kAVecM, kBVecN, true>(tile);
     case kVarHwcnVecNTap: return kernel_pt_for_tile<kHWCN, kAVecM, kBVecNTap, true>(tile);
+    case kVarHwcnVecNTapDma: return kernel_pt_for_tile<kHWCN, kAVecM, kBVecNTapDma, true>(tile);
     default: return nullptr;
   }
 }

@@ -1447,6 +1447,31 @@ void conv_igemm_f32_pt(KArgs a) {
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
   typename ASel<LAYOUT, AM, C, MT, KT, BM>::type al;
   typename BSel<LAYOUT, BM, C, NT, KT>::type bl;
+  // A stage's loads into buffer b go straight into LDS with the direct-to-LDS
+  // loaders, or into registers that commit(b) writes to LDS after the
+  // current stage's MFMAs.  A stage ends when its loads have landed (with the
+  // direct loads: this wave's memory count at zero, then the barrier) and
+  // every wave is done with the buffer it consumed.
+  constexpr bool kDma = BM == kBVecNTapDma;
+  auto issue = [&](int b) {
+    if constexpr (kDma) {
+      al.load(a, wr, As0 + b * C::A_STAGE);
+      bl.load(a, xr, Bs0 + b * C::B_STAGE);
+    } else {
+      al.load(a, wr);
+      bl.load(a, xr);
+    }
+  };
+  auto commit = [&](int b) {
+    if constexpr (!kDma) {
+      al.store(As0 + b * C::A_STAGE);
+      bl.store(Bs0 + b * C::B_STAGE);
+    }
+  };
+  auto stage_end = [&]() {
+    if constexpr (kDma) wait_vmem();
+    __syncthreads();
+  };
 
   int m0 = (tile % a.tiles_m) * MT, n0 = (tile / a.tiles_m) * NT;
   al.init(a, t, m0, 0);
@@ -1458,11 +1483,9 @@ void conv_igemm_f32_pt(KArgs a) {
   const int last_kk = (a.Kg - (a.k_tiles - 1) * KT + 1) / 2;
   const int nk = a.k_tiles;
 
-  al.load(a, wr);
-  bl.load(a, xr);
-  al.store(As0);
-  bl.store(Bs0);
-  __syncthreads();
+  issue(0);
+  commit(0);
+  stage_end();
   int cur = 0;
   int pm0 = 0, pn0 = 0;          // origin of the tile whose stores are pending
   bool pending = false;
@@ -1483,31 +1506,27 @@ void conv_igemm_f32_pt(KArgs a) {
       poison_stage<C>(As0 + (cur ^ 1) * C::A_STAGE, Bs0 + (cur ^ 1) * C::B_STAGE);
       al.advance(a);
       bl.advance(a);
-      al.load(a, wr);
-      bl.load(a, xr);
+      issue(cur ^ 1);
       if (pending) store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, pm0, pn0, wm, wn, hh, q);
       // the stores read acc before it is cleared (else both stay live)
       __builtin_amdgcn_sched_barrier(0);
       clear();
       mma_stage<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q);
       __builtin_amdgcn_sched_barrier(0);
-      al.store(As0 + (cur ^ 1) * C::A_STAGE);
-      bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
-      __syncthreads();
+      commit(cur ^ 1);
+      stage_end();
       cur ^= 1;
       // stages 1 .. nk-2
       for (int it = 1; it + 1 < nk; ++it) {
         poison_stage<C>(As0 + (cur ^ 1) * C::A_STAGE, Bs0 + (cur ^ 1) * C::B_STAGE);
         al.advance(a);
         bl.advance(a);
-        al.load(a, wr);
-        bl.load(a, xr);
+        issue(cur ^ 1);
         __builtin_amdgcn_sched_barrier(0);
         mma_stage<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q);
         __builtin_amdgcn_sched_barrier(0);
-        al.store(As0 + (cur ^ 1) * C::A_STAGE);
-        bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
-        __syncthreads();
+        commit(cur ^ 1);
+        stage_end();
         cur ^= 1;
       }
     }
@@ -1518,8 +1537,7 @@ void conv_igemm_f32_pt(KArgs a) {
     if (fetch) {
       al.init(a, t, (next % a.tiles_m) * MT, 0);
       bl.init(a, t, (next / a.tiles_m) * NT, 0);
-      al.load(a, wr);
-      bl.load(a, xr);
+      issue(cur ^ 1);
     }
     if (nk == 1) {
       if (pending) store_tile_f32_buf<LAYOUT, C, FUSE>(a, acc, pm0, pn0, wm, wn, hh, q);
@@ -1529,11 +1547,8 @@ void conv_igemm_f32_pt(KArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     mma_stage_upto<C, KT>(acc, As0 + cur * C::A_STAGE, Bs0 + cur * C::B_STAGE, wm, wn, hh, q, last_kk);
     __builtin_amdgcn_sched_barrier(0);
-    if (fetch) {
-      al.store(As0 + (cur ^ 1) * C::A_STAGE);
-      bl.store(Bs0 + (cur ^ 1) * C::B_STAGE);
-    }
-    __syncthreads();
+    if (fetch) commit(cur ^ 1);
+    stage_end();
     cur ^= 1;
     pm0 = m0;
     pn0 = n0;

@@ -57,7 +57,7 @@ int lds_bytes(const TileDesc& t, bool acc64) { return (acc64 || t.m16) ? lds_byt
 // patch loader, else the tile's (tuned loader).
 int kernel_regs(const TileDesc& t, int persist_variant) {
   if (persist_variant < 0) return t.regs;
-  return t.regs_pt[persist_variant == kVarHwcnVecNTap ? 1 : 0];
+  return t.regs_pt[persist_variant == kVarHwcnVecNTapDma ? 2 : persist_variant == kVarHwcnVecNTap ? 1 : 0];
 }
 
 // Work-groups of this tile resident on one CU, limited by LDS and registers
@@ -448,9 +448,9 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     if (via) sv.layout = kHWCN;
     if (!shape_plan(sv, acc64, ti, sched, sp, &c)) return;
     // the one-tap HWCN loaders load straight into LDS unless the override says
-    // otherwise, except in the persistent and fp64-accumulating kernels and
-    // the 16-row tile, which stage through VGPRs
-    const bool dma_ok = !c.acc64 && !c.t.m16 && !c.persist;
+    // otherwise, except in the fp64-accumulating kernels and the 16-row tile,
+    // which stage through VGPRs
+    const bool dma_ok = !c.acc64 && !c.t.m16;
     choose_modes(sv, via || x16, via || w16, via || y16, &c, dma_ok && o.dma != 0);
     if (via) {
       auto r256 = [](size_t b) { return (b + 255) / 256 * 256; };
@@ -538,7 +538,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
   if (best < 0) {
     *err = "plan override: no applicable plan for tile " + std::to_string(o.mt) + "x" + std::to_string(o.nt) +
            (o.dma == 1 ? std::string(" dma=1 (the direct-to-LDS loaders serve the fp32 kernel's one-tap HWCN path"
-                                     " with 32x32x2-MFMA tiles, not persistent plans)")
+                                     " with 32x32x2-MFMA tiles)")
                        : std::string()) +
            (o.persist ? " persist=" + std::to_string(o.persist) +
                             " (persistent tiles need the fp32 kernel's batch-vector HWCN loaders: HWCN, N and K"

@@ -165,7 +165,7 @@ def _check_plan(shape, layout, plan=None):
         # persistent: every tile whole, fewer work-groups than tiles, each
         # looping over them
         assert tail == 0 and 1 <= p["grid"] < p["dp_tiles"] and p["grid"] % 256 == 0 or p["grid"] == p["dp_tiles"]
-        assert p["b_mode"] in (0, 3) and klayout == "HWCN" and p["mt"] != 16
+        assert p["b_mode"] in (0, 3, 6) and klayout == "HWCN" and p["mt"] != 16
     else:
         assert p["grid"] == p["dp_tiles"] + wgs <= 2**31 - 1
     # partials (slots up to wgs + tail - 2), plus the [R][S][C][K] filter copy
@@ -174,8 +174,8 @@ def _check_plan(shape, layout, plan=None):
     copy = r256(4 * Mg * Kg) if p["b_mode"] == 5 else 0
     if via:
         copy = r256(4 * N * C * H * W) + r256(4 * Mg * Kg) + r256(4 * Mg * Ng)
-    # the direct-to-LDS one-tap loaders: HWCN, 32x32x2-MFMA tiles, not persistent
-    assert p["b_mode"] != 6 or (klayout == "HWCN" and p["mt"] != 16 and not p["persistent"]
+    # the direct-to-LDS one-tap loaders: HWCN, 32x32x2-MFMA tiles
+    assert p["b_mode"] != 6 or (klayout == "HWCN" and p["mt"] != 16
                                 and N % 4 == 0 and K % 4 == 0 and C % p["kt"] == 0)
     assert p["b_mode"] != 5 or (klayout == "NCHW" and C % p["kt"] == 0 and K % 4 == 0 and R * S > 1
                                 and (st if isinstance(st, int) else st[1]) == 1)
@@ -553,18 +553,25 @@ def test_noalloc_validation_before_any_device_call():
 
 def test_one_tap_loaders_default_to_direct_lds():
     """Where the one-tap HWCN loaders apply, the selector's plans load straight
-    into LDS (b_mode 6) unless they are persistent or on the 16-row tile;
-    dma=0 keeps the same plan with the loaders staging through VGPRs (b_mode 3),
-    and dma=1 is refused where the direct-to-LDS form does not apply."""
+    into LDS (b_mode 6), persistent ones included, unless they are on the
+    16-row tile; dma=0 keeps the same plan with the loaders staging through
+    VGPRs (b_mode 3), and dma=1 is refused where the direct-to-LDS form does
+    not apply."""
     shape = (64, 256, 56, 56, 256, 3, 3, 1, 1)
     p = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN")
     q = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "dma=0")
     assert p["b_mode"] == 6 and q["b_mode"] == 3
     same = ("mt", "nt", "kt", "split", "dp_tiles", "tail_tiles", "tail_wgs", "grid", "workspace_bytes")
     assert all(p[k] == q[k] for k in same), (p, q)
-    for bad in ("tile=16x64,dma=1", "tile=128x128,persist=2,dma=1"):
+    for plan, b_mode in (("tile=128x128,persist=2", 6), ("tile=128x128,persist=2,dma=0", 3)):
+        r = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
+        assert r["persistent"] == 1 and r["b_mode"] == b_mode and r["grid"] == 512, (plan, r)
+    for bad in ("tile=16x64,dma=1", "tile=16x64,persist=2"):
         with pytest.raises(mg3m.Mg3mError):
             mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", bad)
+    # the three-channel stem has no one-tap loader
+    with pytest.raises(mg3m.Mg3mError):
+        mg3m.conv2d_fwd_f32_plan_info(64, 3, 224, 224, 64, 3, 3, 1, 1, "HWCN", "tile=64x256,persist=3,dma=1")
     assert mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "via=none")["b_mode"] == 5
     with pytest.raises(mg3m.Mg3mError):
         mg3m.conv2d_fwd_f32_plan_info(*shape, "NCHW", "dma=1,via=none")

@@ -28,8 +28,9 @@ int main() {
   std::printf("{\"f32\": [");
   for (int i = 0; i < kNumTiles; ++i) {
     const TileDesc& t = kTiles[i];
-    std::printf("%s[%d,%d,%d,%d,%d,%d,%d,%d,%d,%d,%d]", i ? "," : "", t.mt, t.nt, t.kt, t.wm, t.wn, t.regs,
-                t.m16, t.m16 ? lds_bytes_for64(t) : lds_bytes_for(t), t.forced_only, t.regs_pt[0], t.regs_pt[1]);
+    std::printf("%s[%d,%d,%d,%d,%d,%d,%d,%d,%d,%d,%d,%d]", i ? "," : "", t.mt, t.nt, t.kt, t.wm, t.wn, t.regs,
+                t.m16, t.m16 ? lds_bytes_for64(t) : lds_bytes_for(t), t.forced_only, t.regs_pt[0], t.regs_pt[1],
+                t.regs_pt[2]);
   }
   std::printf("], \"f64\": [");
   for (int i = 0; i < kNumTiles64; ++i) {
@@ -95,11 +96,12 @@ def test_lds_model_matches_build(kind, resources):
 
 def test_persistent_register_table_matches_build(resources):
     """regs_pt of every tile = .vgpr_count of its persistent kernel with the
-    batch-vector (kBVecN) and one-tap (kBVecNTap) patch loaders."""
+    batch-vector (kBVecN) and one-tap (kBVecNTap, and its direct-to-LDS form
+    kBVecNTapDma) patch loaders."""
     drift = []
     for i, t in enumerate(tile_tables()["f32"]):
         mt, nt, kt, wm, wn, m16 = t[0], t[1], t[2], t[3], t[4], t[6]
-        for slot, b_mode in ((0, 0), (1, 3)):
+        for slot, b_mode in ((0, 0), (1, 3), (2, 6)):
             name = f"void mg3m::conv_igemm_f32_pt<0, 0, {b_mode}, {mt}, {nt}, {kt}, {wm}, {wn}, false>(mg3m::KArgs)"
             got = resources.get(name, {}).get("vgpr_count", 0)
             if m16:

@@ -22,7 +22,9 @@ CASES = [
     ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,sk=7", False),       # stream-K pieces
     ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=64x64,kt=32,split=3", False),
     ((32, 3, 64, 64, 64, 3, 3, 1, 1), "HWCN", "tile=64x256,persist=1", False),   # persistent, vec-N
-    ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,persist=1", False),  # persistent, one-tap
+    ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,persist=1", False),  # persistent, one-tap into LDS
+    ((4, 64, 13, 11, 68, 3, 3, 1, 1), "HWCN", "tile=128x128,persist=1,dma=0", False),  # persistent, staged
+    ((8, 64, 9, 7, 68, 1, 1, 1, 0), "HWCN", "tile=64x64,kt=32,persist=1", False),  # persistent, 2 stages/tile
     ((8, 16, 14, 14, 16, 3, 3, 1, 1), "HWCN", "tile=16x64", False),              # 16x16x4 MFMAs
     ((3, 32, 10, 9, 40, 3, 3, 1, 1), "NCHW", "tile=64x64,split=3,via=none", False),   # NCHW tap-major
     ((2, 6, 11, 9, 37, 3, 3, 1, 1), "NCHW", "tile=128x128,via=none", False),          # NCHW element-wise

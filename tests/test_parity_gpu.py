@@ -129,16 +129,19 @@ PERSIST_SHAPES = [((4, 3, 13, 11, 68, 3, 3, 1, 1), 0), ((4, 64, 13, 11, 68, 3, 3
 
 @pytest.mark.parametrize("tile", [t for t in TILES if t != "16x64"])
 def test_every_tile_persistent(tile):
+    """... and the one-tap shapes again with the loaders that load straight
+    into LDS (dma=1, b_mode 6)."""
     for si, (shape, b_mode) in enumerate(PERSIST_SHAPES):
         x, w, st, pd, exact = _int_case(shape, 97 + si)
-        for wgs in (1, 2, 3):
-            plan = f"tile={tile},persist={wgs}"
-            info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
-            assert info["persistent"] == 1 and info["b_mode"] == b_mode, info
-            assert info["grid"] == min(info["dp_tiles"], 256 * wgs) and info["tail_tiles"] == 0, info
-            say(f"persistent {plan} shape={shape}: grid {info['grid']} tiles {info['dp_tiles']}")
-            y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
-            assert np.array_equal(y, exact), f"{shape} {plan}: not bit-exact"
+        for dma in ((0, 1) if b_mode == 3 else (0,)):
+            for wgs in (1, 2, 3):
+                plan = f"tile={tile},persist={wgs}" + (",dma=1" if dma else ",dma=0")
+                info = mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", plan)
+                assert info["persistent"] == 1 and info["b_mode"] == (6 if dma else b_mode), info
+                assert info["grid"] == min(info["dp_tiles"], 256 * wgs) and info["tail_tiles"] == 0, info
+                say(f"persistent {plan} shape={shape}: grid {info['grid']} tiles {info['dp_tiles']}")
+                y = run_gpu(x, w, st, pd, "HWCN", plan=plan)
+                assert np.array_equal(y, exact), f"{shape} {plan}: not bit-exact"
 
 
 @pytest.mark.parametrize("tile", TILES)
