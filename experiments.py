@@ -5,6 +5,7 @@
     python experiments.py ablation [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
     python experiments.py acc64 [--workloads W,...] [--fixed PLAN;PLAN...] [--reps R] [--out FILE]
     python experiments.py net [--nets vgg16,alexnet,resnet50] [--batch B] [--layout L] [--reps R] [--out FILE]
+    python experiments.py datavalues [--workloads W] [--layers L,...] [--reps R] [--rounds N] [--out FILE]
 
 adaptability -- Sec. 5.1: the channel-scale scenes (5.1.1), the batch sweep
     (5.1.2), the filter-size sweep (5.1.3) and the padding/stride sweep
@@ -28,6 +29,12 @@ net -- whole convolution stacks of the real networks (Sec. 5.2) through the
     max pooling between blocks.  Per network: forward time run eagerly and
     replayed from a HIP graph, convolution TFLOPS over the whole forward, and
     the activation arena against keeping every activation.
+datavalues -- the same layers, plans and instruction streams on different
+    data values: the benchmark's (uniform x, He-normal w), small integers in
+    {-2..2} and zeros, timed in interleaved rounds (3 warm-up calls and R
+    timed calls per data set and round, in that order).  The MFMA work and the
+    cycles it takes do not depend on the values; the power it draws does, and
+    with it the clock the chip holds under load.
 Inputs are the seeded synthetic tensors of ``workloads`` (HWCN, resident on
 the GPU before timing).  Each scene is warmed up for ~100 ms, then timed over
 R calls with HIP events on the calling stream.  One JSON line per scene and
@@ -186,13 +193,55 @@ def run_nets(names, batch, layout, reps, emit):
     return recs
 
 
+def run_datavalues(workload, layer_names, reps, rounds, emit):
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2307_04941_amd import mg3m
+
+    mg3m.load_library()
+    Ls = workloads.workload(workload)
+    ws = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    for i, L in enumerate(Ls):
+        if layer_names and L.name not in layer_names:
+            continue
+        Ho, Wo = mg3m.conv2d_out_dims(L.H, L.W, L.R, L.S, L.stride, L.pad)
+        sx, sw = workloads.seeds(workload, i)
+        xu, wu = workloads.make_tensors(L, sx, sw, "HWCN")
+        xi, wi = workloads.make_tensors(L, sx, sw, "HWCN", "int")
+        sets = {"uniform": (xu, wu), "int": (xi, wi), "zeros": (np.zeros_like(xu), np.zeros_like(wu))}
+        dev = {k: (torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()) for k, (a, b) in sets.items()}
+        y = torch.empty((Ho, Wo, L.K, L.N), dtype=torch.float32, device="cuda")
+        args = (L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad, "HWCN")
+        flops = 2.0 * L.N * L.K * L.C * L.R * L.S * Ho * Wo
+        us = {k: [] for k in dev}
+        for _ in range(rounds):
+            for k, (xd, wd) in dev.items():
+                for _ in range(3):
+                    mg3m.conv2d_fwd_f32_ex(xd, wd, y, *args, ws, ws.numel() * 4, None)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    mg3m.conv2d_fwd_f32_ex(xd, wd, y, *args, ws, ws.numel() * 4, None)
+                e1.record()
+                torch.cuda.synchronize()
+                us[k].append(e0.elapsed_time(e1) * 1e3 / reps)
+        emit({"workload": workload, "layer": L.name, "plan": mg3m.conv2d_fwd_f32_plan_string(*args),
+              "us_min": {k: round(min(v), 2) for k, v in us.items()},
+              "tflops": {k: round(flops / min(v) / 1e6, 2) for k, v in us.items()}})
+        del dev, y
+
+
 def _mean(v):
     return round(sum(v) / len(v), 2) if v else None
 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64", "net"])
+    ap.add_argument("mode", choices=["adaptability", "ablation", "acc64", "net", "datavalues"])
+    ap.add_argument("--layers", default=None, help="datavalues: layer names, comma-separated (default: all)")
+    ap.add_argument("--rounds", type=int, default=3, help="datavalues: interleaved rounds")
     ap.add_argument("--nets", default="vgg16,alexnet,resnet50")
     ap.add_argument("--batch", default="vgg16=64,alexnet=128,resnet50=64",
                     help="net: batch per network, name=N,...")
@@ -214,7 +263,10 @@ def main():
             out.write(line + "\n")
             out.flush()
 
-    if a.mode == "net":
+    if a.mode == "datavalues":
+        run_datavalues(a.workloads or "vgg16_n64", a.layers.split(",") if a.layers else None, a.reps, a.rounds,
+                       emit)
+    elif a.mode == "net":
         batch = {k: int(v) for k, v in (kv.split("=") for kv in a.batch.split(","))}
         run_nets(a.nets.split(","), batch, a.layout, a.reps, emit)
     elif a.mode == "adaptability":

@@ -1416,10 +1416,11 @@ __device__ __forceinline__ void mma_stage_upto(floatx16 (&acc)[C::TM][C::TN], co
 // the previous stage's MFMAs run; the last stage of a tile loads the first
 // stage of the next one.  A tile's output stores are issued one stage later,
 // right after the loads of the next tile's second stage (or of the tile after
-// it when a tile has one stage): the memory counter a wave waits on before it
-// stages its loads counts stores too, in issue order, so stores issued after
-// those loads do not hold up that wait, and a whole stage of MFMAs passes
-// before a later wait needs them finished.  The last stage of each tile
+// it when a tile has one stage), and before that stage's MFMAs.  On gfx9 one
+// memory counter counts loads and stores, so the wait that ends the stage
+// (for its loads) covers the stores as well, but only after a stage of MFMAs
+// has run beside them.  The loaders stage through registers or, for the
+// one-tap HWCN path, load straight into LDS.  The last stage of each tile
 // computes only the k-pairs that hold rows below Kg.
 template <int LAYOUT, int AM, int BM, int MT, int NT, int KT, int WM, int WN, bool FUSE>
 __global__ __launch_bounds__(WM * WN * 64)

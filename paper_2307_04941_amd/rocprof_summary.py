@@ -30,6 +30,15 @@ by kernel family.
 writes <out>/<kernel tag>_<workload>_mfma.txt: the dominant kernel's MFMA
 utilisation per launch from a ``rocprofv3 --pmc GRBM_GUI_ACTIVE
 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES`` run, and its HBM GB/s.
+
+    python -m paper_2307_04941_amd.rocprof_summary --clock DIR --kernel SUBSTR \
+        --groups uniform:13,int:13,zeros:13 --label NAME --out DIR --command-clock "..."
+
+writes <out>/NAME_clock.txt: from a ``rocprofv3 --pmc GRBM_GUI_ACTIVE`` run,
+the launches of the kernel whose name contains SUBSTR, in dispatch order,
+cut into consecutive named groups of the given sizes (e.g. the data sets of
+``experiments.py datavalues``); per group, the mean launch time, clock cycles
+per XCD and effective clock.
 """
 from __future__ import annotations
 
@@ -185,6 +194,42 @@ def mfma_summary(a):
     return 0
 
 
+def clock_summary(a):
+    """Effective clock per group of launches (see the module docstring)."""
+    agent = next(r for r in _csv(a.clock, "agent_info.csv") if int(r.get("Simd_Count") or 0) > 0)
+    xcc = int(agent["Num_Xcc"])
+    clk_max = float(agent["Max_Engine_Clk_Fcompute"]) * 1e6
+    acc = {}
+    for r in _csv(a.clock, "counter_collection.csv"):
+        if r["Counter_Name"] != "GRBM_GUI_ACTIVE" or a.kernel not in r["Kernel_Name"]:
+            continue
+        d = acc.setdefault(int(r["Dispatch_Id"]), {"ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"]),
+                                                   "cyc": 0.0, "name": r["Kernel_Name"]})
+        d["cyc"] += float(r["Counter_Value"])
+    launches = [acc[k] for k in sorted(acc)]
+    groups = [(g.split(":")[0], int(g.split(":")[1])) for g in a.groups.split(",")]
+    if sum(n for _, n in groups) != len(launches):
+        raise ValueError(f"{len(launches)} launches of *{a.kernel}* against groups of {sum(n for _, n in groups)}")
+    names = sorted({d["name"] for d in launches})
+    lines = [f"Effective clock by group of launches: {', '.join(names)}",
+             f"command: {a.command_clock}", "",
+             f"GPU: {xcc} XCDs, {clk_max / 1e9:.2f} GHz maximum engine clock; "
+             "clock = GRBM_GUI_ACTIVE / XCDs / launch time", "",
+             f"{'group':>10} {'launches':>9} {'mean us':>9} {'Mcycles/XCD':>12} {'clock GHz':>10}"]
+    i = 0
+    for g, n in groups:
+        part = launches[i:i + n]
+        i += n
+        ns = sum(d["ns"] for d in part) / n
+        cyc = sum(d["cyc"] for d in part) / n / xcc
+        lines.append(f"{g:>10} {n:9d} {ns / 1e3:9.1f} {cyc / 1e6:12.3f} {cyc / ns:10.3f}")
+    os.makedirs(a.out, exist_ok=True)
+    with open(os.path.join(a.out, f"{a.label}_clock.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--stats-only", default=None, metavar="NAME")
@@ -205,7 +250,17 @@ def main(argv=None):
                     help="rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES ... directory: "
                          "write <kernel>_<workload>_mfma.txt (needs --workload, --bench-log)")
     ap.add_argument("--command-mfma", default="")
+    ap.add_argument("--clock", default=None, metavar="DIR",
+                    help="rocprofv3 --pmc GRBM_GUI_ACTIVE directory: write <label>_clock.txt "
+                         "(needs --kernel, --groups, --label)")
+    ap.add_argument("--kernel", default="conv_igemm")
+    ap.add_argument("--groups", default=None, help="name:launches,... in dispatch order")
+    ap.add_argument("--command-clock", default="")
     a = ap.parse_args(argv)
+    if a.clock:
+        if not (a.groups and a.label):
+            ap.error("--clock needs --groups and --label")
+        return clock_summary(a)
     if a.stats_only:
         return stats_only(a)
     if a.mfma:

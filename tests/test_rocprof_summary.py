@@ -84,3 +84,30 @@ def test_mfma_utilisation(tmp_path):
     assert "MFMA busy 90.0% of the clocked SIMD cycles at 2.000 GHz" in text
     assert "= 75.0% of the MFMA cycles at 2.40 GHz" in text          # 0.9 * 2.0 / 2.4
     assert "4000 GB/s = 50.0% of the 8.0 TB/s" in text                # 4 GB in 1 ms
+
+
+def test_clock_by_group(tmp_path):
+    d = tmp_path / "clock"
+    os.makedirs(d)
+    with open(d / "run_agent_info.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, ["Agent_Type", "Simd_Count", "Num_Xcc", "Max_Engine_Clk_Fcompute"])
+        w.writeheader()
+        w.writerow({"Agent_Type": "GPU", "Simd_Count": 1024, "Num_Xcc": 8, "Max_Engine_Clk_Fcompute": 2400})
+    # two launches of 2e6 cycles per XCD at 2.0 GHz (1000 us), then two at
+    # 2.4 GHz; another kernel in between does not count
+    rows = [(1, KERNEL, "GRBM_GUI_ACTIVE", 8 * 2.0e6, 0, 1_000_000),
+            (2, KERNEL, "GRBM_GUI_ACTIVE", 8 * 2.0e6, 0, 1_000_000),
+            (3, "other", "GRBM_GUI_ACTIVE", 5.0, 0, 10),
+            (4, KERNEL, "GRBM_GUI_ACTIVE", 8 * 2.0e6, 0, 833_333),
+            (5, KERNEL, "GRBM_GUI_ACTIVE", 8 * 2.0e6, 0, 833_333)]
+    _counters(d, rows)
+    out = tmp_path / "out"
+    rs.main(["--clock", str(d), "--kernel", "conv_igemm", "--groups", "slow:2,fast:2", "--label", "t",
+             "--out", str(out)])
+    text = open(out / "t_clock.txt").read().splitlines()
+    slow = next(ln for ln in text if ln.strip().startswith("slow")).split()
+    fast = next(ln for ln in text if ln.strip().startswith("fast")).split()
+    assert slow[1:] == ["2", "1000.0", "2.000", "2.000"], slow
+    assert fast[1:] == ["2", "833.3", "2.000", "2.400"], fast
+    with pytest.raises(ValueError):         # the group sizes must cover every launch
+        rs.main(["--clock", str(d), "--groups", "a:3", "--label", "t", "--out", str(out)])
