@@ -108,9 +108,6 @@ static KernelFn kernel_for(int variant, int tile) {
   }
 }
 
-// The direct-to-LDS variant has no fused instantiation: its plans (tile,
-// schedule, workspace) are exactly those of the register-staged one-tap
-// loaders, whose fused kernel runs them.
 static KernelFn kernel_fused_for(int variant, int tile) {
   switch (variant) {
     case kVarHwcnVecNTap: return conv_kernel_hwcn_vecn_tap_fused(tile);
