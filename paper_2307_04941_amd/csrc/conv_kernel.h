@@ -753,6 +753,9 @@ struct BVecN {
   __device__ void init(const KArgs& a, int t, int n0, int kbeg) {
     n4 = t % NC4;
     kr0 = t / NC4;
+    // with a whole wave per tile row (NC4 a multiple of 64) a thread's rows
+    // are its wave's: k, r, s and c then live in scalar registers
+    if constexpr (NC4 % 64 == 0) kr0 = __builtin_amdgcn_readfirstlane(kr0);
     const int n = n0 + n4 * 4;
     col_ok = n < a.Ng;
     const int pix = n / a.N;

@@ -93,7 +93,7 @@ constexpr int kNumTiles = 15;
 inline constexpr TileDesc kTiles[kNumTiles] = {
     // mt,  nt, kt, wm, wn, regs, eff,  m16, forced, eff_multitap, regs_pt {vec_n, vec_n_tap, vec_n_tap_dma}
     {128, 128, 16, 2, 2, 116, 0.913, 0, 0, 1.0, {136, 121, 105}},  // 0: 2-D wave grid sharing both operands (TB(8,8)-like)
-    {64, 256, 16, 1, 4, 116, 0.865, 0, 0, 1.0, {158, 125, 104}},   // 1: four waves sharing one filter tile (TB(1,8)-like)
+    {64, 256, 16, 1, 4, 116, 0.865, 0, 0, 1.0, {126, 125, 104}},   // 1: four waves sharing one filter tile (TB(1,8)-like)
     {256, 64, 16, 4, 1, 120, 0.891, 0, 0, 1.0, {134, 125, 104}},   // 2: four waves sharing one patch tile
     {64, 128, 16, 1, 2, 120, 0.890, 0, 0, 1.0, {161, 129, 104}},   // 3
     {128, 64, 16, 2, 1, 128, 0.823, 0, 0, 1.0, {145, 129, 104}},   // 4
@@ -103,7 +103,7 @@ inline constexpr TileDesc kTiles[kNumTiles] = {
     {128, 32, 16, 2, 1, 88, 0.808, 0, 0, 1.0, {99, 90, 68}},     // 8
     {64, 32, 16, 1, 1, 92, 0.750, 0, 0, 1.0, {109, 92, 66}},      // 9
     {256, 128, 16, 4, 2, 111, 0.886, 0, 0, 1.0, {127, 119, 106}},  // 10: eight waves
-    {128, 256, 16, 2, 4, 111, 0.832, 0, 0, 1.0, {135, 119, 106}},  // 11: eight waves
+    {128, 256, 16, 2, 4, 111, 0.832, 0, 0, 1.0, {120, 119, 106}},  // 11: eight waves
     {128, 128, 32, 2, 2, 140, 0.785, 0, 0, 1.0, {169, 137, 105}},  // 12: deeper reduction step
     {16, 64, 16, 1, 1, 88, 0.50, 1, 0, 1.0, {0, 0, 0}},          // 13: 16-row tile (16x16x4 MFMAs): 16 output channels
     {64, 64, 32, 2, 2, 60, 0.78, 0, 0, 0.9, {86, 71, 55}},        // 14: four 32x32 waves, deep step
