@@ -48,6 +48,21 @@ int mg3m_probe_copy(const void *src, void *dst, size_t bytes, void *stream);
  * MG3M_ERR_ALIGN. */
 int mg3m_probe_fill(void *dst, size_t bytes, void *stream);
 
+/* Timing events: hipEvent_t handles that record timestamps without the
+ * system-scope memory fence a default HIP event performs when it is reached.
+ * That fence writes back and invalidates the GPU's caches at every event, a
+ * cost the timed work would otherwise pay between kernels; these events only
+ * time, they do not order host reads of device memory.  Create (into *event,
+ * on the current device), record on a stream (NULL = the default stream),
+ * read the milliseconds between two recorded events once both have
+ * completed (after a synchronisation), destroy.  The handles also serve
+ * mg3m_time_next_kernel.  NULL handles or outputs: MG3M_ERR_NULL; HIP
+ * failures: MG3M_ERR_HIP with the text in mg3m_last_error(). */
+int mg3m_timing_event_create(void **event);
+int mg3m_timing_event_record(void *event, void *stream);
+int mg3m_timing_event_elapsed_ms(void *start, void *stop, float *ms);
+int mg3m_timing_event_destroy(void *event);
+
 #ifdef __cplusplus
 }
 #endif

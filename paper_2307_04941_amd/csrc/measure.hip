@@ -126,4 +126,39 @@ int mg3m_probe_fill(void* dst, size_t bytes, void* stream) {
   return launched("fill probe launch");
 }
 
+int mg3m_timing_event_create(void** event) {
+  mg3m::clear_error();
+  if (event == nullptr) return mg3m::set_error(MG3M_ERR_NULL, "event must be non-NULL");
+  hipEvent_t e = nullptr;
+  const hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
+  if (r != hipSuccess) return mg3m::set_error(MG3M_ERR_HIP, std::string("hipEventCreateWithFlags: ") + hipGetErrorString(r));
+  *event = e;
+  return MG3M_OK;
+}
+
+int mg3m_timing_event_record(void* event, void* stream) {
+  mg3m::clear_error();
+  if (event == nullptr) return mg3m::set_error(MG3M_ERR_NULL, "event must be non-NULL");
+  const hipError_t r = hipEventRecord(static_cast<hipEvent_t>(event), static_cast<hipStream_t>(stream));
+  if (r != hipSuccess) return mg3m::set_error(MG3M_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(r));
+  return MG3M_OK;
+}
+
+int mg3m_timing_event_elapsed_ms(void* start, void* stop, float* ms) {
+  mg3m::clear_error();
+  if (start == nullptr || stop == nullptr || ms == nullptr)
+    return mg3m::set_error(MG3M_ERR_NULL, "start, stop and ms must be non-NULL");
+  const hipError_t r = hipEventElapsedTime(ms, static_cast<hipEvent_t>(start), static_cast<hipEvent_t>(stop));
+  if (r != hipSuccess) return mg3m::set_error(MG3M_ERR_HIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(r));
+  return MG3M_OK;
+}
+
+int mg3m_timing_event_destroy(void* event) {
+  mg3m::clear_error();
+  if (event == nullptr) return mg3m::set_error(MG3M_ERR_NULL, "event must be non-NULL");
+  const hipError_t r = hipEventDestroy(static_cast<hipEvent_t>(event));
+  if (r != hipSuccess) return mg3m::set_error(MG3M_ERR_HIP, std::string("hipEventDestroy: ") + hipGetErrorString(r));
+  return MG3M_OK;
+}
+
 }  // extern "C"

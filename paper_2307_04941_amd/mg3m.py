@@ -107,6 +107,10 @@ def load_library(path: str = LIB_PATH):
     lib.mg3m_probe_mfma_f32.argtypes = [p, i, i, p, ctypes.POINTER(ctypes.c_double)]
     lib.mg3m_probe_copy.argtypes = [p, p, sz, p]
     lib.mg3m_probe_fill.argtypes = [p, sz, p]
+    lib.mg3m_timing_event_create.argtypes = [ctypes.POINTER(p)]
+    lib.mg3m_timing_event_record.argtypes = [p, p]
+    lib.mg3m_timing_event_elapsed_ms.argtypes = [p, p, ctypes.POINTER(ctypes.c_float)]
+    lib.mg3m_timing_event_destroy.argtypes = [p]
     lib.conv2d_fwd_f32_ex.argtypes = [p, p, p] + shape + [p, sz, cp, p]
     lib.conv2d_fwd_f32_workspace_bytes.argtypes = shape + [cp, ctypes.POINTER(sz)]
     lib.conv2d_fwd_f32_plan_string.argtypes = shape + [cp, ctypes.c_char_p, sz]
@@ -408,13 +412,48 @@ def conv2d_fwd_f32_plan_info(N, C, H, W, K, R, S, stride, pad, layout, plan=None
 
 
 def mg3m_time_next_kernel(start, stop):
-    """start/stop: torch.cuda.Event objects (already recorded once, so that
-    they exist), raw hipEvent_t handles as ints, or None, None."""
+    """start/stop: TimingEvent objects, torch.cuda.Event objects (already
+    recorded once, so that they exist), raw hipEvent_t handles as ints, or
+    None, None."""
     def h(e):
         if e is None or isinstance(e, int):
             return e
+        if isinstance(e, TimingEvent):
+            return e.handle
         return e.cuda_event
     _check(load_library().mg3m_time_next_kernel(h(start), h(stop)))
+
+
+class TimingEvent:
+    """A HIP timing event without the system-scope fence of a default event
+    (mg3m_timing_event_*): it records a timestamp on a stream and nothing
+    else, so timing a sequence of kernels does not flush the caches between
+    them."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(load_library().mg3m_timing_event_create(ctypes.byref(h)))
+        self.handle = h.value
+
+    def record(self, stream=None):
+        _check(load_library().mg3m_timing_event_record(self.handle, _stream(stream)))
+
+    def elapsed_ms(self, stop: "TimingEvent") -> float:
+        """Milliseconds from this event to stop; both recorded and completed."""
+        ms = ctypes.c_float()
+        _check(load_library().mg3m_timing_event_elapsed_ms(self.handle, stop.handle, ctypes.byref(ms)))
+        return ms.value
+
+    def close(self):
+        if self.handle is not None and _lib is not None:
+            _lib.mg3m_timing_event_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def mg3m_padding_overhead(M, N, C, mt, nt):

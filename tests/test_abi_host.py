@@ -54,6 +54,10 @@ def test_measurement_calls_validate_before_launching():
     assert lib.mg3m_probe_copy(X, X + 32, 64, None) == 5
     assert lib.mg3m_probe_fill(None, 64, None) == 1
     assert lib.mg3m_probe_fill(Y, 0, None) == 10
+    assert lib.mg3m_timing_event_create(None) == 1
+    assert lib.mg3m_timing_event_record(None, None) == 1
+    assert lib.mg3m_timing_event_elapsed_ms(None, None, None) == 1
+    assert lib.mg3m_timing_event_destroy(None) == 1
 
 
 def test_status_strings():
