@@ -23,11 +23,11 @@ namespace {
 // 16-byte aligned): 16-byte stores.  The extra column keeps the transposed
 // reads off one bank.  Tiles run j-fastest over a 1-D grid.
 template <bool VL, bool VS>
-__global__ __launch_bounds__(256) void swap_outer_inner(const float* __restrict__ in, float* out, int A, int Cm,
-                                                        int B, const float* add, int relu, unsigned tiles_j) {
-  __shared__ float t[64][65];
+__device__ __forceinline__ void swap_tile(float (&t)[64][65], const float* __restrict__ in, float* out, int A,
+                                          int Cm, int B, const float* add, int relu, unsigned tiles_j,
+                                          unsigned block) {
   const unsigned J = (unsigned)Cm * (unsigned)B;
-  const unsigned tj = blockIdx.x % tiles_j, ta = blockIdx.x / tiles_j;
+  const unsigned tj = block % tiles_j, ta = block / tiles_j;
   const int a0 = (int)ta * 64;
   const unsigned j0 = tj * 64;
   const int tid = (int)threadIdx.x;
@@ -92,6 +92,32 @@ __global__ __launch_bounds__(256) void swap_outer_inner(const float* __restrict_
   }
 }
 
+template <bool VL, bool VS>
+__global__ __launch_bounds__(256) void swap_outer_inner(const float* __restrict__ in, float* out, int A, int Cm,
+                                                        int B, const float* add, int relu, unsigned tiles_j) {
+  __shared__ float t[64][65];
+  swap_tile<VL, VS>(t, in, out, A, Cm, B, add, relu, tiles_j, blockIdx.x);
+}
+
+// A batch: work-group i runs tile i - tile0 of the job whose work-groups
+// hold i (the last job with tile0 <= i).
+__global__ __launch_bounds__(256) void swap_outer_inner_batch(const mg3m::SwapJob* __restrict__ jobs, int n) {
+  __shared__ float t[64][65];
+  const unsigned blk = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (jobs[mid].tile0 <= blk) lo = mid;
+    else hi = mid - 1;
+  }
+  const mg3m::SwapJob& j = jobs[lo];
+  const unsigned local = blk - j.tile0;
+  if (j.vl && j.vs) swap_tile<true, true>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else if (j.vl) swap_tile<true, false>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else if (j.vs) swap_tile<false, true>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else swap_tile<false, false>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 template <bool VL, bool VS>
@@ -127,6 +153,18 @@ int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, v
   else if (vl) launch<true, false>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
   else if (vs) launch<false, true>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
   else launch<false, false>(blocks, tiles_j, in, out, A, Cm, B, add, relu, s);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("layout change launch: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  return MG3M_OK;
+}
+
+int launch_swap_outer_inner_batch(const SwapJob* dev_jobs, int n, unsigned tiles, void* stream, std::string* err) {
+  if (n < 1 || tiles < 1) return MG3M_OK;
+  hipLaunchKernelGGL(swap_outer_inner_batch, dim3(tiles), dim3(256), 0, static_cast<hipStream_t>(stream), dev_jobs,
+                     n);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("layout change launch: ") + hipGetErrorString(e);

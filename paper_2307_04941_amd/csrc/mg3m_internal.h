@@ -302,6 +302,21 @@ int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, v
                             const float* add = nullptr, int relu = 0);
 int launch_filter_to_rsck(const float* w, float* wt, int K, int C, int R, int S, void* stream,
                           std::string* err);
+// A batch of layout changes in one launch (an NCHW network's filter copies):
+// the caller fills in, out, A, Cm and B; prepare_swap_batch checks each
+// change against the single launch's limits and fills in the rest (its
+// 64 x 64 tiles along j = c * B + b, its first work-group, its access widths)
+// and the batch's work-groups.  The launch takes the jobs in device memory.
+struct SwapJob {
+  const float* in;
+  float* out;
+  int A, Cm, B;
+  unsigned tiles_j;   // 64-wide tiles along j
+  unsigned tile0;     // the job's first work-group
+  int vl, vs;         // 16-byte loads (J % 4 == 0, in aligned); 16-byte stores (A % 4 == 0, out aligned)
+};
+int prepare_swap_batch(SwapJob* jobs, int n, unsigned* tiles, std::string* err);
+int launch_swap_outer_inner_batch(const SwapJob* dev_jobs, int n, unsigned tiles, void* stream, std::string* err);
 
 // Shared by the C entry points and the network executor (abi.cpp): validate,
 // plan and launch one convolution (y = act(conv + add)).  own_workspace: take

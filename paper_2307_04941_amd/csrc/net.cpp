@@ -39,6 +39,11 @@ struct mg3m_net {
   float* wt = nullptr;
   size_t wt_bytes = 0;
   std::vector<long long> wt_off;
+  // ... and the layout changes that make them, one batch per forward pass
+  // (the job table in device memory)
+  mg3m::SwapJob* wt_jobs = nullptr;
+  int wt_njobs = 0;
+  unsigned wt_tiles = 0;
   // captured forward pass
   hipGraph_t graph = nullptr;
   hipGraphExec_t exec = nullptr;
@@ -211,12 +216,7 @@ int run_layers(mg3m_net& n, const float* x, float* y, hipStream_t stream) {
     // the input and every filter to HWCN ([N][C][H][W] -> [H][W][C][N], [K][C][R][S] -> [R][S][C][K])
     int rc = mg3m::launch_swap_outer_inner(x, const_cast<float*>(act_ptr(n, 0, x, y)), n.N, n.C[0],
                                            n.H[0] * n.W[0], stream, &err);
-    for (int i = 0; rc == MG3M_OK && i < L; ++i) {
-      const mg3m_layer& ly = n.layers[i];
-      if (ly.op == MG3M_OP_CONV)
-        rc = mg3m::launch_filter_to_rsck(ly.w, n.wt + n.wt_off[i] / 4, ly.K, n.C[ly.input], ly.R, ly.S, stream,
-                                         &err);
-    }
+    if (rc == MG3M_OK) rc = mg3m::launch_swap_outer_inner_batch(n.wt_jobs, n.wt_njobs, n.wt_tiles, stream, &err);
     if (rc) return mg3m::set_error(rc, err);
   }
   for (int i = 0; i < L; ++i) {
@@ -274,12 +274,45 @@ void release(mg3m_net* n) {
   if (n->arena) (void)hipFree(n->arena);
   if (n->ws) (void)hipFree(n->ws);
   if (n->wt) (void)hipFree(n->wt);
+  if (n->wt_jobs) (void)hipFree(n->wt_jobs);
   n->arena = nullptr;
   n->ws = nullptr;
   n->wt = nullptr;
+  n->wt_jobs = nullptr;
 }
 
 }  // namespace
+
+namespace mg3m {
+
+int prepare_swap_batch(SwapJob* jobs, int n, unsigned* tiles, std::string* err) {
+  long long total = 0;
+  for (int i = 0; i < n; ++i) {
+    SwapJob& j = jobs[i];
+    if (j.in == nullptr || j.out == nullptr || j.A < 1 || j.Cm < 1 || j.B < 1) {
+      *err = "internal: empty layout change in a batch";
+      return MG3M_ERR_SHAPE;
+    }
+    const long long J = (long long)j.Cm * j.B, tj = (J + 63) / 64, ta = (j.A + 63) / 64;
+    if (J > 0x7fffffffLL) {
+      *err = "layout change: a dimension exceeds the launch grid";
+      return MG3M_ERR_TOO_LARGE;
+    }
+    j.tiles_j = (unsigned)tj;
+    j.tile0 = (unsigned)total;
+    j.vl = J % 4 == 0 && (reinterpret_cast<uintptr_t>(j.in) & 15) == 0;
+    j.vs = j.A % 4 == 0 && (reinterpret_cast<uintptr_t>(j.out) & 15) == 0;
+    total += tj * ta;
+    if (total > (1LL << 24) - 1) {
+      *err = "layout change: the batch exceeds the launch grid";
+      return MG3M_ERR_TOO_LARGE;
+    }
+  }
+  *tiles = (unsigned)total;
+  return MG3M_OK;
+}
+
+}  // namespace mg3m
 
 extern "C" {
 
@@ -312,6 +345,35 @@ int mg3m_net_create(const mg3m_layer* layers, int n_layers, int N, int C, int H,
       release(n);
       delete n;
       return mg3m::set_error(MG3M_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    if (n->wt != nullptr) {
+      // the filter copies: [K][C][R*S] -> [R*S][C][K], one job per convolution
+      std::vector<mg3m::SwapJob> jobs;
+      for (int i = 0; i < n_layers; ++i) {
+        const mg3m_layer& ly = n->layers[i];
+        if (ly.op != MG3M_OP_CONV) continue;
+        mg3m::SwapJob j{};
+        j.in = ly.w;
+        j.out = n->wt + n->wt_off[i] / 4;
+        j.A = ly.K;
+        j.Cm = n->C[ly.input];
+        j.B = ly.R * ly.S;
+        jobs.push_back(j);
+      }
+      std::string err;
+      rc = mg3m::prepare_swap_batch(jobs.data(), (int)jobs.size(), &n->wt_tiles, &err);
+      if (rc == MG3M_OK) {
+        e = hipMalloc(reinterpret_cast<void**>(&n->wt_jobs), jobs.size() * sizeof(mg3m::SwapJob));
+        if (e == hipSuccess)
+          e = hipMemcpy(n->wt_jobs, jobs.data(), jobs.size() * sizeof(mg3m::SwapJob), hipMemcpyHostToDevice);
+        if (e != hipSuccess) rc = MG3M_ERR_HIP, err = std::string("filter copy table: ") + hipGetErrorString(e);
+      }
+      if (rc) {
+        release(n);
+        delete n;
+        return mg3m::set_error(rc, err);
+      }
+      n->wt_njobs = (int)jobs.size();
     }
     *net = n;
     return MG3M_OK;

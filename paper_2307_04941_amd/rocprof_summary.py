@@ -96,6 +96,24 @@ FAMILIES = [("conv_igemm_f32<", ", false>", "convolution (fp32, plain output)"),
             ("filter_kcrs_to_rsck", "", "NCHW filter copy")]
 
 
+def timed_launch_us(directory: str, kernel: str, steps, per_step):
+    """Mean duration (us) of the kernel's last steps * per_step launches in a
+    --kernel-trace run, i.e. those of the benchmark's timed steps, which come
+    after its warm-up steps; None without a trace file or enough launches."""
+    if not steps or not per_step:
+        return None
+    try:
+        rows = _csv(directory, "kernel_trace.csv")
+    except FileNotFoundError:
+        return None
+    ds = sorted((int(r["Dispatch_Id"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+                for r in rows if r["Kernel_Name"] == kernel)
+    n = int(steps) * int(per_step)
+    if len(ds) < n:
+        return None
+    return sum(d for _, d in ds[-n:]) / n / 1e3, n
+
+
 def kernel_tag(kernel: str) -> str:
     """Short file-name tag of a kernel: its function name (persistent and
     16-row kernels keep their suffix) and its integer template arguments."""
@@ -296,6 +314,10 @@ def main(argv=None):
     if dom is not None:
         lines.append(f"  rocprofv3 average per launch:          {float(dom['AverageNs']) / 1e3:.2f} us "
                      f"over {dom['Calls']} calls (warm-up included)")
+    timed = timed_launch_us(a.trace, kernel, bench.get("steps"), roof.get("launches_per_step"))
+    if timed is not None:
+        lines.append(f"  rocprofv3 average over the timed steps: {timed[0]:.2f} us over the last {timed[1]} calls "
+                     f"({bench['steps']} steps x {roof['launches_per_step']} launches; the warm-up's are left out)")
     lines += [f"  achieved {roof['achieved']} TFLOP/s of {roof['peak']} ({100 * roof['frac']:.1f}%)",
               f"bench.py value: {bench['value']} {bench['unit']} ({bench.get('pct_peak')}% of peak), "
               f"{bench['ms_per_step']} ms per step, kernel digest {bench['kernel_digest']}"]

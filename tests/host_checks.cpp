@@ -115,6 +115,12 @@ int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, v
   return MG3M_OK;
 }
 
+int launch_swap_outer_inner_batch(const SwapJob* jobs, int n, unsigned tiles, void*, std::string*) {
+  ++g_seen.swaps;
+  CHECK(n == 0 || (jobs != nullptr && tiles >= 1), "layout change batch");
+  return MG3M_OK;
+}
+
 }  // namespace mg3m
 
 // ------------------------------------------------------------ helpers
@@ -246,6 +252,28 @@ static void check_errors() {
   CHECK(mg3m_net_create(L, 2, 2, 4, 8, 8, 0, 0, &net) != MG3M_OK && net == nullptr, "net add shape");
   CHECK(mg3m_net_create(nullptr, 2, 2, 4, 8, 8, 0, 0, &net) != MG3M_OK, "net null layers");
   CHECK(mg3m_net_destroy(nullptr) == MG3M_OK, "destroy null");
+  // a batch of layout changes: each job's tiles follow the previous job's,
+  // and the access widths follow the sizes and the alignments
+  {
+    mg3m::SwapJob jobs[3] = {};
+    jobs[0].in = fake(0); jobs[0].out = fake(1); jobs[0].A = 64; jobs[0].Cm = 64; jobs[0].B = 9;    // 1 x 9 tiles
+    jobs[1].in = fake(2) + 1; jobs[1].out = fake(3); jobs[1].A = 130; jobs[1].Cm = 3; jobs[1].B = 1;  // 3 x 1
+    jobs[2].in = fake(4); jobs[2].out = fake(5) + 2; jobs[2].A = 8; jobs[2].Cm = 100; jobs[2].B = 49;  // 1 x 77
+    unsigned tiles = 0;
+    std::string err;
+    CHECK(mg3m::prepare_swap_batch(jobs, 3, &tiles, &err) == MG3M_OK, "swap batch: %s", err.c_str());
+    CHECK(tiles == 9 + 3 + 77, "swap batch tiles %u", tiles);
+    CHECK(jobs[0].tile0 == 0 && jobs[1].tile0 == 9 && jobs[2].tile0 == 12, "swap batch tile0");
+    CHECK(jobs[0].tiles_j == 9 && jobs[1].tiles_j == 1 && jobs[2].tiles_j == 77, "swap batch tiles_j");
+    CHECK(jobs[0].vl && jobs[0].vs, "swap batch widths 0");
+    CHECK(!jobs[1].vl && !jobs[1].vs, "swap batch widths 1");        // J = 3; A = 130
+    CHECK(jobs[2].vl && !jobs[2].vs, "swap batch widths 2");        // out not 16-byte aligned
+    jobs[1].A = 0;
+    CHECK(mg3m::prepare_swap_batch(jobs, 3, &tiles, &err) == MG3M_ERR_SHAPE, "swap batch empty job");
+    jobs[1].A = 130;
+    jobs[2].Cm = 1 << 20; jobs[2].B = 1 << 12;                      // J = 2^32
+    CHECK(mg3m::prepare_swap_batch(jobs, 3, &tiles, &err) == MG3M_ERR_TOO_LARGE, "swap batch J");
+  }
   double fo = 0, dov = 0;
   CHECK(mg3m_padding_overhead(30, 44, 16, 4, 16, &fo, &dov) == MG3M_OK, "padding overhead");
   std::printf("errors: validation paths checked\n");

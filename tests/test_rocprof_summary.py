@@ -111,3 +111,20 @@ def test_clock_by_group(tmp_path):
     assert fast[1:] == ["2", "833.3", "2.000", "2.400"], fast
     with pytest.raises(ValueError):         # the group sizes must cover every launch
         rs.main(["--clock", str(d), "--groups", "a:3", "--label", "t", "--out", str(out)])
+
+
+def test_timed_launch_average_leaves_out_the_warm_up(tmp_path):
+    d = tmp_path / "trace"
+    os.makedirs(d)
+    with open(d / "run_kernel_trace.csv", "w", newline="") as f:
+        w = csv.DictWriter(f, ["Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        # two warm-up launches of 5 us, then 2 steps x 2 launches of 1, 2, 3, 4 us; another kernel between
+        for i, us in enumerate([5, 5, 1, 2, 3, 4]):
+            w.writerow({"Dispatch_Id": 2 * i + 1, "Kernel_Name": KERNEL, "Start_Timestamp": 0,
+                        "End_Timestamp": us * 1000})
+            w.writerow({"Dispatch_Id": 2 * i + 2, "Kernel_Name": "other", "Start_Timestamp": 0,
+                        "End_Timestamp": 99_000})
+    assert rs.timed_launch_us(str(d), KERNEL, 2, 2) == (2.5, 4)
+    assert rs.timed_launch_us(str(d), KERNEL, 4, 2) is None          # fewer launches than the steps need
+    assert rs.timed_launch_us(str(tmp_path / "none"), KERNEL, 2, 2) is None
