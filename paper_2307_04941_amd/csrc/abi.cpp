@@ -364,8 +364,13 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   std::string err;
   if (wt != nullptr) rc = mg3m::launch_filter_to_rsck(w, wt, s.K, s.C, s.R, s.S, stream, &err);
   if (via) {
-    rc = mg3m::launch_swap_outer_inner(x, xh, s.N, s.C, s.H * s.W, stream, &err);   // [N][C][H][W] -> [H][W][C][N]
-    if (rc == MG3M_OK) rc = mg3m::launch_filter_to_rsck(w, wh, s.K, s.C, s.R, s.S, stream, &err);
+    // one launch: [N][C][H][W] -> [H][W][C][N] and [K][C][R][S] -> [R][S][C][K]
+    mg3m::SwapJob jobs[2] = {};
+    jobs[0].in = x; jobs[0].out = xh; jobs[0].A = s.N; jobs[0].Cm = s.C; jobs[0].B = s.H * s.W;
+    jobs[1].in = w; jobs[1].out = wh; jobs[1].A = s.K; jobs[1].Cm = s.C; jobs[1].B = s.R * s.S;
+    unsigned tiles = 0;
+    rc = mg3m::prepare_swap_batch(jobs, 2, &tiles, &err);
+    if (rc == MG3M_OK) rc = mg3m::launch_swap_outer_inner_pair(jobs, tiles, stream, &err);
   }
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
   g_ev_start = g_ev_stop = nullptr;

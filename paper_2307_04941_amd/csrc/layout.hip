@@ -118,6 +118,21 @@ __global__ __launch_bounds__(256) void swap_outer_inner_batch(const mg3m::SwapJo
   else swap_tile<false, false>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
 }
 
+// Two jobs passed by value (an NCHW call run as HWCN: its x and its filter).
+struct SwapPair {
+  mg3m::SwapJob j[2];
+};
+__global__ __launch_bounds__(256) void swap_outer_inner_pair(SwapPair p) {
+  __shared__ float t[64][65];
+  const int k = blockIdx.x >= p.j[1].tile0 ? 1 : 0;
+  const mg3m::SwapJob& j = p.j[k];
+  const unsigned local = blockIdx.x - j.tile0;
+  if (j.vl && j.vs) swap_tile<true, true>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else if (j.vl) swap_tile<true, false>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else if (j.vs) swap_tile<false, true>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+  else swap_tile<false, false>(t, j.in, j.out, j.A, j.Cm, j.B, nullptr, 0, j.tiles_j, local);
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 template <bool VL, bool VS>
@@ -165,6 +180,19 @@ int launch_swap_outer_inner_batch(const SwapJob* dev_jobs, int n, unsigned tiles
   if (n < 1 || tiles < 1) return MG3M_OK;
   hipLaunchKernelGGL(swap_outer_inner_batch, dim3(tiles), dim3(256), 0, static_cast<hipStream_t>(stream), dev_jobs,
                      n);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    *err = std::string("layout change launch: ") + hipGetErrorString(e);
+    return MG3M_ERR_HIP;
+  }
+  return MG3M_OK;
+}
+
+int launch_swap_outer_inner_pair(const SwapJob jobs[2], unsigned tiles, void* stream, std::string* err) {
+  SwapPair p;
+  p.j[0] = jobs[0];
+  p.j[1] = jobs[1];
+  hipLaunchKernelGGL(swap_outer_inner_pair, dim3(tiles), dim3(256), 0, static_cast<hipStream_t>(stream), p);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     *err = std::string("layout change launch: ") + hipGetErrorString(e);

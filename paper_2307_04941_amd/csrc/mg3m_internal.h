@@ -317,6 +317,8 @@ struct SwapJob {
 };
 int prepare_swap_batch(SwapJob* jobs, int n, unsigned* tiles, std::string* err);
 int launch_swap_outer_inner_batch(const SwapJob* dev_jobs, int n, unsigned tiles, void* stream, std::string* err);
+// Two prepared jobs passed by value: no table in device memory.
+int launch_swap_outer_inner_pair(const SwapJob jobs[2], unsigned tiles, void* stream, std::string* err);
 
 // Shared by the C entry points and the network executor (abi.cpp): validate,
 // plan and launch one convolution (y = act(conv + add)).  own_workspace: take

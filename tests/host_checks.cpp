@@ -115,6 +115,12 @@ int launch_swap_outer_inner(const float* in, float* out, int A, int Cm, int B, v
   return MG3M_OK;
 }
 
+int launch_swap_outer_inner_pair(const SwapJob jobs[2], unsigned tiles, void*, std::string*) {
+  ++g_seen.swaps;
+  CHECK(jobs[1].tile0 >= 1 && tiles > jobs[1].tile0, "layout change pair");
+  return MG3M_OK;
+}
+
 int launch_swap_outer_inner_batch(const SwapJob* jobs, int n, unsigned tiles, void*, std::string*) {
   ++g_seen.swaps;
   CHECK(n == 0 || (jobs != nullptr && tiles >= 1), "layout change batch");
