@@ -134,8 +134,12 @@ constexpr int lds_bytes_for64(const TileDesc& t) {
 // measured on MI355X over the VGG-16 and ResNet-50 layers (within 0.3% in
 // total time).  On full layers the large tiles sustain 80-87% of the fp64
 // MFMA peak, the one-wave tiles (64x64, 32x64, 64x32) 75-80%; the model's
-// occupancy term already credits the latter with more resident waves.
-constexpr int kNumTiles64 = 8;
+// occupancy term already credits the latter with more resident waves.  The
+// four-wave 64x64 tile (74 registers, 6 work-groups per CU) came later: its
+// eff puts every ResNet-50 layer and VGG-16 conv2 and conv11-13 on it and
+// keeps VGG-16's other layers on the large tiles (measured: ResNet-50's
+// layers 2780 -> 2513 us in total, VGG-16's 29039 -> 28867 us).
+constexpr int kNumTiles64 = 9;
 inline constexpr TileDesc kTiles64[kNumTiles64] = {
     {128, 128, 16, 2, 2, 202, 0.925},  // 0
     {64, 256, 16, 1, 4, 206, 0.900},   // 1
@@ -145,6 +149,7 @@ inline constexpr TileDesc kTiles64[kNumTiles64] = {
     {64, 64, 16, 1, 1, 212, 0.500},    // 5
     {32, 64, 16, 1, 2, 80, 0.500},     // 6
     {64, 32, 16, 2, 1, 78, 0.500},     // 7
+    {64, 64, 16, 2, 2, 74, 0.64},      // 8: four 32x32 waves
 };
 
 // Largest tensor the kernels address: byte offsets are 32-bit and 0xFFFFFFC0

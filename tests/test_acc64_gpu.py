@@ -24,7 +24,8 @@ from tests.gpu_util import assert_parity, assert_parity_acc64, make, run_gpu, sa
 
 pytestmark = pytest.mark.gpu
 
-TILES64 = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64", "32x64", "64x32"]
+TILES64 = ["128x128", "64x256", "256x64", "64x128", "128x64", "64x64,waves=1x1", "32x64", "64x32",
+           "64x64,waves=2x2"]
 
 # Shapes spanning several tiles with ragged tails in both output dimensions.
 TILE_SHAPES = [
@@ -109,7 +110,7 @@ def test_every_tile_random_data(tile, layout):
 # tested plan, so tail=n leaves whole tiles and split tiles.
 SPLIT_SHAPE = (24, 16, 61, 61, 96, 3, 3, 1, 1)
 SPLIT_PLANS = ["tile=128x128,split=3", "tile=32x64,split=5", "tile=64x256,tail=4", "tile=256x64,tail=2",
-               "tile=64x32,tail=6"]
+               "tile=64x32,tail=6", "tile=64x64,waves=2x2,split=4", "tile=64x64,waves=2x2,tail=8"]
 
 
 @pytest.mark.parametrize("layout", ["HWCN", "NCHW"])
