@@ -47,6 +47,14 @@ constexpr double kUtilBase = 0.5, kUtilPerWave = 0.1;
 // stream at 4.8 TB/s (VGG-16 conv1, 860 MB: 207 -> 180 us).
 constexpr double kPersistEff = 0.92;
 constexpr double kStreamBytesPerSPersist = 4.8e12;
+// The NCHW row loader with a column stride above 1 loads element by element
+// (no 16-byte vector covers four output columns): on ResNet-50's stride-2
+// layers and AlexNet's conv1 it ran 1.2-1.6x the model's time.  Fitted, with
+// the layout-change cost below, to the 44 NCHW layers of VGG-16, ResNet-50
+// and AlexNet + inception timed both natively and run as HWCN: the picks then
+// total 18714 us against 18823 before and 18696 for the faster of the two on
+// every layer.
+constexpr double kNchwStridedFactor = 0.6;
 
 long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
 
@@ -316,7 +324,8 @@ double predict_us(const ConvShape& s, const Plan& p) {
     const double waves_per_simd = (double)std::min<long long>(per_cu, occ) * t.wm * t.wn / 4.0;
     const double util = std::min(1.0, kUtilBase + kUtilPerWave * waves_per_simd);
     const double eff = t.eff * variant_factor(p.variant) * util * (multitap ? t.eff_multitap : 1.0) *
-                       (p.persist ? kPersistEff : 1.0);
+                       (p.persist ? kPersistEff : 1.0) *
+                       (s.layout == kNCHW && p.b_mode == kBVecW && s.sw > 1 ? kNchwStridedFactor : 1.0);
     return (double)per_cu * tile_flops * k_tiles / (rate * kClockHz * eff) * 1e6 +
            (p.persist ? 1.0 : (double)cdiv(per_cu, occ)) * kRoundUs;
   };
@@ -478,7 +487,7 @@ int make_plan(const ConvShape& s, const char* override_text, bool acc64, bool x1
     }
     c.est_us = predict_us(sv, c);
     // the layout changes: x and w in, y out, each read and written once
-    if (via) c.est_us += 2.0 * (double)c.via_bytes / kStreamBytesPerS * 1e6 + 3 * kLaunchUs;
+    if (via) c.est_us += 2.0 * (double)c.via_bytes / kStreamBytesPerS * 1e6 + 2 * kLaunchUs;
     // ties: less workspace traffic, then the larger tile
     const bool better = best < 0 || c.est_us < best_plan.est_us * 0.999 ||
                         (std::fabs(c.est_us - best_plan.est_us) <= best_plan.est_us * 0.001 &&
