@@ -669,3 +669,22 @@ def test_override_waves_key(bad):
     assert ei.value.status == 7, bad
     with pytest.raises(mg3m.Mg3mError):
         mg3m.conv2d_fwd_f32_plan_info(*shape, "HWCN", "tile=64x64,waves=3x1")
+
+
+def test_selector_runs_strided_nchw_layers_as_hwcn():
+    """NCHW layers whose row loader goes element by element (column stride
+    above 1) are priced at 0.6 of the tuned rate: ResNet-50's 7x7 stride-2
+    stem and its 3x3 stride-2 layers run as HWCN on workspace copies (each
+    timed faster that way on MI355X), while VGG-16's stride-1 stem and
+    ResNet-50's first 1x1 layers keep the NCHW kernels."""
+    rn = {L.name: L for L in workloads.workload("resnet50_n32")}
+    vgg = {L.name: L for L in workloads.workload("vgg16_n64")}
+
+    def via(L):
+        return mg3m.conv2d_fwd_f32_plan_info(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.stride, L.pad,
+                                             "NCHW")["via_hwcn"]
+    for name in ("rn50_stem", "rn50_c3_3x3_s2", "rn50_c4_3x3_s2", "rn50_c5_3x3_s2"):
+        assert via(rn[name]) == 1, name
+    for name in ("rn50_c2_1x1a_first", "rn50_c3_1x1b"):
+        assert via(rn[name]) == 0, name
+    assert via(vgg["vgg16_conv1"]) == 0
