@@ -346,8 +346,9 @@ int conv2d_fwd_f32_plan_info(int N, int C, int H, int W, int K, int R, int S,
  * events on the stream it runs on.  start and stop are hipEvent_t handles
  * created by the caller (both non-NULL), or both NULL to clear the hook.  The
  * next compute call (conv2d_fwd_f32, _ex, _hw or _acc64) made on the calling host thread
- * records start on its stream immediately before launching its main kernel
- * and stop immediately after it -- before any split-K reduction -- and then
+ * launches its main kernel with the two events attached (hipExtLaunchKernel):
+ * start takes the kernel's start time and stop its end time -- before any
+ * split-K reduction, with no separate event packets on the stream -- and then
  * clears the hook; a call rejected by validation leaves it set.  The library
  * keeps only the handles: both events must stay alive until that call has
  * returned (or the hook is cleared).  Returns MG3M_OK, or MG3M_ERR_ARG if

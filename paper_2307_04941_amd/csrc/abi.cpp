@@ -374,15 +374,7 @@ int run(const float* x, const float* w, float* y, const Geom& g, void* workspace
   }
   hipEvent_t ev0 = g_ev_start, ev1 = g_ev_stop;
   g_ev_start = g_ev_stop = nullptr;
-  if (ev0 != nullptr) {
-    hipError_t e = hipEventRecord(ev0, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) err = std::string("hipEventRecord: ") + hipGetErrorString(e), rc = MG3M_ERR_HIP;
-  }
-  if (rc == MG3M_OK) rc = mg3m::launch_conv(p, a, stream, &err);
-  if (rc == MG3M_OK && ev1 != nullptr) {
-    hipError_t e = hipEventRecord(ev1, static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) err = std::string("hipEventRecord: ") + hipGetErrorString(e), rc = MG3M_ERR_HIP;
-  }
+  if (rc == MG3M_OK) rc = mg3m::launch_conv(p, a, stream, &err, ev0, ev1);
   if (rc == MG3M_OK && p.tail_tiles > 0) {
     mg3m::RArgs r{};
     r.ws = part; r.y = yk; r.mt = p.t.mt; r.nt = p.t.nt;

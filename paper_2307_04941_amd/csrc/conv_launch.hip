@@ -1,5 +1,6 @@
 // Kernel launch: picks the instantiation for a plan's loader variant and
 // tile, and the deterministic split-K reduction.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
@@ -147,7 +148,7 @@ static bool launch_failure_injected() {
 }
 
 // One launch: dp_tiles work-groups of whole tiles, then tail_wgs of tail runs.
-int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
+int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err, void* start, void* stop) {
   if (launch_failure_injected()) {
     *err = "kernel launch: failure injected by MG3M_TEST_FAIL_LAUNCH";
     return MG3M_ERR_HIP;
@@ -179,8 +180,20 @@ int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err) {
     *err = "internal: no kernel for this loader variant and tile";
     return MG3M_ERR_PLAN;
   }
-  hipLaunchKernelGGL(fn, dim3((unsigned)p.grid), dim3(p.t.wm * p.t.wn * 64), 0, (hipStream_t)stream, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e = hipSuccess;
+  if (start != nullptr || stop != nullptr) {
+    // the events take the kernel's own start and end times from its dispatch
+    // (no separate event packets around it on the stream)
+    KArgs ka = a;
+    void* args[] = {&ka};
+    e = hipExtLaunchKernel(reinterpret_cast<const void*>(fn), dim3((unsigned)p.grid), dim3(p.t.wm * p.t.wn * 64),
+                           args, 0, static_cast<hipStream_t>(stream), static_cast<hipEvent_t>(start),
+                           static_cast<hipEvent_t>(stop), 0);
+    if (e == hipSuccess) e = hipGetLastError();
+  } else {
+    hipLaunchKernelGGL(fn, dim3((unsigned)p.grid), dim3(p.t.wm * p.t.wn * 64), 0, (hipStream_t)stream, a);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) {
     *err = std::string("kernel launch: ") + hipGetErrorString(e);
     return MG3M_ERR_HIP;

@@ -294,7 +294,10 @@ KernelFn conv_kernel64_hwcn(int variant, int tile);
 KernelFn conv_kernel64_nchw(int variant, int tile);
 
 // Kernel launchers (conv_launch.hip, pool.hip).
-int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err);
+// start / stop: hipEvent_t handles (or null) that take the main kernel's own
+// start and end times (mg3m_time_next_kernel).
+int launch_conv(const Plan& p, const KArgs& a, void* stream, std::string* err, void* start = nullptr,
+                void* stop = nullptr);
 int launch_tail_reduce(const RArgs& r, void* stream, std::string* err);
 int launch_maxpool(const PArgs& p, void* stream, std::string* err);
 // wt[R][S][C][K] = w[K][C][R][S] (conv_launch.hip).

@@ -51,7 +51,7 @@ struct Seen {
 
 namespace mg3m {
 
-int launch_conv(const Plan& p, const KArgs& a, void*, std::string* err) {
+int launch_conv(const Plan& p, const KArgs& a, void*, std::string* err, void*, void*) {
   ++g_seen.convs;
   g_seen.plan = p;
   g_seen.args = a;
