@@ -146,7 +146,7 @@ int conv2d_fwd_f32_workspace_bytes(int N, int C, int H, int W, int K, int R, int
  *   dma=0|1          the one-tap HWCN loaders (HWCN, N and K multiples of 4, C a
  *                    multiple of kt, aligned buffers) load straight into LDS (1, the
  *                    default where it applies: 32x32x2-MFMA tiles of the fp32
- *                    kernel, not persistent plans) or stage through VGPRs (0);
+ *                    kernel, persistent plans included) or stage through VGPRs (0);
  *                    dma=1 where it does not apply -> MG3M_ERR_PLAN
  *   sk=<g>           the left-over tiles' k-tiles dealt out to g work-groups in equal
  *                    runs (stream-K); g from the number of left-over tiles to their
