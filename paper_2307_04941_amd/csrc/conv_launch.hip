@@ -40,24 +40,46 @@ __global__ __launch_bounds__(256) void tail_reduce(RArgs r) {
   // runs covering the tile: split plans give tile t the runs t*sk_s ... t*sk_s + sk_s - 1
   const int w0 = r.sk_s > 0 ? t * r.sk_s : run_of_step(r, t * r.k_tiles);
   const int w1 = r.sk_s > 0 ? w0 + r.sk_s - 1 : run_of_step(r, (t + 1) * r.k_tiles - 1);
-  // the piece of run w in tail tile t sits in slot w + t
+  // the piece of run w in tail tile t sits in slot w + t.  Pieces are loaded
+  // up to four at a time, all of them in flight before the first add, so a
+  // thread waits out the memory latency once per four pieces, not once per
+  // piece; the adds stay in run order.
   const long long off = ((long long)w0 + t) * tile_elems + e;
   f32x4r sum;
   if constexpr (F64) {
     const double* p = static_cast<const double*>(r.ws) + off;
-    f64x2r lo = *reinterpret_cast<const f64x2r*>(p), hi = *reinterpret_cast<const f64x2r*>(p + 2);
-    for (int w = w0 + 1; w <= w1; ++w) {
-      p += tile_elems;
-      lo += *reinterpret_cast<const f64x2r*>(p);
-      hi += *reinterpret_cast<const f64x2r*>(p + 2);
+    auto ld = [&](long long i) { return *reinterpret_cast<const f64x2r*>(p + i); };
+    f64x2r lo = ld(0), hi = ld(2);
+    for (int w = w0 + 1; w <= w1; w += 4, p += 4 * tile_elems) {
+      const int n = min(4, w1 - w + 1);
+      f64x2r l[4], h[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (u < n) {
+          l[u] = ld((u + 1) * tile_elems);
+          h[u] = ld((u + 1) * tile_elems + 2);
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (u < n) {
+          lo += l[u];
+          hi += h[u];
+        }
     }
     sum = f32x4r{(float)lo[0], (float)lo[1], (float)hi[0], (float)hi[1]};
   } else {
     const float* p = static_cast<const float*>(r.ws) + off;
-    sum = *reinterpret_cast<const f32x4r*>(p);
-    for (int w = w0 + 1; w <= w1; ++w) {
-      p += tile_elems;
-      sum += *reinterpret_cast<const f32x4r*>(p);
+    auto ld = [&](long long i) { return *reinterpret_cast<const f32x4r*>(p + i); };
+    sum = ld(0);
+    for (int w = w0 + 1; w <= w1; w += 4, p += 4 * tile_elems) {
+      const int n = min(4, w1 - w + 1);
+      f32x4r v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (u < n) v[u] = ld((u + 1) * tile_elems);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (u < n) sum += v[u];
     }
   }
   const int tile = r.dp_tiles + t;
