@@ -31,6 +31,15 @@ writes <out>/<kernel tag>_<workload>_mfma.txt: the dominant kernel's MFMA
 utilisation per launch from a ``rocprofv3 --pmc GRBM_GUI_ACTIVE
 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES`` run, and its HBM GB/s.
 
+    python -m paper_2307_04941_amd.rocprof_summary --waves DIR --workload vgg16_n64 \
+        --bench-log FILE --out DIR --command-waves "..."
+
+writes <out>/<kernel tag>_<workload>_waves.txt: where the dominant kernel's
+waves spend their cycles (waiting at s_waitcnt or a barrier, waiting for an
+issue slot, issuing) and its LDS bank-conflict cycles, from a ``rocprofv3
+--pmc SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY
+SQ_LDS_BANK_CONFLICT`` run.
+
     python -m paper_2307_04941_amd.rocprof_summary --clock DIR --kernel SUBSTR \
         --groups uniform:13,int:13,zeros:13 --label NAME --out DIR --command-clock "..."
 
@@ -212,6 +221,46 @@ def mfma_summary(a):
     return 0
 
 
+WAVE_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY")
+
+
+def waves_summary(a):
+    """Where the dominant kernel's waves spend their cycles, from a
+    ``rocprofv3 --pmc SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY
+    SQ_ACTIVE_INST_ANY SQ_LDS_BANK_CONFLICT ...`` run: the wave-cycles
+    waiting at s_waitcnt or a barrier, waiting for an issue slot (the MFMA
+    pipe busy with another wave's MFMA, or a dependency), and issuing, each
+    over all wave-cycles, summed over the kernel's dispatches; and the LDS
+    cycles lost to bank conflicts."""
+    with open(a.bench_log) as f:
+        bench = json.loads([ln for ln in f if ln.startswith("{")][-1])
+    kernel = bench["roofline"]["kernel"]
+    tot, dispatches = {}, set()
+    for r in _csv(a.waves, "counter_collection.csv"):
+        if r["Kernel_Name"] != kernel:
+            continue
+        dispatches.add(int(r["Dispatch_Id"]))
+        tot[r["Counter_Name"]] = tot.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    missing = [c for c in WAVE_COUNTERS if c not in tot]
+    if missing or not tot["SQ_WAVE_CYCLES"]:
+        raise ValueError(f"no {', '.join(missing) or 'SQ_WAVE_CYCLES'} for {kernel} in {a.waves}")
+    wc = tot["SQ_WAVE_CYCLES"]
+    lines = [f"Wave states of {kernel}, workload {a.workload}",
+             f"command: {a.command_waves}", "",
+             f"{len(dispatches)} dispatches; fractions of all wave-cycles (SQ_WAVE_CYCLES):",
+             f"  waiting at s_waitcnt or a barrier (SQ_WAIT_ANY):        {100 * tot['SQ_WAIT_ANY'] / wc:5.1f}%",
+             f"  waiting for an issue slot (SQ_WAIT_INST_ANY):           {100 * tot['SQ_WAIT_INST_ANY'] / wc:5.1f}%",
+             f"  issuing (SQ_ACTIVE_INST_ANY):                           {100 * tot['SQ_ACTIVE_INST_ANY'] / wc:5.1f}%"]
+    if "SQ_LDS_BANK_CONFLICT" in tot:
+        lines.append(f"LDS cycles stalled by bank conflicts (SQ_LDS_BANK_CONFLICT), all dispatches: "
+                     f"{tot['SQ_LDS_BANK_CONFLICT']:.0f}")
+    os.makedirs(a.out, exist_ok=True)
+    with open(os.path.join(a.out, f"{kernel_tag(kernel)}_{a.label or a.workload}_waves.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def clock_summary(a):
     """Effective clock per group of launches (see the module docstring)."""
     agent = next(r for r in _csv(a.clock, "agent_info.csv") if int(r.get("Simd_Count") or 0) > 0)
@@ -271,6 +320,10 @@ def main(argv=None):
     ap.add_argument("--clock", default=None, metavar="DIR",
                     help="rocprofv3 --pmc GRBM_GUI_ACTIVE directory: write <label>_clock.txt "
                          "(needs --kernel, --groups, --label)")
+    ap.add_argument("--waves", default=None, metavar="DIR",
+                    help="rocprofv3 --pmc SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY ... "
+                         "directory: write <kernel>_<workload>_waves.txt (needs --workload, --bench-log)")
+    ap.add_argument("--command-waves", default="")
     ap.add_argument("--kernel", default="conv_igemm")
     ap.add_argument("--groups", default=None, help="name:launches,... in dispatch order")
     ap.add_argument("--command-clock", default="")
@@ -283,6 +336,10 @@ def main(argv=None):
         return stats_only(a)
     if a.mfma:
         return mfma_summary(a)
+    if a.waves:
+        if not (a.workload and a.bench_log):
+            ap.error("--waves needs --workload and --bench-log")
+        return waves_summary(a)
     if a.trace is None:
         ap.error("--trace is required without --mfma")
     for need in ("workload", "fetch", "write", "bench_log", "copy_mib"):

@@ -128,3 +128,31 @@ def test_timed_launch_average_leaves_out_the_warm_up(tmp_path):
     assert rs.timed_launch_us(str(d), KERNEL, 2, 2) == (2.5, 4)
     assert rs.timed_launch_us(str(d), KERNEL, 4, 2) is None          # fewer launches than the steps need
     assert rs.timed_launch_us(str(tmp_path / "none"), KERNEL, 2, 2) is None
+
+
+def test_wave_states(tmp_path):
+    d = tmp_path / "waves"
+    os.makedirs(d)
+    # two dispatches of the dominant kernel: 1000 + 3000 wave-cycles, of which
+    # 200 + 600 waiting, 700 + 2100 waiting for issue, 100 + 300 issuing; the
+    # other kernel does not count
+    rows = []
+    for disp, scale in ((1, 1.0), (3, 3.0)):
+        for name, v in (("SQ_WAVE_CYCLES", 1000), ("SQ_WAIT_ANY", 200), ("SQ_WAIT_INST_ANY", 700),
+                        ("SQ_ACTIVE_INST_ANY", 100), ("SQ_LDS_BANK_CONFLICT", 0)):
+            rows.append((disp, KERNEL, name, v * scale, 0, 1000))
+    rows.append((2, "other", "SQ_WAIT_ANY", 1e9, 0, 10))
+    _counters(d, rows)
+    _bench_log(tmp_path / "bench.log", [])
+    out = tmp_path / "out"
+    rs.main(["--waves", str(d), "--workload", "w", "--bench-log", str(tmp_path / "bench.log"), "--out", str(out)])
+    text = open(out / f"{rs.kernel_tag(KERNEL)}_w_waves.txt").read()
+    assert "2 dispatches" in text
+    lines = text.splitlines()
+    pct = [float(ln.split()[-1].rstrip("%")) for ln in lines if ln.strip().startswith(("waiting", "issuing"))]
+    assert pct == [20.0, 70.0, 10.0], pct
+    assert "bank conflicts (SQ_LDS_BANK_CONFLICT), all dispatches: 0" in text
+    with pytest.raises(ValueError):          # a counter the summary needs is missing
+        _counters(d, [r for r in rows if r[2] != "SQ_WAIT_INST_ANY"])
+        rs.main(["--waves", str(d), "--workload", "w", "--bench-log", str(tmp_path / "bench.log"),
+                 "--out", str(out)])
